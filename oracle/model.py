@@ -1,0 +1,164 @@
+"""The decoder the sensitivity profile runs on (Section 4.1), written out plainly.
+
+A Llama-style pre-norm decoder: token embedding, L blocks of
+  a = RMSNorm(h); q, k, v = a Wq^T, a Wk^T, a Wv^T; rotary(q, k);
+  o = causal softmax(q k^T / sqrt(d_h)) v per query head (grouped-query: query
+  head hq reads KV head hq // (H / H_kv)); h <- h + o Wo^T;
+  m = RMSNorm(h); h <- h + (silu(m Wg^T) * (m Wu^T)) Wd^T,
+then a final RMSNorm and an untied LM head.  Rotary embedding is rotate-half:
+coordinate pairs (j, j + d_h/2) of position t turn by t * theta**(-2j/d_h).
+
+The clean pass keeps each block's input h_l (the "prefix" a perturbed pass resumes
+from) and the final normalised hidden state.  Everything runs in one numpy dtype
+chosen by the caller; nothing is fused, blocked or reordered.
+"""
+from __future__ import annotations
+
+from typing import Callable, List, Optional
+
+import numpy as np
+
+
+class Model:
+    """Weights (as produced by ``fixtures.make_weights(bits=False)``) in a numpy dtype."""
+
+    def __init__(self, cfg, weights: dict, dtype=np.float64):
+        self.cfg = cfg
+        self.dtype = np.dtype(dtype)
+        cast = lambda a: np.asarray(a, dtype=self.dtype)
+        if cfg.dtype == "bf16" and np.asarray(weights["tok_emb"]).dtype == np.uint16:
+            raise ValueError("pass fp32 weights (fixtures.make_weights(..., bits=False))")
+        self.tok_emb = cast(weights["tok_emb"])
+        self.lm_head = cast(weights["lm_head"])
+        self.final_norm = cast(weights["final_norm"])
+        self.w_qkv = [cast(w) if w is not None else None for w in weights["w_qkv"]]
+        self.w_o = [cast(w) if w is not None else None for w in weights["w_o"]]
+        self.w_gate_up = [cast(w) if w is not None else None for w in weights["w_gate_up"]]
+        self.w_down = [cast(w) if w is not None else None for w in weights["w_down"]]
+        self.attn_norm = [cast(w) for w in weights["attn_norm"]]
+        self.mlp_norm = [cast(w) for w in weights["mlp_norm"]]
+
+
+def rmsnorm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
+    """x / sqrt(mean(x^2) + eps) * g over the last axis."""
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    return (x / np.sqrt(ms + x.dtype.type(eps))) * g
+
+
+def rope(x: np.ndarray, positions: np.ndarray, theta: float) -> np.ndarray:
+    """Rotate-half rotary embedding of x [T, n_heads, d_h] at integer positions [T].
+
+    The angle of pair j is computed in float64 (t * theta**(-2j/d_h)) and its
+    cosine and sine are cast to x's dtype.
+    """
+    T, nh, dh = x.shape
+    half = dh // 2
+    j = np.arange(half, dtype=np.float64)
+    inv_freq = theta ** (-(2.0 * j) / dh)
+    ang = np.asarray(positions, dtype=np.float64)[:, None] * inv_freq[None, :]
+    cos = np.cos(ang).astype(x.dtype)[:, None, :]
+    sin = np.sin(ang).astype(x.dtype)[:, None, :]
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * cos - x2 * sin, x2 * cos + x1 * sin], axis=-1)
+
+
+def silu(x: np.ndarray) -> np.ndarray:
+    return x / (x.dtype.type(1) + np.exp(-x))
+
+
+def softmax(x: np.ndarray, axis: int = -1) -> np.ndarray:
+    m = np.max(x, axis=axis, keepdims=True)
+    e = np.exp(x - m)
+    return e / np.sum(e, axis=axis, keepdims=True)
+
+
+def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_chunk: int = 1024) -> np.ndarray:
+    """q [T, H, d_h], k/v [T, H_kv, d_h] -> o [T, H, d_h]; position t sees u <= t."""
+    T, H, dh = q.shape
+    Hkv = k.shape[1]
+    group = H // Hkv
+    scale = q.dtype.type(1.0 / np.sqrt(dh))
+    o = np.empty_like(q)
+    for hq in range(H):
+        hk = hq // group
+        for t0 in range(0, T, q_chunk):
+            t1 = min(T, t0 + q_chunk)
+            s = (q[t0:t1, hq, :] @ k[:t1, hk, :].T) * scale          # [tq, t1]
+            mask = np.arange(t1)[None, :] > np.arange(t0, t1)[:, None]
+            s = np.where(mask, -np.inf, s)
+            o[t0:t1, hq, :] = softmax(s, axis=-1) @ v[:t1, hk, :]
+    return o
+
+
+def block(m: Model, l: int, h: np.ndarray, positions: np.ndarray,
+          v_hook: Optional[Callable[[np.ndarray], np.ndarray]] = None) -> np.ndarray:
+    """One decoder block.  ``v_hook`` (if given) replaces the layer's Value states
+    [T, H_kv, d_h] before attention; Q and K are untouched."""
+    c = m.cfg
+    H, Hkv, dh = c.n_heads, c.n_kv_heads, c.head_dim
+    T = h.shape[0]
+    a = rmsnorm(h, m.attn_norm[l], c.rms_eps)
+    qkv = a @ m.w_qkv[l].T
+    q = qkv[:, : H * dh].reshape(T, H, dh)
+    k = qkv[:, H * dh:(H + Hkv) * dh].reshape(T, Hkv, dh)
+    v = qkv[:, (H + Hkv) * dh:].reshape(T, Hkv, dh)
+    q = rope(q, positions, c.rope_theta)
+    k = rope(k, positions, c.rope_theta)
+    if v_hook is not None:
+        v = v_hook(v)
+    o = causal_attention(q, k, v).reshape(T, H * dh)
+    h = h + o @ m.w_o[l].T
+    x = rmsnorm(h, m.mlp_norm[l], c.rms_eps)
+    gu = x @ m.w_gate_up[l].T
+    f = silu(gu[:, : c.d_ff]) * gu[:, c.d_ff:]
+    return h + f @ m.w_down[l].T
+
+
+def embed(m: Model, tokens: np.ndarray) -> np.ndarray:
+    return m.tok_emb[np.asarray(tokens, dtype=np.int64)].copy()
+
+
+def final_hidden(m: Model, h: np.ndarray) -> np.ndarray:
+    return rmsnorm(h, m.final_norm, m.cfg.rms_eps)
+
+
+def logits(m: Model, xf: np.ndarray) -> np.ndarray:
+    return xf @ m.lm_head.T
+
+
+class CleanState:
+    """What ReferencePredict leaves behind: h_l (input of block l) for every l, and
+    the final normalised hidden state of the clean pass."""
+
+    def __init__(self, hs: List[np.ndarray], xfinal: np.ndarray):
+        self.hs = hs
+        self.xfinal = xfinal
+
+
+def clean_pass(m: Model, tokens: np.ndarray) -> CleanState:
+    pos = np.arange(len(tokens))
+    h = embed(m, tokens)
+    hs = []
+    for l in range(m.cfg.n_layers):
+        hs.append(h)
+        h = block(m, l, h, pos)
+    return CleanState(hs, final_hidden(m, h))
+
+
+def resume(m: Model, h_l: np.ndarray, l: int, v_hook) -> np.ndarray:
+    """Run blocks l..L-1 from the cached input h_l, with ``v_hook`` applied to block
+    l's Value states only; returns the final normalised hidden state."""
+    pos = np.arange(h_l.shape[0])
+    h = block(m, l, h_l, pos, v_hook)
+    for lp in range(l + 1, m.cfg.n_layers):
+        h = block(m, lp, h, pos)
+    return final_hidden(m, h)
+
+
+def full_forward(m: Model, tokens: np.ndarray, l: Optional[int] = None, v_hook=None) -> np.ndarray:
+    """Forward from the embedding (no prefix reuse); the hook acts at block l."""
+    pos = np.arange(len(tokens))
+    h = embed(m, tokens)
+    for lp in range(m.cfg.n_layers):
+        h = block(m, lp, h, pos, v_hook if lp == l else None)
+    return final_hidden(m, h)

@@ -1,0 +1,123 @@
+"""Sensitivity profiling, the first half of Algorithm 1 (Section 4.3).
+
+* ReferencePredict: the clean forward; its output distribution P_{i,t} at every
+  position of the evaluation window (``model.clean_pass``).
+* Value perturbation (Eq. value-perturbation): at layer l only, every eligible
+  Value vector becomes v + alpha * ||v||_2 * epsilon with epsilon ~ N(0, I) drawn
+  per (sequence, layer, KV head, position); Keys and all other layers are left
+  alone.
+* PerturbedPredict: the forward resumed from the cached input of layer l (layers
+  below l are never recomputed) with the perturbed Values; output Q_{i,l,t}.
+* WindowKL (Eq. sample-response): d_{i,l} = mean over t in W_i of
+  KL(P_{i,t} || Q_{i,l,t}), natural log.
+* Calibration mean (Eq. layer-sensitivity): s_l = (1/N) sum_i d_{i,l}.
+
+Readings where the paper is silent: W_i is [window_start, T_i) (all positions by
+default); positions [protect_head, T_i - protect_tail) are eligible for noise (all
+by default); the same epsilon serves every alpha; epsilon is independent per
+(sequence, layer) and shared by the query heads of a KV head.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+from . import model as M
+from .philox import value_noise
+
+
+@dataclasses.dataclass
+class PerturbParams:
+    alpha: float
+    seed: int = 2
+    window_start: int = 0
+    protect_head: int = 0
+    protect_tail: int = 0
+
+
+def perturb_values(v: np.ndarray, alpha: float, eps: np.ndarray, lo: int, hi: int) -> np.ndarray:
+    """Eq. value-perturbation on v [T, H_kv, d_h] for positions lo <= u < hi.
+
+    The norm ||v||_2 is taken in float64; the result is cast back to v's dtype."""
+    out = v.copy()
+    if hi <= lo:
+        return out
+    seg = v[lo:hi].astype(np.float64)
+    norm = np.sqrt(np.sum(seg * seg, axis=-1, keepdims=True))
+    out[lo:hi] = (seg + float(alpha) * norm * eps[lo:hi].astype(np.float64)).astype(v.dtype)
+    return out
+
+
+def log_softmax64(x: np.ndarray) -> np.ndarray:
+    x = np.asarray(x, dtype=np.float64)
+    mx = np.max(x, axis=-1, keepdims=True)
+    return x - (mx + np.log(np.sum(np.exp(x - mx), axis=-1, keepdims=True)))
+
+
+def kl_rows(logits_p: np.ndarray, logits_q: np.ndarray) -> np.ndarray:
+    """KL(P || Q) per row with P = softmax(logits_p), Q = softmax(logits_q); float64."""
+    lp = log_softmax64(logits_p)
+    lq = log_softmax64(logits_q)
+    return np.sum(np.exp(lp) * (lp - lq), axis=-1)
+
+
+def kl_per_position(m: M.Model, x_clean: np.ndarray, x_pert: np.ndarray, chunk: int = 512) -> np.ndarray:
+    """KL_t for every position from the two final normalised hidden states; logits
+    are formed in token chunks to bound memory."""
+    T = x_clean.shape[0]
+    out = np.empty(T, dtype=np.float64)
+    for t0 in range(0, T, chunk):
+        t1 = min(T, t0 + chunk)
+        out[t0:t1] = kl_rows(M.logits(m, x_clean[t0:t1]), M.logits(m, x_pert[t0:t1]))
+    return out
+
+
+def _hook(m: M.Model, seq: int, layer: int, T: int, p: PerturbParams):
+    c = m.cfg
+    lo, hi = p.protect_head, T - p.protect_tail
+    eps = value_noise(p.seed, seq, layer, c.n_kv_heads, np.arange(T), c.head_dim)
+    return lambda v: perturb_values(v, p.alpha, eps, lo, hi)
+
+
+def perturbed_final(m: M.Model, st: M.CleanState, tokens: np.ndarray, seq: int, layer: int,
+                    p: PerturbParams, full_recompute: bool = False) -> np.ndarray:
+    """PerturbedPredict: final normalised hidden state with layer ``layer``'s Values
+    perturbed; resumed from the cached h_l unless ``full_recompute``."""
+    hook = _hook(m, seq, layer, len(tokens), p)
+    if full_recompute:
+        return M.full_forward(m, tokens, layer, hook)
+    return M.resume(m, st.hs[layer], layer, hook)
+
+
+def profile_layer(m: M.Model, st: M.CleanState, tokens: np.ndarray, seq: int, layer: int,
+                  p: PerturbParams, full_recompute: bool = False):
+    """(d_{i,l}, KL_t for every position) for one sequence and one layer."""
+    xp = perturbed_final(m, st, tokens, seq, layer, p, full_recompute)
+    kl = kl_per_position(m, st.xfinal, xp)
+    w0 = min(max(p.window_start, 0), len(tokens))
+    d = float(np.mean(kl[w0:])) if w0 < len(tokens) else 0.0
+    return d, kl
+
+
+def sensitivity_profile(m: M.Model, token_seqs: Sequence[np.ndarray], layers: Sequence[int],
+                        alphas: Sequence[float], seed: int = 2, window_start: int = 0,
+                        protect_head: int = 0, protect_tail: int = 0,
+                        seq_indices: Optional[Sequence[int]] = None) -> Dict[str, np.ndarray]:
+    """Algorithm 1, profiling half.  Returns s [n_alpha, |A|] and d [n_alpha, N, |A|].
+
+    ``seq_indices`` gives each sequence's index i in the calibration set (it keys
+    the noise); by default 0..N-1."""
+    N = len(token_seqs)
+    if seq_indices is None:
+        seq_indices = list(range(N))
+    d = np.zeros((len(alphas), N, len(layers)), dtype=np.float64)
+    for n, toks in enumerate(token_seqs):
+        st = M.clean_pass(m, toks)
+        for a, alpha in enumerate(alphas):
+            p = PerturbParams(alpha, seed, window_start, protect_head, protect_tail)
+            for j, l in enumerate(layers):
+                d[a, n, j], _ = profile_layer(m, st, toks, seq_indices[n], l, p)
+    s = d.sum(axis=1) / N
+    return {"s": s, "d": d}
