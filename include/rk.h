@@ -1,0 +1,230 @@
+/*
+ * rk.h -- C ABI of the RippleKV sensitivity-profile library for MI355X (gfx950).
+ *
+ * The library computes the perturbation-propagation sensitivity profile of a
+ * decoder-only Transformer and maps it to per-layer KV-cache budgets
+ * (RippleKV, Algorithm 1; Sections 4.1-4.4):
+ *
+ *   for every calibration sequence x_i and every compressible layer l:
+ *     perturb layer l's Value cache only, v~ = v + alpha * ||v||_2 * eps
+ *       (Eq. value-perturbation; eps ~ N(0, I) per sequence, layer, KV head and
+ *       position; Keys and all other layers untouched),
+ *     resume the forward from the clean input of layer l (layers below l are
+ *       never recomputed) through the LM head,
+ *     d_{i,l} = mean over the window of KL(P_clean || Q_perturbed)
+ *       (Eq. sample-response);
+ *   s_l = (1/N) sum_i d_{i,l}                                (Eq. layer-sensitivity)
+ *   b   = round(B/|A| * ClipNormalize(r ** minmax(s), gamma)) (Eqs. 9-12)
+ *
+ * The model is the Llama-style decoder of Section 4.1: token embedding, L
+ * pre-norm blocks (RMSNorm, fused q|k|v projection, rotate-half rotary embedding
+ * on Q and K, grouped-query causal attention, output projection, RMSNorm, SwiGLU
+ * feed-forward), a final RMSNorm and an untied LM head.
+ *
+ * Conventions for every entry point:
+ *  - Ownership: the library never allocates, frees or retains caller memory.
+ *    All device buffers (weights, tokens, outputs, clean state, workspace) are
+ *    allocated by the caller; rk_model keeps pointers only.
+ *  - Streams: GPU entry points enqueue work on `stream` (a hipStream_t passed as
+ *    void*, NULL = the null stream) and return without synchronising.  Outputs
+ *    are valid once the stream reaches that point.
+ *  - Errors: every argument is validated before the first launch; on error the
+ *    function returns a negative rk_status, writes no output and records a
+ *    message for rk_last_error().  A HIP launch failure returns RK_ERR_HIP.
+ *  - Determinism: for the same inputs, seed and shapes the results are bitwise
+ *    repeatable (fixed-order reductions, no floating-point atomics).  With
+ *    alpha = 0 every KL is exactly 0.
+ *  - Layouts: row-major; weight matrices in [out_features, in_features] layout;
+ *    bf16 buffers hold raw bf16 bit patterns (uint16).
+ *  - Thread safety: calls that share a workspace or clean-state buffer must be
+ *    ordered by the caller (same stream or explicit synchronisation).
+ */
+#ifndef RK_H
+#define RK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RK_OK = 0,
+  RK_ERR_ARG = -1,          /* null pointer, out-of-range scalar, bad layer index     */
+  RK_ERR_SHAPE = -2,        /* inconsistent sizes (offsets, rows, batch too large)   */
+  RK_ERR_WORKSPACE = -3,    /* workspace or clean-state buffer smaller than required */
+  RK_ERR_HIP = -4,          /* a HIP call or kernel launch failed                    */
+  RK_ERR_UNSUPPORTED = -5   /* model shape outside what the kernels implement        */
+} rk_status;
+
+typedef enum { RK_F32 = 0, RK_BF16 = 1 } rk_dtype;
+
+typedef enum {
+  RK_ROUND_LARGEST_REMAINDER = 0,  /* keeps sum(b) = B exactly (default reading)  */
+  RK_ROUND_NEAREST_EVEN = 1        /* literal per-layer round() of Eq. layer-budget */
+} rk_rounding;
+
+/* Flags of rk_perturb_params.flags */
+#define RK_FLAG_FULL_RECOMPUTE 0x1u  /* recompute layers below l instead of resuming
+                                        (verification of prefix reuse)              */
+#define RK_FLAG_UNFUSED_KL     0x2u  /* materialise fp32 logits and run the separate
+                                        log-softmax + KL kernel instead of the fused
+                                        LM-head + KL kernel                          */
+
+/* Most sequences one batch (one call's rows) may hold. */
+#define RK_MAX_BATCH_SEQS 64
+
+/* Model shape (Section 4.1).  dtype selects the storage of weights and GEMM
+ * operands: RK_BF16 = bf16 operands, fp32 accumulation, fp32 residual stream;
+ * RK_F32 = fp32 throughout.
+ * Supported: head_dim in {64, 128} for RK_BF16 and {32, 64, 128} for RK_F32; n_heads a multiple of n_kv_heads; d_model, n_heads*head_dim, the q|k|v
+ * width and vocab multiples of 128; d_ff a multiple of 64.                      */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff, vocab;
+  float rope_theta;   /* rotary base theta                  */
+  float rms_eps;      /* RMSNorm epsilon                    */
+  rk_dtype dtype;
+} rk_model_config;
+
+/* Device pointers to the weights (caller-owned).  Matrices are in the config's
+ * dtype; the norm gains are always fp32.  The per-layer members are HOST arrays
+ * of n_layers device pointers (copied by rk_model_create).                     */
+typedef struct {
+  const void *tok_emb;                 /* [vocab, d_model]                               */
+  const void *const *w_qkv;            /* [L] -> [(H + 2*Hkv)*head_dim, d_model]: q rows,
+                                          then k rows, then v rows                       */
+  const void *const *w_o;              /* [L] -> [d_model, H*head_dim]                   */
+  const void *const *w_gate_up;        /* [L] -> [2*d_ff, d_model]: gate rows, then up   */
+  const void *const *w_down;           /* [L] -> [d_model, d_ff]                         */
+  const float *const *attn_norm;       /* [L] -> [d_model] fp32                          */
+  const float *const *mlp_norm;        /* [L] -> [d_model] fp32                          */
+  const float *final_norm;             /* [d_model] fp32                                 */
+  const void *lm_head;                 /* [vocab, d_model] (untied)                      */
+} rk_model_weights;
+
+typedef struct rk_model rk_model;      /* opaque, host-side */
+
+/* A batch of calibration sequences processed together (their rows concatenated).
+ * tokens: DEVICE int32 [offsets[n_seqs]]; offsets: HOST int64 [n_seqs + 1],
+ * offsets[0] = 0, non-decreasing; seq_index0: index in the calibration set of the
+ * batch's first sequence (sequence k of the batch has index seq_index0 + k, which
+ * keys its noise).  1 <= n_seqs <= RK_MAX_BATCH_SEQS.                          */
+typedef struct {
+  const int32_t *tokens;
+  const int64_t *offsets;
+  int32_t n_seqs;
+  int32_t seq_index0;
+} rk_batch;
+
+/* Perturbation and window parameters (Section 4.3).  Positions u of sequence i
+ * with protect_head <= u < T_i - protect_tail are perturbed (the paper excludes
+ * positions the base compressor protects); the evaluation window is
+ * W_i = [window_start, T_i).  seed keys the Philox4x32-10 noise; the same noise
+ * serves every alpha.                                                          */
+typedef struct {
+  uint64_t seed;
+  int32_t window_start;
+  int32_t protect_head;
+  int32_t protect_tail;
+  uint32_t flags;              /* RK_FLAG_* */
+} rk_perturb_params;
+
+/* ---------------------------------------------------------------- model handle */
+
+/* Validates the config and the weight pointers and returns a handle that stores
+ * them (no device work, no device memory).  RK_ERR_UNSUPPORTED for shapes outside
+ * the kernels' envelope (see rk_model_config).                                 */
+rk_status rk_model_create(const rk_model_config *cfg, const rk_model_weights *w, rk_model **out);
+void rk_model_destroy(rk_model *m);
+
+/* ---------------------------------------------------------------- sizes */
+
+/* Bytes of the clean state of a batch of n_rows rows (Algorithm 1,
+ * ReferencePredict): the fp32 input h_l of every block l ([L, n_rows, d_model])
+ * and the final normalised hidden state ([n_rows, d_model] in the model dtype).  */
+size_t rk_clean_state_size(const rk_model *m, int64_t n_rows);
+
+/* Flag of rk_workspace_size: the workspace also holds one clean state
+ * (rk_sensitivity_profile keeps its clean state there).                        */
+#define RK_WS_CLEAN_STATE 0x100u
+
+/* Workspace bytes for batches of at most max_rows rows, scoring at most
+ * max_group perturbed passes per LM-head launch (1 <= max_group <= 16; a larger
+ * group amortises the clean logits over more passes).  flags: RK_WS_CLEAN_STATE
+ * and/or RK_FLAG_UNFUSED_KL (room for materialised fp32 logits; implied for
+ * RK_F32 models).  Returns 0 for invalid arguments.                            */
+size_t rk_workspace_size(const rk_model *m, int64_t max_rows, int32_t max_group, uint32_t flags);
+
+/* ---------------------------------------------------------------- profiling */
+
+/* ReferencePredict (Algorithm 1) for one batch: the clean forward, leaving the
+ * per-layer inputs h_l and the final normalised hidden state in clean_state.    */
+rk_status rk_reference_forward(const rk_model *m, const rk_batch *batch, void *clean_state,
+                               size_t clean_bytes, void *workspace, size_t ws_bytes, void *stream);
+
+/* PerturbedPredict + WindowKL (Algorithm 1; Eqs. value-perturbation and
+ * sample-response) for one batch, one layer and one alpha, resumed from a clean
+ * state produced by rk_reference_forward for the same model and batch.
+ *   d_out:      DEVICE fp32 [n_seqs]: d_{i,l} of each sequence of the batch.
+ *   kl_pos:     DEVICE fp32 [rows] or NULL: KL(P_t || Q_t) at every position.
+ *   logits_out: DEVICE fp32 [rows, vocab] or NULL: the perturbed logits
+ *               (selects the unfused LM-head path; for verification).
+ * workspace must be at least rk_workspace_size(m, rows, 1, f) with f =
+ * RK_FLAG_UNFUSED_KL when logits_out is given, the flag is set or the model is
+ * fp32, else 0.                                                                 */
+rk_status rk_profile_layer(const rk_model *m, const rk_batch *batch, int32_t layer, float alpha,
+                           const rk_perturb_params *p, const void *clean_state, size_t clean_bytes,
+                           float *d_out, float *kl_pos, float *logits_out,
+                           void *workspace, size_t ws_bytes, void *stream);
+
+/* Algorithm 1, profiling half, for a whole calibration set:
+ *   s_out[a * n_A + j] = (1/N) sum_i d_{i, layers[j]} at alpha = alphas[a]
+ *   (Eq. layer-sensitivity; an unweighted mean of per-sequence window means).
+ * calib: all N sequences (offsets[N] rows); they are processed in batches of
+ *   consecutive sequences holding at most max_rows rows each (a single sequence
+ *   longer than max_rows is RK_ERR_SHAPE).
+ * layers: HOST int32 [n_A], distinct, in [0, n_layers).  alphas: HOST [n_alpha],
+ *   finite and >= 0.  s_out: DEVICE fp32 [n_alpha, n_A].  d_out: DEVICE fp32
+ *   [n_alpha, N, n_A] or NULL.  One clean pass per batch serves every alpha.
+ * max_group: passes scored per LM-head launch (1..16).
+ * workspace must be at least rk_workspace_size(m, max_rows, max_group,
+ * RK_WS_CLEAN_STATE | (p->flags & RK_FLAG_UNFUSED_KL)).                         */
+rk_status rk_sensitivity_profile(const rk_model *m, const rk_batch *calib, const int32_t *layers,
+                                 int32_t n_A, const float *alphas, int32_t n_alpha,
+                                 const rk_perturb_params *p, int64_t max_rows, int32_t max_group,
+                                 float *s_out, float *d_out, void *workspace, size_t ws_bytes,
+                                 void *stream);
+
+/* Eq. value-perturbation on its own: v (DEVICE, model dtype) holds the Values of
+ * one layer for a batch, row r at v + r * row_stride elements, n_kv_heads *
+ * head_dim contiguous values per row; they are replaced in place by
+ * v + alpha * ||v||_2 * eps on the eligible positions.  eps is the Philox stream
+ * of (seed, sequence index, layer, KV head, position).                          */
+rk_status rk_perturb_values(const rk_model *m, const rk_batch *batch, int32_t layer, float alpha,
+                            const rk_perturb_params *p, void *v, int64_t row_stride, void *stream);
+
+/* ---------------------------------------------------------------- allocation */
+
+/* Algorithm 1, allocation half (Section 4.4, Eqs. sensitivity-normalization,
+ * sensitivity-mapping, weight-normalization, layer-budget).  Host only,
+ * synchronous, float64.
+ *   s: [n] finite sensitivities; B >= 0 global budget; r >= 1 ratio;
+ *   gamma: clip bound >= 1, or <= 0 / infinity for no clipping;
+ *   eps: denominator guard of the min-max step (0 = the equation, with a
+ *        constant profile mapped to all zeros);
+ *   w_out: [n] multipliers or NULL; b_out: [n] integer budgets.
+ * With RK_ROUND_LARGEST_REMAINDER sum(b) == B: b = floor(q) for q = B w / n
+ * snapped to multiples of 2^-20, then the leftover units go to the largest
+ * fractional parts (ties: larger s, then lower index).                          */
+rk_status rk_layer_budgets(const double *s, int32_t n, int64_t B, double r, double gamma, double eps,
+                           rk_rounding mode, double *w_out, int64_t *b_out);
+
+/* Message of the last error on the calling thread ("" if none). */
+const char *rk_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RK_H */

@@ -1,0 +1,517 @@
+// C ABI and pass scheduler of the sensitivity profile (Algorithm 1, Section 4.3).
+//
+// Scheduling: the sequences of a calibration set are processed in batches whose
+// rows are concatenated, so every projection GEMM sees M = sum of the batch's
+// lengths.  Per batch:
+//   ReferencePredict  embed -> L blocks (keeping each block's fp32 input h_l)
+//                     -> final RMSNorm -> clean log-sum-exp of the LM head;
+//   per (alpha, l)    resume from h_l: block l with the Value noise injected
+//                     between the q|k|v projection and attention, blocks
+//                     l+1..L-1, final RMSNorm -> x_pert (one slot of a group);
+//   per group         one LM-head + KL launch scores up to 16 passes against
+//                     the clean logits computed once per tile, then window
+//                     means and the calibration accumulator.
+// Layers below l are never recomputed (prefix reuse); the same kernels on the
+// same row layout make the clean and perturbed computations bitwise identical
+// until the noise enters, so alpha = 0 gives KL = 0 exactly.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "rk_internal.h"
+
+struct rk_model {
+  rk_model_config cfg;
+  bool bf16;
+  int qkv_cols, attn_cols;
+  const void* tok_emb;
+  const void* lm_head;
+  const float* final_norm;
+  std::vector<const void*> w_qkv, w_o, w_gate_up, w_down;
+  std::vector<const float*> attn_norm, mlp_norm;
+};
+
+namespace rk {
+
+static thread_local std::string g_error;
+
+void set_error(const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_error = buf;
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+static size_t act_bytes(const rk_model* m) { return m->bf16 ? 2 : 4; }
+
+// ----------------------------------------------------------------------------- memory plans
+struct CleanPlan {
+  size_t h, xf, lse, total;
+};
+
+static CleanPlan clean_plan(const rk_model* m, int64_t R) {
+  const int64_t d = m->cfg.d_model;
+  CleanPlan p;
+  size_t o = 0;
+  p.h = o;   o += align256((size_t)m->cfg.n_layers * R * d * 4);
+  p.xf = o;  o += align256((size_t)R * d * act_bytes(m));
+  p.lse = o; o += align256((size_t)R * 4);
+  p.total = o;
+  return p;
+}
+
+struct WsPlan {
+  size_t h, x, qkv, att, ff, xp, part, logits_c, logits_p, kl, rope, dbatch, sacc, clean, total;
+  bool unfused;
+};
+
+static const int kMaxSAcc = 4096;
+
+static WsPlan ws_plan(const rk_model* m, int64_t R, int G, uint32_t flags) {
+  const rk_model_config& c = m->cfg;
+  const size_t a = act_bytes(m);
+  WsPlan p;
+  p.unfused = !m->bf16 || (flags & RK_FLAG_UNFUSED_KL);
+  size_t o = 0;
+  p.h = o;        o += align256((size_t)R * c.d_model * 4);
+  p.x = o;        o += align256((size_t)R * c.d_model * a);
+  p.qkv = o;      o += align256((size_t)R * m->qkv_cols * a);
+  p.att = o;      o += align256((size_t)R * m->attn_cols * a);
+  p.ff = o;       o += align256((size_t)R * c.d_ff * a);
+  p.xp = o;       o += align256((size_t)G * R * c.d_model * a);
+  p.part = o;
+  if (m->bf16) {
+    // chunks(rows) * rows <= min(n_vt * 128 * n_tt, (2048 + n_tt) * 128) for rows <= R
+    const size_t n_vt = c.vocab / 128, n_tt = (R + 127) / 128;
+    const size_t bound = std::min(n_vt * 128 * n_tt, (2048 + n_tt) * 128);
+    o += align256(bound * (size_t)G * 8);
+  }
+  p.logits_c = o;
+  if (p.unfused) o += align256((size_t)R * c.vocab * 4);
+  p.logits_p = o;
+  if (p.unfused) o += align256((size_t)G * R * c.vocab * 4);
+  p.kl = o;       o += align256((size_t)G * R * 4);
+  p.rope = o;     o += align256((size_t)R * (c.head_dim / 2) * 8);
+  p.dbatch = o;   o += align256((size_t)G * RK_MAX_BATCH_SEQS * 4);
+  p.sacc = o;     o += align256((size_t)kMaxSAcc * 8);
+  p.clean = o;
+  if (flags & RK_WS_CLEAN_STATE) o += clean_plan(m, R).total;
+  p.total = o;
+  return p;
+}
+
+// Device buffers of one batch, carved from the workspace.
+struct Bufs {
+  float* h; void* x; void* qkv; void* att; void* ff; void* xp;
+  float2* part; float* logits_c; float* logits_p; float* kl; float2* rope; float* dbatch; double* sacc;
+  char* clean;
+};
+
+static Bufs carve(const WsPlan& p, void* ws) {
+  char* b = (char*)ws;
+  Bufs u;
+  u.h = (float*)(b + p.h); u.x = b + p.x; u.qkv = b + p.qkv; u.att = b + p.att; u.ff = b + p.ff;
+  u.xp = b + p.xp; u.part = (float2*)(b + p.part); u.logits_c = (float*)(b + p.logits_c);
+  u.logits_p = (float*)(b + p.logits_p); u.kl = (float*)(b + p.kl); u.rope = (float2*)(b + p.rope);
+  u.dbatch = (float*)(b + p.dbatch); u.sacc = (double*)(b + p.sacc); u.clean = b + p.clean;
+  return u;
+}
+
+struct Clean {
+  float* h; void* xf; float* lse;
+};
+
+static Clean clean_view(const rk_model* m, int64_t R, const void* base) {
+  const CleanPlan p = clean_plan(m, R);
+  char* b = (char*)base;
+  return Clean{(float*)(b + p.h), b + p.xf, (float*)(b + p.lse)};
+}
+
+// ----------------------------------------------------------------------------- passes
+#define RK_TRY(expr)                                                       \
+  do {                                                                     \
+    hipError_t _e = (expr);                                                \
+    if (_e != hipSuccess) {                                                \
+      set_error("HIP error in %s: %s", #expr, hipGetErrorString(_e));      \
+      return RK_ERR_HIP;                                                   \
+    }                                                                      \
+  } while (0)
+
+struct Noise {
+  float alpha;
+  const rk_perturb_params* p;
+};
+
+// One decoder block from h_in to h_out (h_out may equal h_in); `noise` perturbs
+// the block's Values between the q|k|v projection and attention.
+static rk_status run_block(const rk_model* m, int l, const float* h_in, float* h_out, const Bufs& b,
+                           const SeqTable& st, const Noise* noise, hipStream_t s) {
+  const rk_model_config& c = m->cfg;
+  const int R = st.rows, d = c.d_model;
+  RK_TRY(launch_rmsnorm(h_in, m->attn_norm[l], b.x, m->bf16, R, d, c.rms_eps, s));
+  GemmArgs g{};
+  g.A = b.x; g.lda = d; g.B = m->w_qkv[l]; g.ldb = d; g.M = R; g.N = m->qkv_cols; g.K = d;
+  g.epi = Epi::kStoreRope; g.out = b.qkv; g.ldo = m->qkv_cols;
+  g.rope_cols = (c.n_heads + c.n_kv_heads) * c.head_dim; g.head_dim = c.head_dim; g.rope_tab = b.rope; g.seq = st;
+  RK_TRY(launch_gemm(g, m->bf16, s));
+  if (noise) {
+    char* v = (char*)b.qkv + (size_t)(c.n_heads + c.n_kv_heads) * c.head_dim * act_bytes(m);
+    RK_TRY(launch_value_noise(v, m->bf16, m->qkv_cols, st, c.n_kv_heads, c.head_dim, l, noise->alpha,
+                              noise->p->seed, noise->p->protect_head, noise->p->protect_tail, s));
+  }
+  RK_TRY(launch_attention(b.qkv, m->qkv_cols, b.att, m->attn_cols, st, c.n_heads, c.n_kv_heads, c.head_dim,
+                          m->bf16, s));
+  g = GemmArgs{};
+  g.A = b.att; g.lda = m->attn_cols; g.B = m->w_o[l]; g.ldb = m->attn_cols; g.M = R; g.N = d; g.K = m->attn_cols;
+  g.epi = Epi::kResidual; g.out = h_out; g.ldo = d; g.res = h_in; g.ldr = d;
+  RK_TRY(launch_gemm(g, m->bf16, s));
+  RK_TRY(launch_rmsnorm(h_out, m->mlp_norm[l], b.x, m->bf16, R, d, c.rms_eps, s));
+  g = GemmArgs{};
+  g.A = b.x; g.lda = d; g.B = m->w_gate_up[l]; g.ldb = d; g.M = R; g.N = 2 * c.d_ff; g.K = d;
+  g.epi = Epi::kSwiGLU; g.out = b.ff; g.ldo = c.d_ff; g.d_ff = c.d_ff;
+  RK_TRY(launch_gemm(g, m->bf16, s));
+  g = GemmArgs{};
+  g.A = b.ff; g.lda = c.d_ff; g.B = m->w_down[l]; g.ldb = c.d_ff; g.M = R; g.N = d; g.K = c.d_ff;
+  g.epi = Epi::kResidual; g.out = h_out; g.ldo = d; g.res = h_out; g.ldr = d;
+  RK_TRY(launch_gemm(g, m->bf16, s));
+  return RK_OK;
+}
+
+static rk_status reference_forward(const rk_model* m, const int32_t* tokens, const SeqTable& st, const Clean& cl,
+                                   const Bufs& b, hipStream_t s) {
+  const rk_model_config& c = m->cfg;
+  const int64_t R = st.rows, d = c.d_model;
+  RK_TRY(launch_rope_table(b.rope, st.max_len, c.head_dim, c.rope_theta, s));
+  RK_TRY(launch_embed(m->tok_emb, m->bf16, tokens, cl.h, (int)R, (int)d, s));
+  for (int l = 0; l < c.n_layers; ++l) {
+    float* out = (l + 1 < c.n_layers) ? cl.h + (size_t)(l + 1) * R * d : b.h;
+    rk_status e = run_block(m, l, cl.h + (size_t)l * R * d, out, b, st, nullptr, s);
+    if (e != RK_OK) return e;
+  }
+  RK_TRY(launch_rmsnorm(b.h, m->final_norm, cl.xf, m->bf16, (int)R, (int)d, c.rms_eps, s));
+  if (m->bf16)
+    RK_TRY(launch_lm_lse((const bf16_t*)cl.xf, (const bf16_t*)m->lm_head, (int)R, (int)d, c.vocab, b.part, cl.lse, s));
+  return RK_OK;
+}
+
+// PerturbedPredict up to the final normalised hidden state (written to xf_out).
+static rk_status perturbed_final(const rk_model* m, const int32_t* tokens, const SeqTable& st, const Clean& cl,
+                                 int layer, float alpha, const rk_perturb_params* p, void* xf_out, const Bufs& b,
+                                 hipStream_t s) {
+  const rk_model_config& c = m->cfg;
+  const int64_t R = st.rows, d = c.d_model;
+  const float* h_in = cl.h + (size_t)layer * R * d;
+  if (p->flags & RK_FLAG_FULL_RECOMPUTE) {
+    RK_TRY(launch_embed(m->tok_emb, m->bf16, tokens, b.h, (int)R, (int)d, s));
+    for (int l = 0; l < layer; ++l) {
+      rk_status e = run_block(m, l, b.h, b.h, b, st, nullptr, s);
+      if (e != RK_OK) return e;
+    }
+    h_in = b.h;
+  }
+  Noise nz{alpha, p};
+  rk_status e = run_block(m, layer, h_in, b.h, b, st, &nz, s);
+  if (e != RK_OK) return e;
+  for (int l = layer + 1; l < c.n_layers; ++l) {
+    e = run_block(m, l, b.h, b.h, b, st, nullptr, s);
+    if (e != RK_OK) return e;
+  }
+  RK_TRY(launch_rmsnorm(b.h, m->final_norm, xf_out, m->bf16, (int)R, (int)d, c.rms_eps, s));
+  return RK_OK;
+}
+
+// KL at every position for G passes whose final hidden states sit at xp (stride R*d).
+// Unfused: the clean logits must already be in logits_c; pass logits go to lp.
+static rk_status score_group(const rk_model* m, const SeqTable& st, const Clean& cl, const void* xp, int G,
+                             bool unfused, float* lp, float* kl, const Bufs& b, hipStream_t s) {
+  const rk_model_config& c = m->cfg;
+  const int64_t R = st.rows, d = c.d_model;
+  if (!unfused) {
+    RK_TRY(launch_lm_kl((const bf16_t*)cl.xf, (const bf16_t*)xp, R * d, G, (const bf16_t*)m->lm_head, (int)R, (int)d,
+                        c.vocab, cl.lse, b.part, kl, s));
+    return RK_OK;
+  }
+  for (int g = 0; g < G; ++g) {
+    GemmArgs a{};
+    a.A = (const char*)xp + (size_t)g * R * d * act_bytes(m); a.lda = d; a.B = m->lm_head; a.ldb = d;
+    a.M = (int)R; a.N = c.vocab; a.K = (int)d; a.epi = Epi::kStoreF32;
+    a.out = lp + (size_t)g * R * c.vocab; a.ldo = c.vocab;
+    RK_TRY(launch_gemm(a, m->bf16, s));
+  }
+  RK_TRY(launch_kl_logits(b.logits_c, lp, R * c.vocab, G, (int)R, c.vocab, kl, s));
+  return RK_OK;
+}
+
+static rk_status clean_logits(const rk_model* m, const SeqTable& st, const Clean& cl, float* out, hipStream_t s) {
+  const rk_model_config& c = m->cfg;
+  GemmArgs a{};
+  a.A = cl.xf; a.lda = c.d_model; a.B = m->lm_head; a.ldb = c.d_model;
+  a.M = st.rows; a.N = c.vocab; a.K = c.d_model; a.epi = Epi::kStoreF32; a.out = out; a.ldo = c.vocab;
+  RK_TRY(launch_gemm(a, m->bf16, s));
+  return RK_OK;
+}
+
+// ----------------------------------------------------------------------------- validation
+static rk_status make_table(const rk_batch* bt, int first, int count, SeqTable* st) {
+  if (count < 1 || count > RK_MAX_BATCH_SEQS) {
+    set_error("batch holds %d sequences (1..%d allowed)", count, RK_MAX_BATCH_SEQS);
+    return RK_ERR_SHAPE;
+  }
+  const int64_t base = bt->offsets[first];
+  st->n = count;
+  st->seq_index0 = bt->seq_index0 + first;
+  st->max_len = 0;
+  for (int k = 0; k <= count; ++k) {
+    const int64_t o = bt->offsets[first + k] - base;
+    if (o < 0 || o > (int64_t)0x7fffffff) { set_error("offsets out of range"); return RK_ERR_SHAPE; }
+    st->off[k] = (int32_t)o;
+    if (k > 0) {
+      const int64_t len = bt->offsets[first + k] - bt->offsets[first + k - 1];
+      if (len < 0) { set_error("offsets must be non-decreasing"); return RK_ERR_SHAPE; }
+      if (len > st->max_len) st->max_len = (int32_t)len;
+    }
+  }
+  st->rows = st->off[count];
+  if (st->rows < 1) { set_error("batch has no tokens"); return RK_ERR_SHAPE; }
+  return RK_OK;
+}
+
+static rk_status check_batch(const rk_model* m, const rk_batch* b) {
+  if (!m || !b || !b->tokens || !b->offsets) { set_error("null model, batch, tokens or offsets"); return RK_ERR_ARG; }
+  if (b->n_seqs < 1) { set_error("n_seqs must be >= 1"); return RK_ERR_ARG; }
+  if (b->seq_index0 < 0) { set_error("seq_index0 must be >= 0"); return RK_ERR_ARG; }
+  if (b->offsets[0] != 0) { set_error("offsets[0] must be 0"); return RK_ERR_SHAPE; }
+  return RK_OK;
+}
+
+static rk_status check_params(const rk_perturb_params* p) {
+  if (!p) { set_error("null perturbation params"); return RK_ERR_ARG; }
+  if (p->window_start < 0 || p->protect_head < 0 || p->protect_tail < 0) {
+    set_error("window_start / protect_head / protect_tail must be >= 0");
+    return RK_ERR_ARG;
+  }
+  if (p->flags & ~(RK_FLAG_FULL_RECOMPUTE | RK_FLAG_UNFUSED_KL)) { set_error("unknown flags"); return RK_ERR_ARG; }
+  return RK_OK;
+}
+
+}  // namespace rk
+
+using namespace rk;
+
+// ============================================================================= C ABI
+extern "C" {
+
+const char* rk_last_error(void) { return g_error.c_str(); }
+
+rk_status rk_model_create(const rk_model_config* cfg, const rk_model_weights* w, rk_model** out) {
+  if (!cfg || !w || !out) { set_error("rk_model_create: null argument"); return RK_ERR_ARG; }
+  *out = nullptr;
+  const rk_model_config& c = *cfg;
+  if (c.n_layers < 1 || c.d_model < 1 || c.n_heads < 1 || c.n_kv_heads < 1 || c.head_dim < 1 || c.d_ff < 1 ||
+      c.vocab < 1) {
+    set_error("rk_model_create: sizes must be positive");
+    return RK_ERR_ARG;
+  }
+  if (!(c.rope_theta > 1.0f) || !isfinite(c.rope_theta) || !(c.rms_eps >= 0.0f) || !isfinite(c.rms_eps)) {
+    set_error("rk_model_create: rope_theta must be > 1 and rms_eps >= 0");
+    return RK_ERR_ARG;
+  }
+  if (c.dtype != RK_F32 && c.dtype != RK_BF16) { set_error("rk_model_create: unknown dtype"); return RK_ERR_ARG; }
+  if (c.n_heads % c.n_kv_heads) { set_error("n_heads must be a multiple of n_kv_heads"); return RK_ERR_UNSUPPORTED; }
+  const bool bf16 = c.dtype == RK_BF16;
+  const int qkv = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim, att = c.n_heads * c.head_dim;
+  if (bf16 ? (c.head_dim != 64 && c.head_dim != 128) : (c.head_dim != 32 && c.head_dim != 64 && c.head_dim != 128)) {
+    set_error("head_dim %d not supported for this dtype", c.head_dim);
+    return RK_ERR_UNSUPPORTED;
+  }
+  if (c.d_model % 128 || att % 128 || qkv % 128 || c.vocab % 128 || c.d_ff % 64) {
+    set_error("d_model, n_heads*head_dim, q|k|v width and vocab must be multiples of 128 and d_ff of 64");
+    return RK_ERR_UNSUPPORTED;
+  }
+  if (!w->tok_emb || !w->lm_head || !w->final_norm || !w->w_qkv || !w->w_o || !w->w_gate_up || !w->w_down ||
+      !w->attn_norm || !w->mlp_norm) {
+    set_error("rk_model_create: null weight pointer");
+    return RK_ERR_ARG;
+  }
+  for (int l = 0; l < c.n_layers; ++l)
+    if (!w->w_qkv[l] || !w->w_o[l] || !w->w_gate_up[l] || !w->w_down[l] || !w->attn_norm[l] || !w->mlp_norm[l]) {
+      set_error("rk_model_create: null weight pointer in layer %d", l);
+      return RK_ERR_ARG;
+    }
+  rk_model* m = new rk_model();
+  m->cfg = c;
+  m->bf16 = bf16;
+  m->qkv_cols = qkv;
+  m->attn_cols = att;
+  m->tok_emb = w->tok_emb;
+  m->lm_head = w->lm_head;
+  m->final_norm = w->final_norm;
+  m->w_qkv.assign(w->w_qkv, w->w_qkv + c.n_layers);
+  m->w_o.assign(w->w_o, w->w_o + c.n_layers);
+  m->w_gate_up.assign(w->w_gate_up, w->w_gate_up + c.n_layers);
+  m->w_down.assign(w->w_down, w->w_down + c.n_layers);
+  m->attn_norm.assign(w->attn_norm, w->attn_norm + c.n_layers);
+  m->mlp_norm.assign(w->mlp_norm, w->mlp_norm + c.n_layers);
+  *out = m;
+  return RK_OK;
+}
+
+void rk_model_destroy(rk_model* m) { delete m; }
+
+size_t rk_clean_state_size(const rk_model* m, int64_t n_rows) {
+  if (!m || n_rows < 1) return 0;
+  return clean_plan(m, n_rows).total;
+}
+
+size_t rk_workspace_size(const rk_model* m, int64_t max_rows, int32_t max_group, uint32_t flags) {
+  if (!m || max_rows < 1 || max_group < 1 || max_group > RK_MAX_GROUP) return 0;
+  return ws_plan(m, max_rows, max_group, flags).total;
+}
+
+rk_status rk_reference_forward(const rk_model* m, const rk_batch* batch, void* clean_state, size_t clean_bytes,
+                               void* workspace, size_t ws_bytes, void* stream) {
+  rk_status e = check_batch(m, batch);
+  if (e != RK_OK) return e;
+  if (!clean_state || !workspace) { set_error("null clean state or workspace"); return RK_ERR_ARG; }
+  SeqTable st;
+  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  if (clean_bytes < clean_plan(m, st.rows).total) { set_error("clean state too small"); return RK_ERR_WORKSPACE; }
+  const WsPlan wp = ws_plan(m, st.rows, 1, 0);
+  if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
+  const Bufs b = carve(wp, workspace);
+  return reference_forward(m, batch->tokens, st, clean_view(m, st.rows, clean_state), b, (hipStream_t)stream);
+}
+
+rk_status rk_profile_layer(const rk_model* m, const rk_batch* batch, int32_t layer, float alpha,
+                           const rk_perturb_params* p, const void* clean_state, size_t clean_bytes, float* d_out,
+                           float* kl_pos, float* logits_out, void* workspace, size_t ws_bytes, void* stream) {
+  rk_status e = check_batch(m, batch);
+  if (e != RK_OK) return e;
+  if ((e = check_params(p)) != RK_OK) return e;
+  if (!clean_state || !workspace || !d_out) { set_error("null clean state, workspace or d_out"); return RK_ERR_ARG; }
+  if (layer < 0 || layer >= m->cfg.n_layers) { set_error("layer %d out of range", layer); return RK_ERR_ARG; }
+  if (!(alpha >= 0.0f) || !isfinite(alpha)) { set_error("alpha must be finite and >= 0"); return RK_ERR_ARG; }
+  SeqTable st;
+  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  if (clean_bytes < clean_plan(m, st.rows).total) { set_error("clean state too small"); return RK_ERR_WORKSPACE; }
+  const bool unfused = !m->bf16 || logits_out || (p->flags & RK_FLAG_UNFUSED_KL);
+  const WsPlan wp = ws_plan(m, st.rows, 1, unfused ? RK_FLAG_UNFUSED_KL : 0);
+  if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
+  const Bufs b = carve(wp, workspace);
+  const Clean cl = clean_view(m, st.rows, clean_state);
+  hipStream_t s = (hipStream_t)stream;
+  RK_TRY(launch_rope_table(b.rope, st.max_len, m->cfg.head_dim, m->cfg.rope_theta, s));
+  if ((e = perturbed_final(m, batch->tokens, st, cl, layer, alpha, p, b.xp, b, s)) != RK_OK) return e;
+  float* kl = kl_pos ? kl_pos : b.kl;
+  if (unfused && (e = clean_logits(m, st, cl, b.logits_c, s)) != RK_OK) return e;
+  if ((e = score_group(m, st, cl, b.xp, 1, unfused, logits_out ? logits_out : b.logits_p, kl, b, s)) != RK_OK)
+    return e;
+  RK_TRY(launch_window_mean(kl, st.rows, 1, st, p->window_start, d_out, s));
+  return RK_OK;
+}
+
+rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const int32_t* layers, int32_t n_A,
+                                 const float* alphas, int32_t n_alpha, const rk_perturb_params* p, int64_t max_rows,
+                                 int32_t max_group, float* s_out, float* d_out, void* workspace, size_t ws_bytes,
+                                 void* stream) {
+  if (!m || !calib || !calib->tokens || !calib->offsets) { set_error("null model or calibration set"); return RK_ERR_ARG; }
+  rk_status e = check_params(p);
+  if (e != RK_OK) return e;
+  if (calib->n_seqs < 1 || calib->seq_index0 < 0) { set_error("n_seqs must be >= 1, seq_index0 >= 0"); return RK_ERR_ARG; }
+  if (calib->offsets[0] != 0) { set_error("offsets[0] must be 0"); return RK_ERR_SHAPE; }
+  if (!layers || n_A < 1 || !alphas || n_alpha < 1 || !s_out || !workspace) {
+    set_error("null layers/alphas/s_out/workspace or empty layer/alpha set");
+    return RK_ERR_ARG;
+  }
+  if ((int64_t)n_A * n_alpha > kMaxSAcc) { set_error("n_A * n_alpha must be <= %d", kMaxSAcc); return RK_ERR_ARG; }
+  for (int j = 0; j < n_A; ++j)
+    if (layers[j] < 0 || layers[j] >= m->cfg.n_layers) { set_error("layer %d out of range", layers[j]); return RK_ERR_ARG; }
+  for (int a = 0; a < n_alpha; ++a)
+    if (!(alphas[a] >= 0.0f) || !isfinite(alphas[a])) { set_error("alphas must be finite and >= 0"); return RK_ERR_ARG; }
+  if (max_group < 1 || max_group > RK_MAX_GROUP) { set_error("max_group must be in [1, %d]", RK_MAX_GROUP); return RK_ERR_ARG; }
+  if (max_rows < 1) { set_error("max_rows must be >= 1"); return RK_ERR_ARG; }
+  const int N = calib->n_seqs;
+  for (int i = 0; i < N; ++i) {
+    const int64_t len = calib->offsets[i + 1] - calib->offsets[i];
+    if (len < 0) { set_error("offsets must be non-decreasing"); return RK_ERR_SHAPE; }
+    if (len > max_rows) { set_error("sequence %d (%lld tokens) exceeds max_rows", i, (long long)len); return RK_ERR_SHAPE; }
+    if (len == 0) { set_error("sequence %d is empty", i); return RK_ERR_SHAPE; }
+  }
+  const bool unfused = !m->bf16 || (p->flags & RK_FLAG_UNFUSED_KL);
+  const uint32_t wflags = RK_WS_CLEAN_STATE | (unfused ? RK_FLAG_UNFUSED_KL : 0);
+  const WsPlan wp = ws_plan(m, max_rows, max_group, wflags);
+  if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
+
+  hipStream_t s = (hipStream_t)stream;
+  // Buffers are carved for max_rows; each batch uses the leading rows of each.
+  const Bufs b = carve(wp, workspace);
+  RK_TRY(launch_zero_f64(b.sacc, n_A * n_alpha, s));
+  const int n_pass = n_A * n_alpha;
+  int first = 0;
+  while (first < N) {
+    int count = 0;
+    int64_t rows = 0;
+    while (first + count < N && count < RK_MAX_BATCH_SEQS) {
+      const int64_t len = calib->offsets[first + count + 1] - calib->offsets[first + count];
+      if (count > 0 && rows + len > max_rows) break;
+      rows += len;
+      ++count;
+    }
+    SeqTable st;
+    if ((e = make_table(calib, first, count, &st)) != RK_OK) return e;
+    const int32_t* tokens = calib->tokens + calib->offsets[first];
+    const int64_t R = st.rows;
+    const Clean cl = clean_view(m, R, b.clean);
+    if ((e = reference_forward(m, tokens, st, cl, b, s)) != RK_OK) return e;
+    if (unfused && (e = clean_logits(m, st, cl, b.logits_c, s)) != RK_OK) return e;
+    for (int g0 = 0; g0 < n_pass; g0 += max_group) {
+      const int G = (n_pass - g0 < max_group) ? n_pass - g0 : max_group;
+      PassMap pm{};
+      pm.G = G;
+      pm.seq_index0 = first;
+      pm.d_seq_stride = n_A;
+      for (int k = 0; k < G; ++k) {
+        const int idx = g0 + k, a = idx / n_A, j = idx % n_A;
+        void* xf = (char*)b.xp + (size_t)k * R * m->cfg.d_model * act_bytes(m);
+        if ((e = perturbed_final(m, tokens, st, cl, layers[j], alphas[a], p, xf, b, s)) != RK_OK) return e;
+        pm.d_base[k] = (int64_t)a * N * n_A + j;
+        pm.s_index[k] = a * n_A + j;
+      }
+      if ((e = score_group(m, st, cl, b.xp, G, unfused, b.logits_p, b.kl, b, s)) != RK_OK) return e;
+      RK_TRY(launch_window_mean(b.kl, R, G, st, p->window_start, b.dbatch, s));
+      RK_TRY(launch_accumulate(b.dbatch, st.n, pm, d_out, b.sacc, s));
+    }
+    first += count;
+  }
+  RK_TRY(launch_finalize(b.sacc, n_pass, 1.0 / (double)N, s_out, s));
+  return RK_OK;
+}
+
+rk_status rk_perturb_values(const rk_model* m, const rk_batch* batch, int32_t layer, float alpha,
+                            const rk_perturb_params* p, void* v, int64_t row_stride, void* stream) {
+  rk_status e = check_batch(m, batch);
+  if (e != RK_OK) return e;
+  if ((e = check_params(p)) != RK_OK) return e;
+  if (!v) { set_error("null value buffer"); return RK_ERR_ARG; }
+  if (layer < 0 || layer >= m->cfg.n_layers) { set_error("layer %d out of range", layer); return RK_ERR_ARG; }
+  if (!(alpha >= 0.0f) || !isfinite(alpha)) { set_error("alpha must be finite and >= 0"); return RK_ERR_ARG; }
+  if (row_stride < (int64_t)m->cfg.n_kv_heads * m->cfg.head_dim) { set_error("row_stride too small"); return RK_ERR_SHAPE; }
+  SeqTable st;
+  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  const rk_model_config& c = m->cfg;
+  if (c.head_dim != 32 && c.head_dim != 64 && c.head_dim != 128) { set_error("head_dim unsupported"); return RK_ERR_UNSUPPORTED; }
+  RK_TRY(launch_value_noise(v, m->bf16, row_stride, st, c.n_kv_heads, c.head_dim, layer, alpha, p->seed,
+                            p->protect_head, p->protect_tail, (hipStream_t)stream));
+  return RK_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,252 @@
+// HBM-bound kernels of the profiling path: embedding gather, RMSNorm, the rotary
+// table, the norm-adaptive Value noise (Eq. value-perturbation) and the window /
+// calibration means (Eqs. sample-response and layer-sensitivity).
+#include "rk_internal.h"
+
+namespace rk {
+
+// --------------------------------------------------------------------------- embedding
+template <typename E>
+__global__ void embed_kernel(const E* __restrict__ emb, const int32_t* __restrict__ tok, float* __restrict__ h,
+                             int rows, int d) {
+  const int64_t total = (int64_t)rows * d;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / d, c = i - r * d;
+    h[i] = Act<E>::load(emb + (int64_t)tok[r] * d + c);
+  }
+}
+
+hipError_t launch_embed(const void* emb, bool emb_bf16, const int32_t* tokens, float* h, int rows, int d,
+                        hipStream_t s) {
+  const int64_t total = (int64_t)rows * d;
+  int blocks = (int)((total + 255) / 256);
+  if (blocks > 65536) blocks = 65536;
+  if (blocks < 1) blocks = 1;
+  if (emb_bf16)
+    embed_kernel<bf16_t><<<blocks, 256, 0, s>>>((const bf16_t*)emb, tokens, h, rows, d);
+  else
+    embed_kernel<float><<<blocks, 256, 0, s>>>((const float*)emb, tokens, h, rows, d);
+  return hipGetLastError();
+}
+
+// --------------------------------------------------------------------------- RMSNorm
+// One wave per row: out = h / sqrt(mean(h^2) + eps) * g.  fp32 in, act out.
+template <typename O>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ h, const float* __restrict__ g,
+                                                      O* __restrict__ out, int rows, int d, float eps) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const float4* hr = reinterpret_cast<const float4*>(h + (int64_t)row * d);
+  const int n4 = d >> 2;
+  float ss = 0.f;
+  for (int i = lane; i < n4; i += 64) {
+    float4 v = hr[i];
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  const float4* g4 = reinterpret_cast<const float4*>(g);
+  O* orow = out + (int64_t)row * d;
+  for (int i = lane; i < n4; i += 64) {
+    float4 v = hr[i], w = g4[i];
+    Act<O>::store(orow + 4 * i + 0, v.x * inv * w.x);
+    Act<O>::store(orow + 4 * i + 1, v.y * inv * w.y);
+    Act<O>::store(orow + 4 * i + 2, v.z * inv * w.z);
+    Act<O>::store(orow + 4 * i + 3, v.w * inv * w.w);
+  }
+}
+
+hipError_t launch_rmsnorm(const float* h, const float* g, void* out, bool out_bf16, int rows, int d, float eps,
+                          hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  const int blocks = (rows + 3) / 4;
+  if (out_bf16)
+    rmsnorm_kernel<bf16_t><<<blocks, 256, 0, s>>>(h, g, (bf16_t*)out, rows, d, eps);
+  else
+    rmsnorm_kernel<float><<<blocks, 256, 0, s>>>(h, g, (float*)out, rows, d, eps);
+  return hipGetLastError();
+}
+
+// --------------------------------------------------------------------------- rotary table
+// tab[t * (dh/2) + j] = (cos, sin)(t * theta^(-2j/dh)); the angle is formed and
+// reduced modulo 2*pi in double precision before the fp32 sincos.
+__global__ void rope_table_kernel(float2* tab, int max_len, int half, int dh, double log2_theta) {
+  const int64_t total = (int64_t)max_len * half;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int t = (int)(i / half), j = (int)(i - (int64_t)t * half);
+    const double inv_freq = exp2(-(2.0 * j / dh) * log2_theta);
+    double ang = (double)t * inv_freq;
+    const double two_pi = 6.283185307179586476925;
+    ang -= two_pi * floor(ang / two_pi);
+    double sv, cv;
+    sincos(ang, &sv, &cv);
+    tab[i] = make_float2((float)cv, (float)sv);
+  }
+}
+
+hipError_t launch_rope_table(float2* tab, int max_len, int head_dim, float theta, hipStream_t s) {
+  const int half = head_dim / 2;
+  const int64_t total = (int64_t)max_len * half;
+  int blocks = (int)((total + 255) / 256);
+  if (blocks > 16384) blocks = 16384;
+  if (blocks < 1) blocks = 1;
+  rope_table_kernel<<<blocks, 256, 0, s>>>(tab, max_len, half, head_dim, log2((double)theta));
+  return hipGetLastError();
+}
+
+// --------------------------------------------------------------------------- Value noise
+// Philox4x32-10 (Salmon et al., SC'11): counter (c0..c3), key (k0, k1), ten rounds.
+__device__ __forceinline__ void philox10(uint32_t& c0, uint32_t& c1, uint32_t& c2, uint32_t& c3, uint32_t k0,
+                                         uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
+    const uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
+    const uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+    const uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+    c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
+  }
+}
+
+// 32-bit word -> uniform in (0, 1): (2 * (x >> 9) + 1) * 2^-24, exact in fp32.
+__device__ __forceinline__ float to_uniform(uint32_t x) {
+  return (float)(2u * (x >> 9) + 1u) * 5.9604644775390625e-8f;
+}
+
+// One thread owns four consecutive coordinates j = 4g..4g+3 of one (row, KV head)
+// Value vector; TPV = head_dim / 4 threads cooperate on the vector's norm.
+template <typename T, int TPV>
+__global__ __launch_bounds__(256) void value_noise_kernel(T* __restrict__ v, int64_t row_stride, SeqTable st,
+                                                          int n_kv_heads, int layer, float alpha, uint32_t key0,
+                                                          uint32_t key1, int protect_head, int protect_tail) {
+  constexpr int VPB = 256 / TPV;  // vectors per block
+  const int sub = threadIdx.x % TPV;
+  const int64_t vec = (int64_t)blockIdx.x * VPB + threadIdx.x / TPV;
+  const int64_t n_vec = (int64_t)st.rows * n_kv_heads;
+  const bool live = vec < n_vec;
+  const int row = live ? (int)(vec / n_kv_heads) : 0;
+  const int head = live ? (int)(vec - (int64_t)row * n_kv_heads) : 0;
+  const int k = seq_of_row(st, row);
+  const int u = row - st.off[k];
+  const int len = st.off[k + 1] - st.off[k];
+  T* p = v + (int64_t)row * row_stride + (int64_t)head * (TPV * 4) + sub * 4;
+  float x0 = 0.f, x1 = 0.f, x2 = 0.f, x3 = 0.f;
+  if (live) {
+    x0 = Act<T>::load(p + 0); x1 = Act<T>::load(p + 1);
+    x2 = Act<T>::load(p + 2); x3 = Act<T>::load(p + 3);
+  }
+  float ss = x0 * x0 + x1 * x1 + x2 * x2 + x3 * x3;
+#pragma unroll
+  for (int m = TPV / 2; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
+  const bool eligible = live && u >= protect_head && u < len - protect_tail;
+  if (!eligible) return;
+  const float an = alpha * sqrtf(ss);
+  uint32_t c0 = (uint32_t)u, c1 = (uint32_t)sub | ((uint32_t)head << 16), c2 = (uint32_t)layer,
+           c3 = (uint32_t)(st.seq_index0 + k);
+  philox10(c0, c1, c2, c3, key0, key1);
+  const float r0 = sqrtf(-2.0f * logf(to_uniform(c0)));
+  const float r1 = sqrtf(-2.0f * logf(to_uniform(c2)));
+  float s0, co0, s1, co1;
+  sincospif(2.0f * to_uniform(c1), &s0, &co0);
+  sincospif(2.0f * to_uniform(c3), &s1, &co1);
+  Act<T>::store(p + 0, fmaf(an, r0 * co0, x0));
+  Act<T>::store(p + 1, fmaf(an, r0 * s0, x1));
+  Act<T>::store(p + 2, fmaf(an, r1 * co1, x2));
+  Act<T>::store(p + 3, fmaf(an, r1 * s1, x3));
+}
+
+template <typename T>
+static hipError_t noise_dispatch(T* v, int64_t row_stride, const SeqTable& st, int hkv, int dh, int layer,
+                                 float alpha, uint64_t seed, int ph, int pt, hipStream_t s) {
+  const int64_t n_vec = (int64_t)st.rows * hkv;
+  const uint32_t k0 = (uint32_t)(seed & 0xffffffffu), k1 = (uint32_t)(seed >> 32);
+  const int tpv = dh / 4;
+  const int64_t blocks = (n_vec * tpv + 255) / 256;
+  if (blocks <= 0) return hipSuccess;
+  switch (tpv) {
+    case 8:  value_noise_kernel<T, 8><<<(unsigned)blocks, 256, 0, s>>>(v, row_stride, st, hkv, layer, alpha, k0, k1, ph, pt); break;
+    case 16: value_noise_kernel<T, 16><<<(unsigned)blocks, 256, 0, s>>>(v, row_stride, st, hkv, layer, alpha, k0, k1, ph, pt); break;
+    case 32: value_noise_kernel<T, 32><<<(unsigned)blocks, 256, 0, s>>>(v, row_stride, st, hkv, layer, alpha, k0, k1, ph, pt); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_value_noise(void* v, bool bf16, int64_t row_stride, const SeqTable& st, int n_kv_heads,
+                              int head_dim, int layer, float alpha, uint64_t seed, int protect_head,
+                              int protect_tail, hipStream_t s) {
+  if (bf16)
+    return noise_dispatch<bf16_t>((bf16_t*)v, row_stride, st, n_kv_heads, head_dim, layer, alpha, seed,
+                                  protect_head, protect_tail, s);
+  return noise_dispatch<float>((float*)v, row_stride, st, n_kv_heads, head_dim, layer, alpha, seed, protect_head,
+                               protect_tail, s);
+}
+
+// --------------------------------------------------------------------------- means
+// d[g * n + k] = mean of kl[g * kl_stride + r] for r in [off[k] + window_start, off[k+1]);
+// 0 for an empty window.  Fixed-order double accumulation.
+__global__ __launch_bounds__(256) void window_mean_kernel(const float* __restrict__ kl, int64_t kl_stride,
+                                                          SeqTable st, int window_start, float* __restrict__ d) {
+  const int k = blockIdx.x, g = blockIdx.y;
+  const int r0 = st.off[k] + window_start, r1 = st.off[k + 1];
+  __shared__ double part[256];
+  double acc = 0.0;
+  for (int r = r0 + (int)threadIdx.x; r < r1; r += 256) acc += (double)kl[(int64_t)g * kl_stride + r];
+  part[threadIdx.x] = acc;
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if ((int)threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) d[g * st.n + k] = r1 > r0 ? (float)(part[0] / (double)(r1 - r0)) : 0.0f;
+}
+
+hipError_t launch_window_mean(const float* kl, int64_t kl_stride, int G, const SeqTable& st, int window_start,
+                              float* d, hipStream_t s) {
+  window_mean_kernel<<<dim3(st.n, G), 256, 0, s>>>(kl, kl_stride, st, window_start, d);
+  return hipGetLastError();
+}
+
+// One thread per pass of the group: copies the batch's d values to the caller's
+// d matrix and adds their sum (in sequence order) to the profile accumulator.
+__global__ void accumulate_kernel(const float* __restrict__ dbatch, int n_seqs, PassMap pm, float* __restrict__ d_out,
+                                  double* __restrict__ s_acc) {
+  const int g = threadIdx.x;
+  if (g >= pm.G) return;
+  double acc = 0.0;
+  for (int k = 0; k < n_seqs; ++k) {
+    const float x = dbatch[g * n_seqs + k];
+    acc += (double)x;
+    if (d_out) d_out[pm.d_base[g] + (int64_t)(pm.seq_index0 + k) * pm.d_seq_stride] = x;
+  }
+  s_acc[pm.s_index[g]] += acc;
+}
+
+hipError_t launch_accumulate(const float* dbatch, int n_seqs, const PassMap& pm, float* d_out, double* s_acc,
+                             hipStream_t s) {
+  accumulate_kernel<<<1, 64, 0, s>>>(dbatch, n_seqs, pm, d_out, s_acc);
+  return hipGetLastError();
+}
+
+__global__ void finalize_kernel(const double* __restrict__ s_acc, int n, double inv_n, float* __restrict__ s_out) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+    s_out[i] = (float)(s_acc[i] * inv_n);
+}
+
+__global__ void zero_f64_kernel(double* p, int n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0.0;
+}
+
+hipError_t launch_finalize(const double* s_acc, int n, double inv_n, float* s_out, hipStream_t s) {
+  finalize_kernel<<<(n + 255) / 256, 256, 0, s>>>(s_acc, n, inv_n, s_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_f64(double* p, int n, hipStream_t s) {
+  zero_f64_kernel<<<(n + 255) / 256, 256, 0, s>>>(p, n);
+  return hipGetLastError();
+}
+
+}  // namespace rk

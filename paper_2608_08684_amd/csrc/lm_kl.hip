@@ -1,0 +1,310 @@
+// LM head + log-softmax + KL (Algorithm 1, WindowKL; Eq. sample-response).
+//
+// KL_t = sum_v P_v (log P_v - log Q_v) with P = softmax(a), Q = softmax(b),
+// a = x_clean W^T, b = x_pert W^T.  With delta = a - b and A_t = logsumexp(a):
+//   KL_t = sum_v p_v f(delta_v) - g(S_t),   p_v = exp(a_v - A_t),
+//   f(x) = x + expm1(-x) >= 0,  S_t = sum_v p_v expm1(-delta_v),  g(y) = y - log1p(y) >= 0.
+// Both sums have non-negative, cancellation-free terms (f and g use series near
+// 0), so a KL of 1e-6 nats survives fp32 accumulation; delta = 0 gives exactly 0.
+//
+// Fused path (bf16): logits never reach HBM.  The clean pass runs lm_lse once per
+// batch (A_t).  lm_kl then computes, per 128-token x 128-vocab tile, the clean
+// logits once and the logits of G perturbed passes against the same W tile, and
+// folds each into per-lane (F, S) partials.  The tile is computed transposed
+// (vocab rows = MFMA M, tokens = MFMA N), so a lane owns one token and all its
+// vocab reductions are lane-local.  Vocab is split into chunks across
+// workgroups; a fixed-order merge kernel combines the chunk partials.
+// Unfused path (any dtype): KL over two materialised fp32 logit tensors.
+#include <math.h>
+
+#include "rk_internal.h"
+
+namespace rk {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// f(x) = x + expm1(-x) = x^2/2 - x^3/6 + ...  (>= 0)
+__device__ __forceinline__ float kl_f(float x) {
+  if (fabsf(x) < 0.25f) {
+    float p = x * (1.0f / 40320.0f) - (1.0f / 5040.0f);
+    p = fmaf(p, x, 1.0f / 720.0f);
+    p = fmaf(p, x, -1.0f / 120.0f);
+    p = fmaf(p, x, 1.0f / 24.0f);
+    p = fmaf(p, x, -1.0f / 6.0f);
+    p = fmaf(p, x, 0.5f);
+    return p * x * x;
+  }
+  return (expf(-fmaxf(x, -80.0f)) - 1.0f) + x;
+}
+
+// --------------------------------------------------------------------------- shared tile GEMM
+// acc[vb] (vb = 0..3) = W[v0 + 32 vb + ..] . X[t0 + 32 w + l32]: the 128 x 128 logit
+// tile, transposed, wave w owning tokens 32w..32w+31.  Rows of X past `rows` are
+// clamped (their results are discarded).  Leaves LDS free on return.
+__device__ __forceinline__ void logit_tile(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int v0,
+                                           int t0, int rows, int d, v4u* As, v4u* Bs, f32x16_t acc[4]) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31;
+  const v4u* ga[4];
+  const v4u* gb[4];
+  int so[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
+    ga[i] = reinterpret_cast<const v4u*>(W + (int64_t)(v0 + row) * d) + kc;
+    gb[i] = reinterpret_cast<const v4u*>(X + (int64_t)min(t0 + row, rows - 1) * d) + kc;
+    so[i] = row * 8 + (kc ^ (row & 7));
+  }
+#pragma unroll
+  for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[vb][i] = 0.f;
+  const int nk = d / 64;
+  v4u ra[4], rb[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { ra[i] = ga[i][0]; rb[i] = gb[i][0]; }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { As[so[i]] = ra[i]; Bs[so[i]] = rb[i]; }
+  __syncthreads();
+  const int trow = w * 32 + l32;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) { ra[i] = ga[i][(kt + 1) * 8]; rb[i] = gb[i][(kt + 1) * 8]; }
+    }
+    const v4u* Ab = As + buf * 1024;
+    const v4u* Bb = Bs + buf * 1024;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int ch = ks * 2 + (lane >> 5);
+      const bf16x8_t bx = __builtin_bit_cast(bf16x8_t, Bb[trow * 8 + (ch ^ (trow & 7))]);
+#pragma unroll
+      for (int vb = 0; vb < 4; ++vb) {
+        const int vrow = vb * 32 + l32;
+        const bf16x8_t aw = __builtin_bit_cast(bf16x8_t, Ab[vrow * 8 + (ch ^ (vrow & 7))]);
+        acc[vb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aw, bx, acc[vb], 0, 0, 0);
+      }
+    }
+    if (kt + 1 < nk) {
+      const int nb = (kt + 1) & 1;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) { As[nb * 1024 + so[i]] = ra[i]; Bs[nb * 1024 + so[i]] = rb[i]; }
+    }
+    __syncthreads();
+  }
+}
+
+// --------------------------------------------------------------------------- clean log-sum-exp
+__global__ __launch_bounds__(256) void lm_lse_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W,
+                                                     int rows, int d, int n_vt, int vt_per_chunk,
+                                                     float2* __restrict__ part) {
+  __shared__ __attribute__((aligned(16))) v4u smem[4096];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int t0 = blockIdx.x * 128, chunk = blockIdx.y;
+  const int vt0 = chunk * vt_per_chunk, vt1 = min(n_vt, vt0 + vt_per_chunk);
+  float m = -INFINITY, z = 0.f;
+  f32x16_t acc[4];
+  for (int vt = vt0; vt < vt1; ++vt) {
+    logit_tile(W, X, vt * 128, t0, rows, d, smem, smem + 2048, acc);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, acc[vb][i]);
+    const float m_new = fmaxf(m, mx);
+    float sum = 0.f;
+#pragma unroll
+    for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) sum += expf(acc[vb][i] - m_new);
+    z = z * expf(m - m_new) + sum;
+    m = m_new;
+  }
+  // merge the two half-waves that share a token
+  const float m2 = __shfl_xor(m, 32, 64), z2 = __shfl_xor(z, 32, 64);
+  const float mm = fmaxf(m, m2);
+  const float zz = (mm == -INFINITY) ? 0.f : z * expf(m - mm) + z2 * expf(m2 - mm);
+  const int token = t0 + w * 32 + (lane & 31);
+  if ((lane >> 5) == 0 && token < rows) part[(int64_t)chunk * rows + token] = make_float2(mm, zz);
+}
+
+__global__ void lse_merge_kernel(const float2* __restrict__ part, int n_chunks, int rows, float* __restrict__ lse) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= rows) return;
+  float M = -INFINITY;
+  for (int c = 0; c < n_chunks; ++c) M = fmaxf(M, part[(int64_t)c * rows + r].x);
+  double z = 0.0;
+  for (int c = 0; c < n_chunks; ++c) {
+    const float2 p = part[(int64_t)c * rows + r];
+    if (p.y > 0.f) z += (double)p.y * exp((double)p.x - (double)M);
+  }
+  lse[r] = (float)((double)M + log(z));
+}
+
+// --------------------------------------------------------------------------- fused KL
+template <int GMAX>
+__global__ __launch_bounds__(256) void lm_kl_kernel(const bf16_t* __restrict__ Xc, const bf16_t* __restrict__ Xp,
+                                                    int64_t pass_stride, int G, const bf16_t* __restrict__ W,
+                                                    int rows, int d, int n_vt, int vt_per_chunk,
+                                                    const float* __restrict__ lse, float2* __restrict__ part) {
+  __shared__ __attribute__((aligned(16))) v4u smem[4096];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int t0 = blockIdx.x * 128, chunk = blockIdx.y;
+  const int vt0 = chunk * vt_per_chunk, vt1 = min(n_vt, vt0 + vt_per_chunk);
+  const int token = t0 + w * 32 + (lane & 31);
+  const float A = lse[min(token, rows - 1)];
+  float Fa[GMAX], Sa[GMAX];
+#pragma unroll
+  for (int g = 0; g < GMAX; ++g) { Fa[g] = 0.f; Sa[g] = 0.f; }
+  f32x16_t a[4], p[4], b[4];
+  for (int vt = vt0; vt < vt1; ++vt) {
+    logit_tile(W, Xc, vt * 128, t0, rows, d, smem, smem + 2048, a);
+#pragma unroll
+    for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) p[vb][i] = expf(a[vb][i] - A);
+    for (int g = 0; g < G; ++g) {
+      logit_tile(W, Xp + (int64_t)g * pass_stride, vt * 128, t0, rows, d, smem, smem + 2048, b);
+      float fs = 0.f, ss = 0.f;
+#pragma unroll
+      for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float dl = a[vb][i] - b[vb][i];
+          const float f = kl_f(dl);
+          fs = fmaf(p[vb][i], f, fs);
+          ss = fmaf(p[vb][i], f - dl, ss);
+        }
+#pragma unroll
+      for (int j = 0; j < GMAX; ++j)
+        if (j == g) { Fa[j] += fs; Sa[j] += ss; }
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < GMAX; ++g) {
+    if (g < G) {
+      const float F = Fa[g] + __shfl_xor(Fa[g], 32, 64);
+      const float S = Sa[g] + __shfl_xor(Sa[g], 32, 64);
+      if ((lane >> 5) == 0 && token < rows) part[((int64_t)chunk * G + g) * rows + token] = make_float2(F, S);
+    }
+  }
+}
+
+// kl[g * rows + r] = sum_c F - g(sum_c S), fixed chunk order, double.
+__global__ void kl_merge_kernel(const float2* __restrict__ part, int n_chunks, int G, int rows, float* __restrict__ kl) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x, g = blockIdx.y;
+  if (r >= rows) return;
+  double F = 0.0, S = 0.0;
+  for (int c = 0; c < n_chunks; ++c) {
+    const float2 v = part[((int64_t)c * G + g) * rows + r];
+    F += v.x;
+    S += v.y;
+  }
+  kl[(int64_t)g * rows + r] = (float)(F - (S - log1p(S)));
+}
+
+int lm_chunks(int rows, int vocab) {
+  const int n_vt = vocab / 128, n_tt = (rows + 127) / 128;
+  int chunks = (2048 + n_tt - 1) / n_tt;
+  if (chunks > n_vt) chunks = n_vt;
+  if (chunks < 1) chunks = 1;
+  const int per = (n_vt + chunks - 1) / chunks;
+  return (n_vt + per - 1) / per;
+}
+
+static int vt_per_chunk(int vocab, int chunks) {
+  const int n_vt = vocab / 128;
+  return (n_vt + chunks - 1) / chunks;
+}
+
+hipError_t launch_lm_lse(const bf16_t* x, const bf16_t* W, int rows, int d, int vocab, float2* part, float* lse,
+                         hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  const int chunks = lm_chunks(rows, vocab);
+  dim3 grid((rows + 127) / 128, chunks);
+  lm_lse_kernel<<<grid, 256, 0, s>>>(x, W, rows, d, vocab / 128, vt_per_chunk(vocab, chunks), part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  lse_merge_kernel<<<(rows + 255) / 256, 256, 0, s>>>(part, chunks, rows, lse);
+  return hipGetLastError();
+}
+
+hipError_t launch_lm_kl(const bf16_t* xc, const bf16_t* xp, int64_t pass_stride, int G, const bf16_t* W, int rows,
+                        int d, int vocab, const float* lse, float2* part, float* kl, hipStream_t s) {
+  if (rows <= 0 || G <= 0) return hipSuccess;
+  const int chunks = lm_chunks(rows, vocab);
+  dim3 grid((rows + 127) / 128, chunks);
+  const int vpc = vt_per_chunk(vocab, chunks);
+  if (G <= 4)
+    lm_kl_kernel<4><<<grid, 256, 0, s>>>(xc, xp, pass_stride, G, W, rows, d, vocab / 128, vpc, lse, part);
+  else if (G <= 8)
+    lm_kl_kernel<8><<<grid, 256, 0, s>>>(xc, xp, pass_stride, G, W, rows, d, vocab / 128, vpc, lse, part);
+  else if (G <= RK_MAX_GROUP)
+    lm_kl_kernel<RK_MAX_GROUP><<<grid, 256, 0, s>>>(xc, xp, pass_stride, G, W, rows, d, vocab / 128, vpc, lse, part);
+  else
+    return hipErrorInvalidValue;
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  kl_merge_kernel<<<dim3((rows + 255) / 256, G), 256, 0, s>>>(part, chunks, G, rows, kl);
+  return hipGetLastError();
+}
+
+// --------------------------------------------------------------------------- unfused KL
+// One workgroup per (row, pass): two sweeps over the clean row (max, then sum of
+// exp) and one over both rows for F and S.  Fixed-order block reductions.
+__device__ __forceinline__ double block_sum(double v, double* red) {
+  red[threadIdx.x] = v;
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  const double r = red[0];
+  __syncthreads();
+  return r;
+}
+
+__global__ __launch_bounds__(256) void kl_logits_kernel(const float* __restrict__ lc, const float* __restrict__ lp,
+                                                        int64_t pass_stride, int rows, int vocab,
+                                                        float* __restrict__ kl) {
+  __shared__ double red[256];
+  __shared__ float redf[256];
+  const int r = blockIdx.x, g = blockIdx.y;
+  const float* a = lc + (int64_t)r * vocab;
+  const float* b = lp + (int64_t)g * pass_stride + (int64_t)r * vocab;
+  float mx = -INFINITY;
+  for (int v = threadIdx.x; v < vocab; v += 256) mx = fmaxf(mx, a[v]);
+  redf[threadIdx.x] = mx;
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if ((int)threadIdx.x < w) redf[threadIdx.x] = fmaxf(redf[threadIdx.x], redf[threadIdx.x + w]);
+    __syncthreads();
+  }
+  mx = redf[0];
+  __syncthreads();
+  double z = 0.0;
+  for (int v = threadIdx.x; v < vocab; v += 256) z += (double)expf(a[v] - mx);
+  z = block_sum(z, red);
+  const float A = (float)((double)mx + log(z));
+  double F = 0.0, S = 0.0;
+  for (int v = threadIdx.x; v < vocab; v += 256) {
+    const float p = expf(a[v] - A);
+    const float dl = a[v] - b[v];
+    const float f = kl_f(dl);
+    F += (double)(p * f);
+    S += (double)(p * (f - dl));
+  }
+  F = block_sum(F, red);
+  S = block_sum(S, red);
+  if (threadIdx.x == 0) kl[(int64_t)g * rows + r] = (float)(F - (S - log1p(S)));
+}
+
+hipError_t launch_kl_logits(const float* lc, const float* lp, int64_t pass_stride, int G, int rows, int vocab,
+                            float* kl, hipStream_t s) {
+  if (rows <= 0 || G <= 0) return hipSuccess;
+  kl_logits_kernel<<<dim3(rows, G), 256, 0, s>>>(lc, lp, pass_stride, rows, vocab, kl);
+  return hipGetLastError();
+}
+
+}  // namespace rk

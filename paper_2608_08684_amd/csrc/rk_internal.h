@@ -1,0 +1,127 @@
+// Internal declarations shared by the HIP kernels and the host scheduler.
+// Everything here is private to librk; the public surface is include/rk.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "rk.h"
+
+namespace rk {
+
+typedef uint16_t bf16_t;  // raw bf16 bit pattern in memory
+// 16-byte native vector (promotes to registers, unlike HIP's union-based uint4)
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+
+// Row layout of one batch: sequence k owns rows [off[k], off[k+1]).  Passed to
+// kernels by value (fits easily in the kernel-argument segment).
+struct SeqTable {
+  int32_t n;            // sequences in the batch
+  int32_t seq_index0;   // calibration index of sequence 0 (keys the noise)
+  int32_t max_len;      // longest sequence of the batch
+  int32_t rows;         // off[n]
+  int32_t off[RK_MAX_BATCH_SEQS + 1];
+};
+
+// Work list of the attention kernel: q-blocks of all sequences, flattened.
+struct AttnWork {
+  int32_t total;                         // number of (sequence, q-block) items
+  int32_t cum[RK_MAX_BATCH_SEQS + 1];    // cum[k] = q-blocks of sequences < k
+};
+
+// --------------------------------------------------------------------------- device helpers
+#if defined(__HIPCC__)
+__device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// fp32 -> bf16, round to nearest even (NaN -> quiet NaN).
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)0x7fc0;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+__device__ __forceinline__ int seq_of_row(const SeqTable& st, int r) {
+  int lo = 0, hi = st.n - 1;
+  while (lo < hi) {  // largest k with off[k] <= r
+    int mid = (lo + hi + 1) >> 1;
+    if (st.off[mid] <= r) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+template <typename T> struct Act;
+template <> struct Act<float> {
+  static __device__ __forceinline__ float load(const float* p) { return *p; }
+  static __device__ __forceinline__ void store(float* p, float v) { *p = v; }
+};
+template <> struct Act<bf16_t> {
+  static __device__ __forceinline__ float load(const bf16_t* p) { return bf2f(*p); }
+  static __device__ __forceinline__ void store(bf16_t* p, float v) { *p = f2bf(v); }
+};
+#endif
+
+// --------------------------------------------------------------------------- launchers
+// Each returns hipSuccess or the launch error.  `act_bf16` selects the element type
+// of activation buffers (bf16 when true, fp32 otherwise).
+
+hipError_t launch_embed(const void* emb, bool emb_bf16, const int32_t* tokens, float* h, int rows, int d,
+                        hipStream_t s);
+hipError_t launch_rmsnorm(const float* h, const float* g, void* out, bool out_bf16, int rows, int d,
+                          float eps, hipStream_t s);
+hipError_t launch_rope_table(float2* tab, int max_len, int head_dim, float theta, hipStream_t s);
+hipError_t launch_value_noise(void* v, bool bf16, int64_t row_stride, const SeqTable& st, int n_kv_heads,
+                              int head_dim, int layer, float alpha, uint64_t seed, int protect_head,
+                              int protect_tail, hipStream_t s);
+
+// GEMM family: C[M, N] = A[M, K] * B[N, K]^T with a fused epilogue.
+enum class Epi { kStoreRope, kResidual, kSwiGLU, kStoreF32 };
+struct GemmArgs {
+  const void* A; int64_t lda;
+  const void* B; int64_t ldb;
+  int M, N, K;           // N = columns of B used (for kSwiGLU: 2 * d_ff)
+  Epi epi;
+  void* out; int64_t ldo;         // output (act type, or fp32 for kResidual/kStoreF32)
+  const float* res; int64_t ldr;  // kResidual: out = res + C (res may alias out)
+  // kStoreRope: columns < rope_cols are rotated with the table (pairs j, j + head_dim/2)
+  int rope_cols; int head_dim; const float2* rope_tab; SeqTable seq;
+  int d_ff;                        // kSwiGLU: gate rows [0, d_ff), up rows [d_ff, 2 d_ff)
+};
+hipError_t launch_gemm(const GemmArgs& a, bool bf16, hipStream_t s);
+
+hipError_t launch_attention(const void* qkv, int64_t ldq, void* out, int64_t ldo, const SeqTable& st,
+                            int n_heads, int n_kv_heads, int head_dim, bool bf16, hipStream_t s);
+
+// Clean log-sum-exp of the LM head, fused (bf16): lse[r] = logsumexp_v (x[r] . W[v]).
+int lm_chunks(int rows, int vocab);
+hipError_t launch_lm_lse(const bf16_t* x, const bf16_t* W, int rows, int d, int vocab, float2* part,
+                         float* lse, hipStream_t s);
+// Fused LM head + KL (bf16): for pass g, kl[g][r] = KL(softmax(x_c W^T) || softmax(x_g W^T)).
+hipError_t launch_lm_kl(const bf16_t* xc, const bf16_t* xp, int64_t pass_stride, int G, const bf16_t* W,
+                        int rows, int d, int vocab, const float* lse, float2* part, float* kl,
+                        hipStream_t s);
+// Unfused KL over materialised fp32 logits: kl[g][r] = KL(softmax(lc[r]) || softmax(lp[g][r])).
+hipError_t launch_kl_logits(const float* lc, const float* lp, int64_t pass_stride, int G, int rows, int vocab,
+                            float* kl, hipStream_t s);
+
+// dbatch[g * n_seqs + k] = mean of kl[g * kl_stride + r] over r in [off[k] + window_start, off[k+1]).
+hipError_t launch_window_mean(const float* kl, int64_t kl_stride, int G, const SeqTable& st, int window_start,
+                              float* dbatch, hipStream_t s);
+
+// Where the d values of a group of passes go: pass g of the group writes
+// d_out[d_base[g] + seq * d_seq_stride] and accumulates into s_acc[s_index[g]].
+#define RK_MAX_GROUP 16
+struct PassMap {
+  int32_t G;
+  int32_t seq_index0;
+  int64_t d_seq_stride;
+  int64_t d_base[RK_MAX_GROUP];
+  int32_t s_index[RK_MAX_GROUP];
+};
+hipError_t launch_accumulate(const float* dbatch, int n_seqs, const PassMap& pm, float* d_out, double* s_acc,
+                             hipStream_t s);
+hipError_t launch_finalize(const double* s_acc, int n, double inv_n, float* s_out, hipStream_t s);
+hipError_t launch_zero_f64(double* p, int n, hipStream_t s);
+
+}  // namespace rk

@@ -1,0 +1,110 @@
+"""Shared plumbing of the GPU tests: upload fixture weights, run the library.
+
+Inputs come from ``fixtures`` only; expected values come from ``oracle`` only.
+"""
+from __future__ import annotations
+
+import os
+import sys
+
+import numpy as np
+
+import fixtures as F
+
+
+def log(msg: str):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def upload_weights(cfg, W: dict):
+    """fixtures.make_weights(cfg) output (bf16 bits or fp32) -> dict of cuda tensors."""
+    import torch
+    dev = torch.device("cuda")
+
+    def up(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).to(dev)
+        return torch.from_numpy(a.astype(np.float32, copy=False)).to(dev)
+
+    out = {"tok_emb": up(W["tok_emb"]), "lm_head": up(W["lm_head"]), "final_norm": up(W["final_norm"])}
+    for k in ("w_qkv", "w_o", "w_gate_up", "w_down", "attn_norm", "mlp_norm"):
+        out[k] = [up(x) for x in W[k]]
+    return out
+
+
+def f32_weights(cfg, W: dict) -> dict:
+    """Exact fp32 view of the weights for the oracle (bf16 bits upcast)."""
+    def cv(a):
+        if a is None:
+            return None
+        return F.bf16_to_f32(a) if a.dtype == np.uint16 else a
+    out = {k: cv(W[k]) for k in ("tok_emb", "lm_head", "final_norm")}
+    for k in ("w_qkv", "w_o", "w_gate_up", "w_down", "attn_norm", "mlp_norm"):
+        out[k] = [cv(x) for x in W[k]]
+    return out
+
+
+def make_batch(token_seqs, seq_index0: int = 0):
+    import torch
+    import paper_2608_08684_amd as rk
+    offs = np.zeros(len(token_seqs) + 1, dtype=np.int64)
+    offs[1:] = np.cumsum([len(t) for t in token_seqs])
+    toks = torch.from_numpy(np.concatenate(token_seqs).astype(np.int32)).cuda()
+    return rk.Batch(toks, offs, seq_index0)
+
+
+def empty_bytes(n: int):
+    import torch
+    return torch.empty(max(int(n), 1), dtype=torch.uint8, device="cuda")
+
+
+class Runner:
+    """A model on the GPU plus the buffers to run single-layer profiles."""
+
+    def __init__(self, cfg, W: dict):
+        import paper_2608_08684_amd as rk
+        self.cfg = cfg
+        self.dw = upload_weights(cfg, W)
+        self.model = rk.Model(cfg, self.dw)
+
+    def clean(self, batch):
+        cs = empty_bytes(self.model.clean_state_size(batch.rows))
+        ws = empty_bytes(self.model.workspace_size(batch.rows, 1, 0))
+        self.model.reference_forward(batch, cs, ws)
+        return cs
+
+    def layer(self, batch, cs, layer, alpha, want_logits=False, want_kl=True, **kw):
+        import torch
+        import paper_2608_08684_amd as rk
+        flags = kw.pop("flags", 0)
+        unfused = want_logits or (flags & rk.RK_FLAG_UNFUSED_KL) or self.cfg.dtype == "f32"
+        ws = empty_bytes(self.model.workspace_size(batch.rows, 1, rk.RK_FLAG_UNFUSED_KL if unfused else 0))
+        d = torch.empty(batch.n_seqs, dtype=torch.float32, device="cuda")
+        kl = torch.empty(batch.rows, dtype=torch.float32, device="cuda") if want_kl else None
+        lg = torch.empty(batch.rows, self.cfg.vocab, dtype=torch.float32, device="cuda") if want_logits else None
+        self.model.profile_layer(batch, layer, alpha, cs, d, ws, kl_pos=kl, logits_out=lg, flags=flags, **kw)
+        torch.cuda.synchronize()
+        return (d.cpu().numpy().astype(np.float64), None if kl is None else kl.cpu().numpy().astype(np.float64),
+                None if lg is None else lg.cpu().numpy())
+
+    def profile(self, batch, layers, alphas, max_rows=None, max_group=16, want_d=True, **kw):
+        import torch
+        import paper_2608_08684_amd as rk
+        max_rows = max_rows or batch.rows
+        flags = kw.get("flags", 0)
+        ws = empty_bytes(self.model.workspace_size(max_rows, max_group, rk.RK_WS_CLEAN_STATE | (flags & rk.RK_FLAG_UNFUSED_KL)))
+        s = torch.empty(len(alphas), len(layers), dtype=torch.float32, device="cuda")
+        d = torch.empty(len(alphas), batch.n_seqs, len(layers), dtype=torch.float32, device="cuda") if want_d else None
+        self.model.sensitivity_profile(batch, layers, alphas, s, ws, max_rows, max_group, d_out=d, **kw)
+        torch.cuda.synchronize()
+        return s.cpu().numpy().astype(np.float64), (None if d is None else d.cpu().numpy().astype(np.float64))
+
+
+def gpu_available() -> bool:
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:
+        return False
