@@ -220,6 +220,18 @@ rk_status rk_perturb_values(const rk_model *m, const rk_batch *batch, int32_t la
 rk_status rk_layer_budgets(const double *s, int32_t n, int64_t B, double r, double gamma, double eps,
                            rk_rounding mode, double *w_out, int64_t *b_out);
 
+/* ---------------------------------------------------------------- diagnostics */
+
+/* Per-kernel timing for measurement: after rk_timing_begin(family) every launch
+ * of that kernel family is bracketed by HIP events recorded on its launch stream
+ * (families: "rmsnorm", "gemm_qkv", "noise", "attention", "gemm_o",
+ * "gemm_gate_up", "gemm_down", "lm_lse", "lm_kl", "kl_logits", "lm_logits").
+ * rk_timing_end waits for the recorded events, returns the number of launches
+ * and their summed duration in milliseconds, and stops recording.  Host-side
+ * state is process-wide; not for concurrent use from several threads.          */
+rk_status rk_timing_begin(const char *family);
+rk_status rk_timing_end(int64_t *launches, double *total_ms);
+
 /* Message of the last error on the calling thread ("" if none). */
 const char *rk_last_error(void);
 

@@ -25,7 +25,7 @@ from typing import Optional, Sequence
 
 import numpy as np
 
-__all__ = ["RKError", "load", "Model", "Batch", "layer_budgets", "LIB_PATH", "RK_FLAG_FULL_RECOMPUTE",
+__all__ = ["RKError", "load", "Model", "Batch", "layer_budgets", "timing_begin", "timing_end", "LIB_PATH", "RK_FLAG_FULL_RECOMPUTE",
            "RK_FLAG_UNFUSED_KL", "RK_WS_CLEAN_STATE", "RK_MAX_BATCH_SEQS", "RK_MAX_GROUP"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librk.so")
@@ -103,6 +103,8 @@ def load() -> ctypes.CDLL:
         "rk_layer_budgets": (st, [ctypes.POINTER(f64), i32, i64, f64, f64, f64, ctypes.c_int, ctypes.POINTER(f64),
                                   ctypes.POINTER(i64)]),
         "rk_last_error": (ctypes.c_char_p, []),
+        "rk_timing_begin": (st, [ctypes.c_char_p]),
+        "rk_timing_end": (st, [ctypes.POINTER(i64), ctypes.POINTER(f64)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -229,6 +231,19 @@ class Model:
         p = _params(seed, 0, protect_head, protect_tail, 0)
         _check(load().rk_perturb_values(self._h, ctypes.byref(batch._c), int(layer), float(alpha), ctypes.byref(p),
                                         _ptr(v), int(row_stride), _stream(stream)))
+
+
+def timing_begin(family: str):
+    """rk_timing_begin: bracket every launch of one kernel family with HIP events."""
+    _check(load().rk_timing_begin(family.encode()))
+
+
+def timing_end():
+    """rk_timing_end: (launches, total milliseconds) since timing_begin."""
+    n = ctypes.c_int64()
+    ms = ctypes.c_double()
+    _check(load().rk_timing_end(ctypes.byref(n), ctypes.byref(ms)))
+    return int(n.value), float(ms.value)
 
 
 def layer_budgets(s: Sequence[float], B: int, r: float, gamma: float = 0.0, eps: float = 0.0,

@@ -136,6 +136,39 @@ static Clean clean_view(const rk_model* m, int64_t R, const void* base) {
   return Clean{(float*)(b + p.h), b + p.xf, (float*)(b + p.lse)};
 }
 
+// ----------------------------------------------------------------------------- timing
+// Event pairs around every launch of one kernel family (diagnostics only).
+struct Timing {
+  bool on = false;
+  std::string family;
+  std::vector<hipEvent_t> start, stop;
+  size_t used = 0;
+};
+static Timing g_timing;
+
+class Timed {
+ public:
+  Timed(const char* family, hipStream_t s) : s_(s) {
+    if (!g_timing.on || g_timing.family != family) return;
+    if (g_timing.used == g_timing.start.size()) {
+      hipEvent_t a, b;
+      if (hipEventCreate(&a) != hipSuccess) return;
+      if (hipEventCreate(&b) != hipSuccess) { (void)hipEventDestroy(a); return; }
+      g_timing.start.push_back(a);
+      g_timing.stop.push_back(b);
+    }
+    idx_ = (long)g_timing.used++;
+    (void)hipEventRecord(g_timing.start[idx_], s_);
+  }
+  ~Timed() {
+    if (idx_ >= 0) (void)hipEventRecord(g_timing.stop[idx_], s_);
+  }
+
+ private:
+  hipStream_t s_;
+  long idx_ = -1;
+};
+
 // ----------------------------------------------------------------------------- passes
 #define RK_TRY(expr)                                                       \
   do {                                                                     \
@@ -157,32 +190,36 @@ static rk_status run_block(const rk_model* m, int l, const float* h_in, float* h
                            const SeqTable& st, const Noise* noise, hipStream_t s) {
   const rk_model_config& c = m->cfg;
   const int R = st.rows, d = c.d_model;
-  RK_TRY(launch_rmsnorm(h_in, m->attn_norm[l], b.x, m->bf16, R, d, c.rms_eps, s));
+  { Timed t("rmsnorm", s); RK_TRY(launch_rmsnorm(h_in, m->attn_norm[l], b.x, m->bf16, R, d, c.rms_eps, s)); }
   GemmArgs g{};
   g.A = b.x; g.lda = d; g.B = m->w_qkv[l]; g.ldb = d; g.M = R; g.N = m->qkv_cols; g.K = d;
   g.epi = Epi::kStoreRope; g.out = b.qkv; g.ldo = m->qkv_cols;
   g.rope_cols = (c.n_heads + c.n_kv_heads) * c.head_dim; g.head_dim = c.head_dim; g.rope_tab = b.rope; g.seq = st;
-  RK_TRY(launch_gemm(g, m->bf16, s));
+  { Timed t("gemm_qkv", s); RK_TRY(launch_gemm(g, m->bf16, s)); }
   if (noise) {
     char* v = (char*)b.qkv + (size_t)(c.n_heads + c.n_kv_heads) * c.head_dim * act_bytes(m);
+    Timed t("noise", s);
     RK_TRY(launch_value_noise(v, m->bf16, m->qkv_cols, st, c.n_kv_heads, c.head_dim, l, noise->alpha,
                               noise->p->seed, noise->p->protect_head, noise->p->protect_tail, s));
   }
-  RK_TRY(launch_attention(b.qkv, m->qkv_cols, b.att, m->attn_cols, st, c.n_heads, c.n_kv_heads, c.head_dim,
-                          m->bf16, s));
+  {
+    Timed t("attention", s);
+    RK_TRY(launch_attention(b.qkv, m->qkv_cols, b.att, m->attn_cols, st, c.n_heads, c.n_kv_heads, c.head_dim,
+                            m->bf16, s));
+  }
   g = GemmArgs{};
   g.A = b.att; g.lda = m->attn_cols; g.B = m->w_o[l]; g.ldb = m->attn_cols; g.M = R; g.N = d; g.K = m->attn_cols;
   g.epi = Epi::kResidual; g.out = h_out; g.ldo = d; g.res = h_in; g.ldr = d;
-  RK_TRY(launch_gemm(g, m->bf16, s));
-  RK_TRY(launch_rmsnorm(h_out, m->mlp_norm[l], b.x, m->bf16, R, d, c.rms_eps, s));
+  { Timed t("gemm_o", s); RK_TRY(launch_gemm(g, m->bf16, s)); }
+  { Timed t("rmsnorm", s); RK_TRY(launch_rmsnorm(h_out, m->mlp_norm[l], b.x, m->bf16, R, d, c.rms_eps, s)); }
   g = GemmArgs{};
   g.A = b.x; g.lda = d; g.B = m->w_gate_up[l]; g.ldb = d; g.M = R; g.N = 2 * c.d_ff; g.K = d;
   g.epi = Epi::kSwiGLU; g.out = b.ff; g.ldo = c.d_ff; g.d_ff = c.d_ff;
-  RK_TRY(launch_gemm(g, m->bf16, s));
+  { Timed t("gemm_gate_up", s); RK_TRY(launch_gemm(g, m->bf16, s)); }
   g = GemmArgs{};
   g.A = b.ff; g.lda = c.d_ff; g.B = m->w_down[l]; g.ldb = c.d_ff; g.M = R; g.N = d; g.K = c.d_ff;
   g.epi = Epi::kResidual; g.out = h_out; g.ldo = d; g.res = h_out; g.ldr = d;
-  RK_TRY(launch_gemm(g, m->bf16, s));
+  { Timed t("gemm_down", s); RK_TRY(launch_gemm(g, m->bf16, s)); }
   return RK_OK;
 }
 
@@ -198,8 +235,10 @@ static rk_status reference_forward(const rk_model* m, const int32_t* tokens, con
     if (e != RK_OK) return e;
   }
   RK_TRY(launch_rmsnorm(b.h, m->final_norm, cl.xf, m->bf16, (int)R, (int)d, c.rms_eps, s));
-  if (m->bf16)
+  if (m->bf16) {
+    Timed t("lm_lse", s);
     RK_TRY(launch_lm_lse((const bf16_t*)cl.xf, (const bf16_t*)m->lm_head, (int)R, (int)d, c.vocab, b.part, cl.lse, s));
+  }
   return RK_OK;
 }
 
@@ -236,6 +275,7 @@ static rk_status score_group(const rk_model* m, const SeqTable& st, const Clean&
   const rk_model_config& c = m->cfg;
   const int64_t R = st.rows, d = c.d_model;
   if (!unfused) {
+    Timed t("lm_kl", s);
     RK_TRY(launch_lm_kl((const bf16_t*)cl.xf, (const bf16_t*)xp, R * d, G, (const bf16_t*)m->lm_head, (int)R, (int)d,
                         c.vocab, cl.lse, b.part, kl, s));
     return RK_OK;
@@ -245,8 +285,10 @@ static rk_status score_group(const rk_model* m, const SeqTable& st, const Clean&
     a.A = (const char*)xp + (size_t)g * R * d * act_bytes(m); a.lda = d; a.B = m->lm_head; a.ldb = d;
     a.M = (int)R; a.N = c.vocab; a.K = (int)d; a.epi = Epi::kStoreF32;
     a.out = lp + (size_t)g * R * c.vocab; a.ldo = c.vocab;
+    Timed t("lm_logits", s);
     RK_TRY(launch_gemm(a, m->bf16, s));
   }
+  Timed t("kl_logits", s);
   RK_TRY(launch_kl_logits(b.logits_c, lp, R * c.vocab, G, (int)R, c.vocab, kl, s));
   return RK_OK;
 }
@@ -311,6 +353,30 @@ using namespace rk;
 extern "C" {
 
 const char* rk_last_error(void) { return g_error.c_str(); }
+
+rk_status rk_timing_begin(const char* family) {
+  if (!family) { set_error("null family"); return RK_ERR_ARG; }
+  g_timing.on = true;
+  g_timing.family = family;
+  g_timing.used = 0;
+  return RK_OK;
+}
+
+rk_status rk_timing_end(int64_t* launches, double* total_ms) {
+  if (!launches || !total_ms) { set_error("null output"); return RK_ERR_ARG; }
+  double sum = 0.0;
+  for (size_t i = 0; i < g_timing.used; ++i) {
+    float ms = 0.f;
+    RK_TRY(hipEventSynchronize(g_timing.stop[i]));
+    RK_TRY(hipEventElapsedTime(&ms, g_timing.start[i], g_timing.stop[i]));
+    sum += ms;
+  }
+  *launches = (int64_t)g_timing.used;
+  *total_ms = sum;
+  g_timing.on = false;
+  g_timing.used = 0;
+  return RK_OK;
+}
 
 rk_status rk_model_create(const rk_model_config* cfg, const rk_model_weights* w, rk_model** out) {
   if (!cfg || !w || !out) { set_error("rk_model_create: null argument"); return RK_ERR_ARG; }

@@ -1,0 +1,72 @@
+"""GPU parity at the benchmark's full size, on sampled outputs.
+
+The GPT-2-small-shaped workload (12 layers, d 768, 8 x 2048 Zipf tokens, alpha
+in {0.05, 0.1}) runs through rk_sensitivity_profile in the same launch
+configuration the benchmark times (all sequences in one batch, 12 passes per
+LM-head launch).  The oracle recomputes sampled cells d_{i,l} one by one;
+properties that hold at any size (alpha = 0 gives exactly 0, repeatability,
+identical budgets from the same profile) are checked on the whole output.
+"""
+import numpy as np
+import pytest
+
+import fixtures as F
+from oracle import budgets as OB
+from oracle import model as OM
+from oracle import profile as OPR
+
+from gpu_helpers import Runner, f32_weights, log, make_batch
+
+pytestmark = pytest.mark.gpu
+
+KL_REL, KL_ABS = 0.02, 1e-6
+
+
+@pytest.fixture(scope="module")
+def gpt2s():
+    w = F.get_workload("gpt2s-bf16")
+    W = F.make_weights(w.model)
+    run = Runner(w.model, W)
+    toks = F.make_tokens(w)
+    batch = make_batch(toks)
+    layers = list(range(w.model.n_layers))
+    s, d = run.profile(batch, layers, list(w.alphas), max_group=12)
+    return w, W, run, toks, batch, layers, s, d
+
+
+def test_gpt2s_sampled_cells_match_oracle(gpt2s):
+    w, W, run, toks, batch, layers, s, d = gpt2s
+    cfg = w.model
+    m = OM.Model(cfg, f32_weights(cfg, W), np.float32)
+    a = list(w.alphas).index(0.1)
+    for i, ls in ((0, (0, 11)), (5, (6,))):
+        st = OM.clean_pass(m, toks[i])
+        for l in ls:
+            ref, _ = OPR.profile_layer(m, st, toks[i], i, l, OPR.PerturbParams(0.1))
+            got = d[a, i, l]
+            err = abs(got - ref)
+            log(f"seq {i} layer {l}: gpu {got:.6e} oracle {ref:.6e} rel {err / abs(ref):.2e}")
+            assert err <= KL_REL * abs(ref) or err <= KL_ABS
+
+
+def test_gpt2s_whole_profile_properties(gpt2s):
+    import paper_2608_08684_amd as rk
+    w, W, run, toks, batch, layers, s, d = gpt2s
+    assert np.all(np.isfinite(s)) and np.all(d > 0)
+    assert np.allclose(s, d.mean(axis=1), rtol=1e-6)
+    # more noise, more divergence (every layer, every sequence)
+    assert np.all(d[1] > d[0])
+    # repeatable bit for bit, and alpha = 0 is exactly zero at full size
+    s2, d2 = run.profile(batch, layers, list(w.alphas), max_group=12)
+    assert np.array_equal(s2, s) and np.array_equal(d2, d)
+    s0, d0 = run.profile(batch, layers, [0.0], max_group=12)
+    assert np.all(s0 == 0.0) and np.all(d0 == 0.0)
+    # budgets from the GPU profile: C mapping == oracle mapping, sums preserved
+    T = max(w.lengths())
+    for a in range(len(w.alphas)):
+        for r in w.ratios:
+            for rho in (0.1, 0.2, 0.3):
+                B = int(round(rho * T * len(layers)))
+                _, bg = rk.layer_budgets(s[a], B, r)
+                _, bo = OB.layer_budgets(list(s[a]), B, r)
+                assert list(bg) == bo and sum(bo) == B
