@@ -7,8 +7,10 @@ can both consume it without sharing any of the method's code.
 
 Recipes (all deterministic across machines for a given numpy version):
 
-* weights: tensor ``k`` of a fixed enumeration is
-  ``default_rng([0, k]).standard_normal(shape, float32) * 0.02``; RMSNorm gains
+* weights: tensor ``k`` of a fixed enumeration is drawn in row blocks of
+  ``max(1, 2**24 // cols)`` rows; block ``b`` is
+  ``default_rng([0, k, b]).standard_normal((rows_b, cols), float32) * 0.02``
+  (blocks are independent, so large tensors draw in parallel).  RMSNorm gains
   are 1; there are no biases and the LM head is untied.  For bf16 models the
   fp32 draw is rounded to bf16 (round to nearest even) and both sides consume
   exactly those bits.
@@ -165,13 +167,22 @@ def weight_shapes(m: ModelConfig) -> List[tuple]:
     return out
 
 
-def _draw(k: int, shape: tuple, as_bf16: bool) -> np.ndarray:
-    w = np.random.default_rng([0, k]).standard_normal(shape, dtype=np.float32)
+_BLOCK = 1 << 24
+
+
+def _block_rows(shape: tuple) -> int:
+    return max(1, _BLOCK // int(shape[1]))
+
+
+def _draw_block(k: int, b: int, shape: tuple, out: np.ndarray, as_bf16: bool):
+    br = _block_rows(shape)
+    r0, r1 = b * br, min(shape[0], (b + 1) * br)
+    w = np.random.default_rng([0, k, b]).standard_normal((r1 - r0, shape[1]), dtype=np.float32)
     w *= np.float32(0.02)
-    return bf16_bits(w) if as_bf16 else w
+    out[r0:r1] = bf16_bits(w) if as_bf16 else w
 
 
-def make_weights(m: ModelConfig, *, bits: Optional[bool] = None, threads: int = 8,
+def make_weights(m: ModelConfig, *, bits: Optional[bool] = None, threads: int = 16,
                  layers: Optional[Sequence[int]] = None) -> dict:
     """Draw all weights.
 
@@ -188,19 +199,19 @@ def make_weights(m: ModelConfig, *, bits: Optional[bool] = None, threads: int = 
     specs = weight_shapes(m)
     want = set(range(m.n_layers)) if layers is None else set(layers)
 
-    def job(k):
-        name, l, shape = specs[k]
-        if l >= 0 and l not in want:
-            return k, None
-        w = _draw(k, shape, as_bf16)
-        if as_bf16 and not bits:
-            w = bf16_to_f32(w)
-        return k, w
-
     results = {}
+    jobs = []
+    for k, (name, l, shape) in enumerate(specs):
+        if l >= 0 and l not in want:
+            results[k] = None
+            continue
+        results[k] = np.empty(shape, dtype=np.uint16 if as_bf16 else np.float32)
+        nb = (shape[0] + _block_rows(shape) - 1) // _block_rows(shape)
+        jobs.extend((k, b) for b in range(nb))
     with ThreadPoolExecutor(max_workers=max(1, threads)) as ex:
-        for k, w in ex.map(job, range(len(specs))):
-            results[k] = w
+        list(ex.map(lambda kb: _draw_block(kb[0], kb[1], specs[kb[0]][2], results[kb[0]], as_bf16), jobs))
+    if as_bf16 and not bits:
+        results = {k: (None if v is None else bf16_to_f32(v)) for k, v in results.items()}
     out = {"w_qkv": [], "w_o": [], "w_gate_up": [], "w_down": []}
     for k, (name, l, shape) in enumerate(specs):
         if l < 0:

@@ -53,6 +53,10 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 static size_t act_bytes(const rk_model* m) { return m->bf16 ? 2 : 4; }
 
+// Buffers read as GEMM A operands hold whole 256-row tiles (the tile loads are
+// not clamped); rows past the batch are never stored.
+static int64_t pad_rows(int64_t R) { return (R + 255) / 256 * 256; }
+
 // ----------------------------------------------------------------------------- memory plans
 struct CleanPlan {
   size_t h, xf, lse, total;
@@ -63,14 +67,14 @@ static CleanPlan clean_plan(const rk_model* m, int64_t R) {
   CleanPlan p;
   size_t o = 0;
   p.h = o;   o += align256((size_t)m->cfg.n_layers * R * d * 4);
-  p.xf = o;  o += align256((size_t)R * d * act_bytes(m));
+  p.xf = o;  o += align256((size_t)pad_rows(R) * d * act_bytes(m));
   p.lse = o; o += align256((size_t)R * 4);
   p.total = o;
   return p;
 }
 
 struct WsPlan {
-  size_t h, x, qkv, att, ff, xp, part, logits_c, logits_p, kl, rope, dbatch, sacc, clean, total;
+  size_t h, x, qkv, att, ff, xp, part, logits_c, logits_p, kl, rope, rope_pos, dbatch, sacc, clean, total;
   bool unfused;
 };
 
@@ -83,11 +87,12 @@ static WsPlan ws_plan(const rk_model* m, int64_t R, int G, uint32_t flags) {
   p.unfused = !m->bf16 || (flags & RK_FLAG_UNFUSED_KL);
   size_t o = 0;
   p.h = o;        o += align256((size_t)R * c.d_model * 4);
-  p.x = o;        o += align256((size_t)R * c.d_model * a);
+  const int64_t Rp = pad_rows(R);
+  p.x = o;        o += align256((size_t)Rp * c.d_model * a);
   p.qkv = o;      o += align256((size_t)R * m->qkv_cols * a);
-  p.att = o;      o += align256((size_t)R * m->attn_cols * a);
-  p.ff = o;       o += align256((size_t)R * c.d_ff * a);
-  p.xp = o;       o += align256((size_t)G * R * c.d_model * a);
+  p.att = o;      o += align256((size_t)Rp * m->attn_cols * a);
+  p.ff = o;       o += align256((size_t)Rp * c.d_ff * a);
+  p.xp = o;       o += align256((size_t)G * Rp * c.d_model * a);
   p.part = o;
   if (m->bf16) {
     // chunks(rows) * rows <= min(n_vt * 128 * n_tt, (2048 + n_tt) * 128) for rows <= R
@@ -100,7 +105,8 @@ static WsPlan ws_plan(const rk_model* m, int64_t R, int G, uint32_t flags) {
   p.logits_p = o;
   if (p.unfused) o += align256((size_t)G * R * c.vocab * 4);
   p.kl = o;       o += align256((size_t)G * R * 4);
-  p.rope = o;     o += align256((size_t)R * (c.head_dim / 2) * 8);
+  p.rope = o;     o += align256((size_t)R * (c.head_dim / 2) * 8);   // max_len <= R positions
+  p.rope_pos = o; o += align256((size_t)R * 4);
   p.dbatch = o;   o += align256((size_t)G * RK_MAX_BATCH_SEQS * 4);
   p.sacc = o;     o += align256((size_t)kMaxSAcc * 8);
   p.clean = o;
@@ -112,7 +118,8 @@ static WsPlan ws_plan(const rk_model* m, int64_t R, int G, uint32_t flags) {
 // Device buffers of one batch, carved from the workspace.
 struct Bufs {
   float* h; void* x; void* qkv; void* att; void* ff; void* xp;
-  float2* part; float* logits_c; float* logits_p; float* kl; float2* rope; float* dbatch; double* sacc;
+  float2* part; float* logits_c; float* logits_p; float* kl; float2* rope; int32_t* rope_pos; float* dbatch;
+  double* sacc;
   char* clean;
 };
 
@@ -122,6 +129,7 @@ static Bufs carve(const WsPlan& p, void* ws) {
   u.h = (float*)(b + p.h); u.x = b + p.x; u.qkv = b + p.qkv; u.att = b + p.att; u.ff = b + p.ff;
   u.xp = b + p.xp; u.part = (float2*)(b + p.part); u.logits_c = (float*)(b + p.logits_c);
   u.logits_p = (float*)(b + p.logits_p); u.kl = (float*)(b + p.kl); u.rope = (float2*)(b + p.rope);
+  u.rope_pos = (int32_t*)(b + p.rope_pos);
   u.dbatch = (float*)(b + p.dbatch); u.sacc = (double*)(b + p.sacc); u.clean = b + p.clean;
   return u;
 }
@@ -194,7 +202,8 @@ static rk_status run_block(const rk_model* m, int l, const float* h_in, float* h
   GemmArgs g{};
   g.A = b.x; g.lda = d; g.B = m->w_qkv[l]; g.ldb = d; g.M = R; g.N = m->qkv_cols; g.K = d;
   g.epi = Epi::kStoreRope; g.out = b.qkv; g.ldo = m->qkv_cols;
-  g.rope_cols = (c.n_heads + c.n_kv_heads) * c.head_dim; g.head_dim = c.head_dim; g.rope_tab = b.rope; g.seq = st;
+  g.rope_cols = (c.n_heads + c.n_kv_heads) * c.head_dim; g.head_dim = c.head_dim; g.rope_tab = b.rope;
+  g.rope_pos = b.rope_pos;
   { Timed t("gemm_qkv", s); RK_TRY(launch_gemm(g, m->bf16, s)); }
   if (noise) {
     char* v = (char*)b.qkv + (size_t)(c.n_heads + c.n_kv_heads) * c.head_dim * act_bytes(m);
@@ -227,7 +236,7 @@ static rk_status reference_forward(const rk_model* m, const int32_t* tokens, con
                                    const Bufs& b, hipStream_t s) {
   const rk_model_config& c = m->cfg;
   const int64_t R = st.rows, d = c.d_model;
-  RK_TRY(launch_rope_table(b.rope, st.max_len, c.head_dim, c.rope_theta, s));
+  RK_TRY(launch_rope_table(b.rope, b.rope_pos, st, c.head_dim, c.rope_theta, s));
   RK_TRY(launch_embed(m->tok_emb, m->bf16, tokens, cl.h, (int)R, (int)d, s));
   for (int l = 0; l < c.n_layers; ++l) {
     float* out = (l + 1 < c.n_layers) ? cl.h + (size_t)(l + 1) * R * d : b.h;
@@ -276,13 +285,13 @@ static rk_status score_group(const rk_model* m, const SeqTable& st, const Clean&
   const int64_t R = st.rows, d = c.d_model;
   if (!unfused) {
     Timed t("lm_kl", s);
-    RK_TRY(launch_lm_kl((const bf16_t*)cl.xf, (const bf16_t*)xp, R * d, G, (const bf16_t*)m->lm_head, (int)R, (int)d,
+    RK_TRY(launch_lm_kl((const bf16_t*)cl.xf, (const bf16_t*)xp, pad_rows(R) * d, G, (const bf16_t*)m->lm_head, (int)R, (int)d,
                         c.vocab, cl.lse, b.part, kl, s));
     return RK_OK;
   }
   for (int g = 0; g < G; ++g) {
     GemmArgs a{};
-    a.A = (const char*)xp + (size_t)g * R * d * act_bytes(m); a.lda = d; a.B = m->lm_head; a.ldb = d;
+    a.A = (const char*)xp + (size_t)g * pad_rows(R) * d * act_bytes(m); a.lda = d; a.B = m->lm_head; a.ldb = d;
     a.M = (int)R; a.N = c.vocab; a.K = (int)d; a.epi = Epi::kStoreF32;
     a.out = lp + (size_t)g * R * c.vocab; a.ldo = c.vocab;
     Timed t("lm_logits", s);
@@ -475,7 +484,7 @@ rk_status rk_profile_layer(const rk_model* m, const rk_batch* batch, int32_t lay
   const Bufs b = carve(wp, workspace);
   const Clean cl = clean_view(m, st.rows, clean_state);
   hipStream_t s = (hipStream_t)stream;
-  RK_TRY(launch_rope_table(b.rope, st.max_len, m->cfg.head_dim, m->cfg.rope_theta, s));
+  RK_TRY(launch_rope_table(b.rope, b.rope_pos, st, m->cfg.head_dim, m->cfg.rope_theta, s));
   if ((e = perturbed_final(m, batch->tokens, st, cl, layer, alpha, p, b.xp, b, s)) != RK_OK) return e;
   float* kl = kl_pos ? kl_pos : b.kl;
   if (unfused && (e = clean_logits(m, st, cl, b.logits_c, s)) != RK_OK) return e;
@@ -547,7 +556,7 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
       pm.d_seq_stride = n_A;
       for (int k = 0; k < G; ++k) {
         const int idx = g0 + k, a = idx / n_A, j = idx % n_A;
-        void* xf = (char*)b.xp + (size_t)k * R * m->cfg.d_model * act_bytes(m);
+        void* xf = (char*)b.xp + (size_t)k * pad_rows(R) * m->cfg.d_model * act_bytes(m);
         if ((e = perturbed_final(m, tokens, st, cl, layers[j], alphas[a], p, xf, b, s)) != RK_OK) return e;
         pm.d_base[k] = (int64_t)a * N * n_A + j;
         pm.s_index[k] = a * n_A + j;

@@ -11,8 +11,11 @@
 //     column: the row max and row sum of the softmax are lane-local plus one
 //     exchange with the partner half-wave;
 //   * O^T = V^T P^T: the P^T operand is the lane's own S^T registers rounded to
-//     bf16; V^T is written to LDS with the key order permuted inside each group
-//     of 16 so that the matching V^T fragment is one 16-byte read;
+//     bf16 (keys 4h..4h+3 and 8+4h..8+4h+3 of each 16-key step); V^T is written
+//     to LDS as key pairs and read as two 8-byte pieces that match those keys;
+//   * masks only on diagonal / ragged tiles; the softmax scale is folded into
+//     one FMA before exp2; the running max is raised lazily (rescaling O only
+//     when a tile's max grows by more than 2^8);
 //   * work items run heaviest (latest q-block) first.
 // fp32 kernel: one thread per (row, head), streaming keys; for the small fp32
 // model only.
@@ -25,28 +28,26 @@ namespace rk {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-// Physical position of key w (0..63) of a tile inside the transposed V tile.
-__device__ __forceinline__ int vt_perm(int key) {
-  const int grp = key >> 4, w = key & 15;
-  const int a = w >> 3, hh = (w >> 2) & 1, j = w & 3;
-  return grp * 16 + hh * 8 + a * 4 + j;
-}
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t v2u __attribute__((ext_vector_type(2)));
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
-}
+// Raw scores are kept unscaled; p = 2^((s - m) * c) with c = log2(e) / sqrt(d_h).
+// The running max m is only raised when a tile's max exceeds it by more than
+// kLazy / c (2^8 headroom in P), so most tiles skip the rescale of O and l.
+constexpr float kLazyLog2 = 8.0f;
 
 template <int DH>
 __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict__ qkv, int64_t ldq,
                                                         bf16_t* __restrict__ out, int64_t ldo, SeqTable st,
-                                                        AttnWork wk, int H, int Hkv, float scale_log2) {
+                                                        AttnWork wk, int H, int Hkv, float c_log2) {
   constexpr int BQ = 128, BKV = 64;
   constexpr int KCH = DH / 8;               // 16-byte chunks per K row
   constexpr int NKS = DH / 16;              // k-steps of S^T
   constexpr int NDB = DH / 32;              // 32-row blocks of O^T
-  constexpr int NLD = BKV * KCH / 256;      // K (and V) chunks loaded per thread
+  constexpr int NLK = BKV * KCH / 256;      // K chunks loaded per thread
+  constexpr int NLV = BKV * KCH / 512;      // V key-pair chunks loaded per thread
   __shared__ __attribute__((aligned(16))) v4u Ks[2][BKV * KCH];
-  __shared__ __attribute__((aligned(16))) v4u Vt[2][DH * 8];
+  __shared__ __attribute__((aligned(16))) v4u Vt[2][DH * 8];   // [d][64 keys], 16-byte chunks XOR-swizzled by d
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31, hf = lane >> 5;
   const int item = wk.total - 1 - (int)blockIdx.x;
@@ -77,29 +78,40 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
   const int kv_end = min(T, q0 + BQ);
   const int n_tiles = (kv_end + BKV - 1) / BKV;
 
-  v4u rk[NLD], rv[NLD];
+  v4u rk[NLK], rv[2 * NLV];
   auto gload = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < NLD; ++i) {
+    for (int i = 0; i < NLK; ++i) {
       const int c = tid + 256 * i, key = c / KCH, ch = c % KCH;
       const int64_t r = row0 + min(k0 + key, T - 1);
       rk[i] = *reinterpret_cast<const v4u*>(qkv + r * ldq + kcol + ch * 8);
-      rv[i] = *reinterpret_cast<const v4u*>(qkv + r * ldq + vcol + ch * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < NLV; ++i) {
+      const int c = tid + 256 * i, kp = c / KCH, ch = c % KCH;   // key pair kp: keys 2kp, 2kp+1
+      const int64_t r0 = row0 + min(k0 + 2 * kp, T - 1), r1 = row0 + min(k0 + 2 * kp + 1, T - 1);
+      rv[2 * i] = *reinterpret_cast<const v4u*>(qkv + r0 * ldq + vcol + ch * 8);
+      rv[2 * i + 1] = *reinterpret_cast<const v4u*>(qkv + r1 * ldq + vcol + ch * 8);
     }
   };
   auto lstore = [&](int b) {
 #pragma unroll
-    for (int i = 0; i < NLD; ++i) {
+    for (int i = 0; i < NLK; ++i) {
       const int c = tid + 256 * i, key = c / KCH, ch = c % KCH;
       Ks[b][key * KCH + (ch ^ (key & 7))] = rk[i];
-      const int pk = vt_perm(key);
-      bf16_t* vt = reinterpret_cast<bf16_t*>(Vt[b]);
-      const uint32_t words[4] = {rv[i].x, rv[i].y, rv[i].z, rv[i].w};
+    }
+    uint32_t* vt = reinterpret_cast<uint32_t*>(Vt[b]);
+#pragma unroll
+    for (int i = 0; i < NLV; ++i) {
+      const int c = tid + 256 * i, kp = c / KCH, ch = c % KCH;
+      const int key = 2 * kp;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int dd = ch * 8 + e;
-        const bf16_t val = (bf16_t)((e & 1) ? (words[e >> 1] >> 16) : (words[e >> 1] & 0xffffu));
-        vt[(dd * 8 + ((pk >> 3) ^ (dd & 7))) * 8 + (pk & 7)] = val;
+        const uint32_t lo = (rv[2 * i][e >> 1] >> ((e & 1) * 16)) & 0xffffu;
+        const uint32_t hi = (rv[2 * i + 1][e >> 1] >> ((e & 1) * 16)) & 0xffffu;
+        // word index: row dd (32 words), chunk key/8 swizzled, word (key%8)/2 inside the chunk
+        vt[dd * 32 + (((key >> 3) ^ (dd & 7)) << 2) + ((key & 7) >> 1)] = lo | (hi << 16);
       }
     }
   };
@@ -114,7 +126,8 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
   gload(0);
   lstore(0);
   __syncthreads();
-  const int wave_qmax = q0 + w * 32 + 31;
+  const int wave_qmin = q0 + w * 32, wave_qmax = wave_qmin + 31;
+  const float lazy = kLazyLog2 / c_log2;
   for (int t = 0; t < n_tiles; ++t) {
     const int buf = t & 1, k0 = t * BKV;
     if (t + 1 < n_tiles) gload(k0 + BKV);
@@ -131,51 +144,60 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
           s[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s[rb], 0, 0, 0);
         }
       }
-      float mx = -INFINITY;
+      // masks only where a key can exceed the query or the sequence (wave-uniform test)
+      if (k0 + BKV - 1 > wave_qmin || k0 + BKV > T) {
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int key = k0 + rb * 32 + (i >> 2) * 8 + hf * 4 + (i & 3);
+            if (key > my_q || key >= T) s[rb][i] = -INFINITY;
+          }
+      }
+      float mx = s[0][0];
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = k0 + rb * 32 + (i >> 2) * 8 + hf * 4 + (i & 3);
-          float v = s[rb][i] * scale_log2;
-          if (key > my_q || key >= T) v = -INFINITY;
-          s[rb][i] = v;
-          mx = fmaxf(mx, v);
-        }
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[rb][i]);
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_new = fmaxf(m_run, mx);
-      const float corr = exp2f(m_run - m_new);
+      if (__any(mx > m_run + lazy)) {
+        const float m_new = fmaxf(m_run, mx);
+        const float corr = __builtin_amdgcn_exp2f((m_run - m_new) * c_log2);
+        l_run *= corr;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) o[db][i] *= corr;
+        m_run = m_new;
+      }
+      const float mc = m_run * c_log2;
       float rs = 0.f;
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const float p = exp2f(s[rb][i] - m_new);
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[rb][i], c_log2, -mc));
           s[rb][i] = p;
           rs += p;
         }
-      l_run = l_run * corr + rs;
-      m_run = m_new;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) o[db][i] *= corr;
+      l_run += rs;
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
         for (int ss = 0; ss < 2; ++ss) {
-          v4u pw;
-          pw.x = pack_bf16x2(s[rb][8 * ss + 0], s[rb][8 * ss + 1]);
-          pw.y = pack_bf16x2(s[rb][8 * ss + 2], s[rb][8 * ss + 3]);
-          pw.z = pack_bf16x2(s[rb][8 * ss + 4], s[rb][8 * ss + 5]);
-          pw.w = pack_bf16x2(s[rb][8 * ss + 6], s[rb][8 * ss + 7]);
-          const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, pw);
-          const int ch = rb * 4 + 2 * ss + hf;
+          bf16x8_t pb;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) pb[e] = (__bf16)s[rb][8 * ss + e];
+          // this lane's k-slots: keys 16*(2rb+ss) + 4hf + {0..3} and the same + 8
+          const int kb = rb * 32 + ss * 16 + hf * 4;
 #pragma unroll
           for (int db = 0; db < NDB; ++db) {
             const int dd = db * 32 + l32;
-            const bf16x8_t va = __builtin_bit_cast(bf16x8_t, Vt[buf][dd * 8 + (ch ^ (dd & 7))]);
-            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[db], 0, 0, 0);
+            const v2u* row = reinterpret_cast<const v2u*>(Vt[buf]) + dd * 16;
+            const v2u lo = row[(((kb >> 3) ^ (dd & 7)) << 1) + ((kb & 7) >> 2)];
+            const v2u hi = row[((((kb + 8) >> 3) ^ (dd & 7)) << 1) + ((kb & 7) >> 2)];
+            const v4u vv = {lo[0], lo[1], hi[0], hi[1]};
+            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vv), pb, o[db], 0, 0, 0);
           }
         }
     }
@@ -191,10 +213,10 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        uint2 u;
-        u.x = pack_bf16x2(o[db][g * 4 + 0] * inv, o[db][g * 4 + 1] * inv);
-        u.y = pack_bf16x2(o[db][g * 4 + 2] * inv, o[db][g * 4 + 3] * inv);
-        *reinterpret_cast<uint2*>(op + db * 32 + g * 8 + hf * 4) = u;
+        bf16x4_t u;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) u[e] = (__bf16)(o[db][g * 4 + e] * inv);
+        *reinterpret_cast<bf16x4_t*>(op + db * 32 + g * 8 + hf * 4) = u;
       }
   }
 }
@@ -241,14 +263,14 @@ hipError_t launch_attention(const void* qkv, int64_t ldq, void* out, int64_t ldo
     for (int k = 0; k < st.n; ++k) wk.cum[k + 1] = wk.cum[k] + (st.off[k + 1] - st.off[k] + 127) / 128;
     wk.total = wk.cum[st.n];
     if (wk.total == 0) return hipSuccess;
-    const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)head_dim));
+    const float c_log2 = (float)(1.4426950408889634 / sqrt((double)head_dim));
     dim3 grid(wk.total, n_heads);
     if (head_dim == 128)
       attn_bf16_kernel<128><<<grid, 256, 0, s>>>((const bf16_t*)qkv, ldq, (bf16_t*)out, ldo, st, wk, n_heads,
-                                                 n_kv_heads, scale_log2);
+                                                 n_kv_heads, c_log2);
     else if (head_dim == 64)
       attn_bf16_kernel<64><<<grid, 256, 0, s>>>((const bf16_t*)qkv, ldq, (bf16_t*)out, ldo, st, wk, n_heads,
-                                                n_kv_heads, scale_log2);
+                                                n_kv_heads, c_log2);
     else
       return hipErrorInvalidValue;
   } else {

@@ -1,6 +1,8 @@
 // HBM-bound kernels of the profiling path: embedding gather, RMSNorm, the rotary
 // table, the norm-adaptive Value noise (Eq. value-perturbation) and the window /
 // calibration means (Eqs. sample-response and layer-sensitivity).
+#include <algorithm>
+
 #include "rk_internal.h"
 
 namespace rk {
@@ -70,11 +72,13 @@ hipError_t launch_rmsnorm(const float* h, const float* g, void* out, bool out_bf
 }
 
 // --------------------------------------------------------------------------- rotary table
-// tab[t * (dh/2) + j] = (cos, sin)(t * theta^(-2j/dh)); the angle is formed and
-// reduced modulo 2*pi in double precision before the fp32 sincos.
-__global__ void rope_table_kernel(float2* tab, int max_len, int half, int dh, double log2_theta) {
-  const int64_t total = (int64_t)max_len * half;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+// tab[t * (dh/2) + j] = (cos, sin)(t * theta^(-2j/dh)) for t < max_len; the angle is
+// formed and reduced modulo 2*pi in double precision before the fp32 rounding.
+// pos[r] = position of row r inside its sequence.
+__global__ void rope_table_kernel(float2* tab, int32_t* pos, SeqTable st, int half, int dh, double log2_theta) {
+  const int64_t total = (int64_t)st.max_len * half;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
     const int t = (int)(i / half), j = (int)(i - (int64_t)t * half);
     const double inv_freq = exp2(-(2.0 * j / dh) * log2_theta);
     double ang = (double)t * inv_freq;
@@ -84,15 +88,17 @@ __global__ void rope_table_kernel(float2* tab, int max_len, int half, int dh, do
     sincos(ang, &sv, &cv);
     tab[i] = make_float2((float)cv, (float)sv);
   }
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < st.rows; r += stride)
+    pos[r] = (int32_t)(r - st.off[seq_of_row(st, (int)r)]);
 }
 
-hipError_t launch_rope_table(float2* tab, int max_len, int head_dim, float theta, hipStream_t s) {
+hipError_t launch_rope_table(float2* tab, int32_t* pos, const SeqTable& st, int head_dim, float theta, hipStream_t s) {
   const int half = head_dim / 2;
-  const int64_t total = (int64_t)max_len * half;
+  const int64_t total = std::max((int64_t)st.max_len * half, (int64_t)st.rows);
   int blocks = (int)((total + 255) / 256);
   if (blocks > 16384) blocks = 16384;
   if (blocks < 1) blocks = 1;
-  rope_table_kernel<<<blocks, 256, 0, s>>>(tab, max_len, half, head_dim, log2((double)theta));
+  rope_table_kernel<<<blocks, 256, 0, s>>>(tab, pos, st, half, head_dim, log2((double)theta));
   return hipGetLastError();
 }
 

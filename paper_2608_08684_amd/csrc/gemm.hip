@@ -4,17 +4,16 @@
 //   output / down     -> residual add into the fp32 stream,
 //   gate|up           -> SwiGLU (silu(gate) * up), written as one [M, d_ff] tile,
 //   LM head (unfused) -> plain fp32 logits.
-// bf16 path: 128x128 block tile, 4 waves of 64x64, v_mfma_f32_32x32x16_bf16,
-// K-step 64 double-buffered through LDS with an XOR swizzle of 16-byte chunks.
+// bf16 path: BM x BN block tile (128x128, 256x128 or 256x256), 2x2 waves,
+// v_mfma_f32_32x32x16_bf16, K-step 64 streamed global -> LDS by
+// global_load_lds_dwordx4 into two stages (see mfma_tile.h).
 // fp32 path: a VALU kernel with the same epilogues (64x128 tile).
-// Both stage the finished tile through LDS so each epilogue sees whole rows
-// (a rotary pair j, j + d_h/2 or a gate/up pair lies inside one tile).
-#include "rk_internal.h"
+// Both stage the finished tile through LDS 64 rows at a time so each epilogue
+// sees whole rows (a rotary pair j, j + d_h/2 or a gate/up pair lies inside one
+// tile).
+#include "mfma_tile.h"
 
 namespace rk {
-
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kCsStride = 132;  // staged tile row stride in floats (128 + pad)
 
@@ -33,42 +32,47 @@ __device__ __forceinline__ void store8(bf16_t* p, const float* v) {
 }
 
 // --------------------------------------------------------------------------- epilogues
-// Called per (row, 8 consecutive tile columns starting at c0) with cs = the staged
-// fp32 row of the tile.  kOutCols = output columns one tile produces.
+// Called per (row, 8 consecutive output columns starting at c0) with cs = the
+// staged fp32 row of a BN-wide tile.  out_cols(BN) = output columns per tile.
 template <typename O>
 struct EpiRope {
-  static constexpr int kOutCols = 128;
-  O* out; int64_t ldo; int rope_cols; int head_dim; const float2* tab; SeqTable seq;
-  __device__ void operator()(int row, int bn, int c0, const float* cs) const {
-    const int n0 = bn * 128;
-    const int pos = row - seq.off[seq_of_row(seq, row)];
+  static constexpr int out_cols(int BN) { return BN; }
+  // tab[pos * head_dim/2 + j] = (cos, sin) of position pos, pair j; pos[row] = position of the row
+  O* out; int64_t ldo; int rope_cols; int head_dim; const float2* tab; const int32_t* pos;
+  template <int BN>
+  __device__ void apply(int row, int bn, int c0, const float* cs) const {
+    const int gc0 = bn * BN + c0;
+    O* dst = out + (int64_t)row * ldo + gc0;
+    if (gc0 >= rope_cols) {  // value columns: no rotation
+      store8(dst, cs + c0);
+      return;
+    }
+    // the 8 columns lie in one half of one head: pairs jh0..jh0+7 with partners at +-half
     const int half = head_dim >> 1;
+    const int jh = gc0 & (head_dim - 1);
+    const bool lo = jh < half;
+    const int j0 = lo ? jh : jh - half;
+    const float4* t4 = reinterpret_cast<const float4*>(tab + (int64_t)pos[row] * half + j0);
+    const float* x = cs + c0;
+    const float* y = cs + c0 + (lo ? half : -half);
+    const float sg = lo ? -1.0f : 1.0f;
     float v[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int c = c0 + j, gc = n0 + c;
-      float x = cs[c];
-      if (gc < rope_cols) {
-        const int jh = gc & (head_dim - 1);
-        if (jh < half) {
-          const float2 t = tab[(int64_t)pos * half + jh];
-          x = cs[c] * t.x - cs[c + half] * t.y;
-        } else {
-          const float2 t = tab[(int64_t)pos * half + (jh - half)];
-          x = cs[c] * t.x + cs[c - half] * t.y;
-        }
-      }
-      v[j] = x;
+    for (int q = 0; q < 4; ++q) {
+      const float4 t = t4[q];  // (cos, sin) of pairs 2q and 2q+1
+      v[2 * q] = fmaf(sg * y[2 * q], t.y, x[2 * q] * t.x);
+      v[2 * q + 1] = fmaf(sg * y[2 * q + 1], t.w, x[2 * q + 1] * t.z);
     }
-    store8(out + (int64_t)row * ldo + n0 + c0, v);
+    store8(dst, v);
   }
 };
 
 struct EpiResidual {
-  static constexpr int kOutCols = 128;
+  static constexpr int out_cols(int BN) { return BN; }
   float* out; int64_t ldo; const float* res; int64_t ldr;
-  __device__ void operator()(int row, int bn, int c0, const float* cs) const {
-    const int64_t n = (int64_t)bn * 128 + c0;
+  template <int BN>
+  __device__ void apply(int row, int bn, int c0, const float* cs) const {
+    const int64_t n = (int64_t)bn * BN + c0;
     const float4* r4 = reinterpret_cast<const float4*>(res + (int64_t)row * ldr + n);
     const float4 a = r4[0], b = r4[1];
     float v[8] = {a.x + cs[c0 + 0], a.y + cs[c0 + 1], a.z + cs[c0 + 2], a.w + cs[c0 + 3],
@@ -79,40 +83,43 @@ struct EpiResidual {
 
 template <typename O>
 struct EpiSwiGLU {
-  static constexpr int kOutCols = 64;   // tile columns [0,64) gate, [64,128) up
+  static constexpr int out_cols(int BN) { return BN / 2; }  // tile columns [0, BN/2) gate, [BN/2, BN) up
   O* out; int64_t ldo;
-  __device__ void operator()(int row, int bn, int c0, const float* cs) const {
+  template <int BN>
+  __device__ void apply(int row, int bn, int c0, const float* cs) const {
     float v[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const float g = cs[c0 + j], u = cs[64 + c0 + j];
+      const float g = cs[c0 + j], u = cs[BN / 2 + c0 + j];
       v[j] = g / (1.0f + expf(-g)) * u;
     }
-    store8(out + (int64_t)row * ldo + (int64_t)bn * 64 + c0, v);
+    store8(out + (int64_t)row * ldo + (int64_t)bn * (BN / 2) + c0, v);
   }
 };
 
 struct EpiStoreF32 {
-  static constexpr int kOutCols = 128;
+  static constexpr int out_cols(int BN) { return BN; }
   float* out; int64_t ldo;
-  __device__ void operator()(int row, int bn, int c0, const float* cs) const {
-    store8(out + (int64_t)row * ldo + (int64_t)bn * 128 + c0, cs + c0);
+  template <int BN>
+  __device__ void apply(int row, int bn, int c0, const float* cs) const {
+    store8(out + (int64_t)row * ldo + (int64_t)bn * BN + c0, cs + c0);
   }
 };
 
-template <class E>
+// Run the epilogue over 64 staged rows (row stride BN + 4 floats).
+template <int BN, class E>
 __device__ __forceinline__ void run_epilogue(const E& e, const float* Cs, int row0, int M, int bn) {
-  constexpr int TPR = E::kOutCols / 8;
+  constexpr int TPR = E::out_cols(BN) / 8;
   constexpr int RPP = 256 / TPR;
   const int t = threadIdx.x;
   const int c0 = (t % TPR) * 8;
   for (int r = t / TPR; r < 64; r += RPP) {
     const int row = row0 + r;
-    if (row < M) e(row, bn, c0, Cs + r * kCsStride);
+    if (row < M) e.template apply<BN>(row, bn, c0, Cs + r * (BN + 4));
   }
 }
 
-// Row of B feeding tile column n of column-block bn.
+// Row of B feeding tile column n of column-block bn (fp32 path, 128-wide tiles).
 template <bool SWIGLU>
 __device__ __forceinline__ int b_row(int bn, int n, int d_ff) {
   if (SWIGLU) return n < 64 ? bn * 64 + n : d_ff + bn * 64 + (n - 64);
@@ -120,98 +127,107 @@ __device__ __forceinline__ int b_row(int bn, int n, int d_ff) {
 }
 
 // --------------------------------------------------------------------------- bf16 MFMA kernel
-template <class E, bool SWIGLU>
+template <int BM, int BN, class E, bool SWIGLU>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict__ A, int64_t lda,
                                                         const bf16_t* __restrict__ B, int64_t ldb, int M, int K,
-                                                        int d_ff, E e) {
-  __shared__ __attribute__((aligned(16))) v4u smem[4096];  // 2 x (A 128x64 + B 128x64) bf16 = 64 KB
+                                                        int d_ff, int n_bn, int group_m, E e) {
+  constexpr int MI = BM / 64, NI = BN / 64;       // 32x32 blocks per wave (2x2 waves)
+  constexpr int AS = BM * 8, BS = BN * 8;         // 16-byte slots per stage
+  __shared__ __attribute__((aligned(16))) v4u smem[2 * (AS + BS)];
+  static_assert(64 * (BN + 4) * 4 <= 2 * (AS + BS) * 16, "staging tile must fit");
   v4u* As = smem;
-  v4u* Bs = smem + 2048;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int bn = blockIdx.x, m0 = blockIdx.y * 128;
+  v4u* Bs = smem + 2 * AS;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31;
+  const int wm = w >> 1, wn = w & 1;
+  int bm_, bn;
+  xcd_tile((int)blockIdx.x, (M + BM - 1) / BM, n_bn, group_m, &bm_, &bn);
+  const int m0 = bm_ * BM;
 
-  const v4u* ga[4];
-  const v4u* gb[4];
-  int so[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
-    const int ar = min(m0 + row, M - 1);
-    ga[i] = reinterpret_cast<const v4u*>(A + (int64_t)ar * lda) + kc;
-    gb[i] = reinterpret_cast<const v4u*>(B + (int64_t)b_row<SWIGLU>(bn, row, d_ff) * ldb) + kc;
-    so[i] = row * 8 + (kc ^ (row & 7));
+  TileSrc sa, sb, su;
+  sa.init(A + (int64_t)m0 * lda, lda, w, lane);
+  if (SWIGLU) {
+    sb.init(B + (int64_t)bn * (BN / 2) * ldb, ldb, w, lane);
+    su.init(B + ((int64_t)d_ff + (int64_t)bn * (BN / 2)) * ldb, ldb, w, lane);
+  } else {
+    sb.init(B + (int64_t)bn * BN * ldb, ldb, w, lane);
   }
-  const int nk = K / 64;
-  v4u ra[4], rb[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) { ra[i] = ga[i][0]; rb[i] = gb[i][0]; }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) { As[so[i]] = ra[i]; Bs[so[i]] = rb[i]; }
-  __syncthreads();
+  auto issue = [&](int kt, int stage) {
+    sa.template load<BM>(kt, As + stage * AS, w);
+    if (SWIGLU) {
+      sb.template load<BN / 2>(kt, Bs + stage * BS, w);
+      su.template load<BN / 2>(kt, Bs + stage * BS + (BN / 2) * 8, w);
+    } else {
+      sb.template load<BN>(kt, Bs + stage * BS, w);
+    }
+  };
 
-  f32x16_t acc[2][2];
+  f32x16_t acc[MI][NI];
 #pragma unroll
-  for (int mi = 0; mi < 2; ++mi)
+  for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni)
+    for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[mi][ni][i] = 0.f;
 
+  const int nk = K / kBK;
+  issue(0, 0);
+  wait_vmem();
+  __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) issue(kt + 1, cur ^ 1);
+    const v4u* At = As + cur * AS;
+    const v4u* Bt = Bs + cur * BS;
+    // fragments double-buffered in registers: k-slice ks+1 is read from LDS
+    // while the MFMAs of slice ks run
+    bf16x8_t af[2][MI], bfr[2][NI];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) { ra[i] = ga[i][(kt + 1) * 8]; rb[i] = gb[i][(kt + 1) * 8]; }
-    }
-    const v4u* Ab = As + buf * 1024;
-    const v4u* Bb = Bs + buf * 1024;
+    for (int mi = 0; mi < MI; ++mi) af[0][mi] = frag(At, wm * (BM / 2) + mi * 32 + l32, 0, lane);
+#pragma unroll
+    for (int ni = 0; ni < NI; ++ni) bfr[0][ni] = frag(Bt, wn * (BN / 2) + ni * 32 + l32, 0, lane);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      const int ch = ks * 2 + (lane >> 5);
-      bf16x8_t af[2], bfr[2];
+      const int c = ks & 1;
+      if (ks < 3) {
 #pragma unroll
-      for (int mi = 0; mi < 2; ++mi) {
-        const int row = wm * 64 + mi * 32 + (lane & 31);
-        af[mi] = __builtin_bit_cast(bf16x8_t, Ab[row * 8 + (ch ^ (row & 7))]);
+        for (int mi = 0; mi < MI; ++mi) af[c ^ 1][mi] = frag(At, wm * (BM / 2) + mi * 32 + l32, ks + 1, lane);
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni) bfr[c ^ 1][ni] = frag(Bt, wn * (BN / 2) + ni * 32 + l32, ks + 1, lane);
       }
+      // keep the next slice's LDS reads ahead of this slice's MFMAs
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        const int row = wn * 64 + ni * 32 + (lane & 31);
-        bfr[ni] = __builtin_bit_cast(bf16x8_t, Bb[row * 8 + (ch ^ (row & 7))]);
-      }
+      for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-      for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mi], bfr[ni], acc[mi][ni], 0, 0, 0);
+        for (int ni = 0; ni < NI; ++ni)
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[c][mi], bfr[c][ni], acc[mi][ni], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    if (kt + 1 < nk) {
-      const int nb = (kt + 1) & 1;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) { As[nb * 1024 + so[i]] = ra[i]; Bs[nb * 1024 + so[i]] = rb[i]; }
-    }
+    wait_vmem();
     __syncthreads();
   }
 
-  // Stage 64 rows at a time (the two wave rows) and run the epilogue on whole rows.
+  // Stage 64 rows at a time and run the epilogue on whole rows.
   float* Cs = reinterpret_cast<float*>(smem);
+  constexpr int CSS = BN + 4;
 #pragma unroll
-  for (int half = 0; half < 2; ++half) {
-    if (wm == half) {
+  for (int slice = 0; slice < BM / 64; ++slice) {
+    const int owner = (slice * 64) / (BM / 2);
+    const int mi0 = (slice * 64 - owner * (BM / 2)) / 32;
+    if (wm == owner) {
 #pragma unroll
-      for (int mi = 0; mi < 2; ++mi)
+      for (int mm = 0; mm < 2; ++mm)
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
+        for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
-            const int r = mi * 32 + (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
-            const int c = wn * 64 + ni * 32 + (lane & 31);
-            Cs[r * kCsStride + c] = acc[mi][ni][i];
+            const int r = mm * 32 + (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
+            const int c = wn * (BN / 2) + ni * 32 + l32;
+            Cs[r * CSS + c] = acc[mi0 + mm][ni][i];
           }
     }
     __syncthreads();
-    run_epilogue(e, Cs, m0 + half * 64, M, bn);
+    run_epilogue<BN>(e, Cs, m0 + slice * 64, M, bn);
     __syncthreads();
   }
 }
@@ -222,6 +238,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
                                                        const float* __restrict__ B, int64_t ldb, int M, int K,
                                                        int d_ff, E e) {
   __shared__ __attribute__((aligned(16))) float smem[64 * kCsStride];
+  static_assert(kCsStride == 128 + 4, "fp32 path stages 128-wide tiles");
   float* As = smem;             // [16][68]  k-major
   float* Bs = smem + 16 * 68;   // [16][132] k-major
   const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
@@ -267,18 +284,41 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 #pragma unroll
     for (int j = 0; j < 8; ++j) Cs[(ty * 4 + i) * kCsStride + tx * 8 + j] = acc[i][j];
   __syncthreads();
-  run_epilogue(e, Cs, m0, M, bn);
+  run_epilogue<128>(e, Cs, m0, M, bn);
 }
 
 // --------------------------------------------------------------------------- dispatch
+// Tile choice (measured on MI355X): 256x256 pays off only with a long K loop and
+// enough tiles to fill the CUs; otherwise 128x128 at two workgroups per CU.
+static void pick_tile(const GemmArgs& a, bool swiglu, int* bm, int* bn_) {
+  const int n_cols = swiglu ? 2 * a.d_ff : a.N;
+  const int64_t tiles256 = (int64_t)(a.M + 255) / 256 * (n_cols / 256);
+  const bool fits256 = swiglu ? (a.d_ff % 128 == 0) : (a.N % 256 == 0);
+  if (fits256 && a.K >= 2048 && tiles256 >= 512) { *bm = 256; *bn_ = 256; return; }
+  *bm = 128; *bn_ = 128;
+}
+
+template <int BM, int BN, class E, bool SWIGLU>
+static void go_bf16(const GemmArgs& a, const E& e, hipStream_t s) {
+  const int nbn = SWIGLU ? a.d_ff / (BN / 2) : a.N / BN;
+  const int nbm = (a.M + BM - 1) / BM;
+  const int group_m = a.group_m > 0 ? a.group_m : 8;
+  gemm_bf16_kernel<BM, BN, E, SWIGLU><<<nbm * nbn, 256, 0, s>>>((const bf16_t*)a.A, a.lda, (const bf16_t*)a.B,
+                                                                a.ldb, a.M, a.K, a.d_ff, nbn, group_m, e);
+}
+
 template <class E, bool SWIGLU>
 static hipError_t go(const GemmArgs& a, bool bf16, const E& e, hipStream_t s) {
-  const int nbn = SWIGLU ? a.d_ff / 64 : a.N / 128;
   if (bf16) {
-    dim3 grid(nbn, (a.M + 127) / 128);
-    gemm_bf16_kernel<E, SWIGLU><<<grid, 256, 0, s>>>((const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M,
-                                                     a.K, a.d_ff, e);
+    int bm, bn;
+    pick_tile(a, SWIGLU, &bm, &bn);
+    if (a.tile_m) { bm = a.tile_m; bn = a.tile_n; }
+    if (bm == 256 && bn == 256) go_bf16<256, 256, E, SWIGLU>(a, e, s);
+    else if (bm == 256 && bn == 128) go_bf16<256, 128, E, SWIGLU>(a, e, s);
+    else if (bm == 128 && bn == 128) go_bf16<128, 128, E, SWIGLU>(a, e, s);
+    else return hipErrorInvalidValue;
   } else {
+    const int nbn = SWIGLU ? a.d_ff / 64 : a.N / 128;
     dim3 grid(nbn, (a.M + 63) / 64);
     gemm_f32_kernel<E, SWIGLU><<<grid, 256, 0, s>>>((const float*)a.A, a.lda, (const float*)a.B, a.ldb, a.M, a.K,
                                                     a.d_ff, e);
@@ -291,10 +331,10 @@ hipError_t launch_gemm(const GemmArgs& a, bool bf16, hipStream_t s) {
   switch (a.epi) {
     case Epi::kStoreRope:
       if (bf16) {
-        EpiRope<bf16_t> e{(bf16_t*)a.out, a.ldo, a.rope_cols, a.head_dim, a.rope_tab, a.seq};
+        EpiRope<bf16_t> e{(bf16_t*)a.out, a.ldo, a.rope_cols, a.head_dim, a.rope_tab, a.rope_pos};
         return go<EpiRope<bf16_t>, false>(a, true, e, s);
       } else {
-        EpiRope<float> e{(float*)a.out, a.ldo, a.rope_cols, a.head_dim, a.rope_tab, a.seq};
+        EpiRope<float> e{(float*)a.out, a.ldo, a.rope_cols, a.head_dim, a.rope_tab, a.rope_pos};
         return go<EpiRope<float>, false>(a, false, e, s);
       }
     case Epi::kResidual: {

@@ -1,11 +1,14 @@
 // LM head + log-softmax + KL (Algorithm 1, WindowKL; Eq. sample-response).
 //
 // KL_t = sum_v P_v (log P_v - log Q_v) with P = softmax(a), Q = softmax(b),
-// a = x_clean W^T, b = x_pert W^T.  With delta = a - b and A_t = logsumexp(a):
-//   KL_t = sum_v p_v f(delta_v) - g(S_t),   p_v = exp(a_v - A_t),
-//   f(x) = x + expm1(-x) >= 0,  S_t = sum_v p_v expm1(-delta_v),  g(y) = y - log1p(y) >= 0.
-// Both sums have non-negative, cancellation-free terms (f and g use series near
-// 0), so a KL of 1e-6 nats survives fp32 accumulation; delta = 0 gives exactly 0.
+// a = x_clean W^T, b = x_pert W^T.  With delta = a - b, A_t = logsumexp(a) and
+// p_v = exp(a_v - A_t):
+//   KL_t = sum_v p_v delta_v + log(sum_v p_v e^{-delta_v})
+//        = sum_v p_v delta_v + log1p(S_t),  S_t = sum_v p_v (e^{-delta_v} - 1)
+//        = sum_v p_v f(delta_v) - g(S_t),  f(x) = x + expm1(-x), g(y) = y - log1p(y).
+// The fused kernel accumulates the first form (cheap: no clean max or sums
+// beyond A_t, delta = 0 gives exactly 0); the unfused kernel uses the last form,
+// whose terms are all non-negative (f and g by series near 0), as a cross-check.
 //
 // Fused path (bf16): logits never reach HBM.  The clean pass runs lm_lse once per
 // batch (A_t).  lm_kl then computes, per 128-token x 128-vocab tile, the clean
@@ -17,12 +20,9 @@
 // Unfused path (any dtype): KL over two materialised fp32 logit tensors.
 #include <math.h>
 
-#include "rk_internal.h"
+#include "mfma_tile.h"
 
 namespace rk {
-
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // f(x) = x + expm1(-x) = x^2/2 - x^3/6 + ...  (>= 0)
 __device__ __forceinline__ float kl_f(float x) {
@@ -40,57 +40,39 @@ __device__ __forceinline__ float kl_f(float x) {
 
 // --------------------------------------------------------------------------- shared tile GEMM
 // acc[vb] (vb = 0..3) = W[v0 + 32 vb + ..] . X[t0 + 32 w + l32]: the 128 x 128 logit
-// tile, transposed, wave w owning tokens 32w..32w+31.  Rows of X past `rows` are
-// clamped (their results are discarded).  Leaves LDS free on return.
+// tile, transposed, wave w owning tokens 32w..32w+31.  X is padded to whole
+// 128-row tiles by the caller.  Leaves LDS free on return.
 __device__ __forceinline__ void logit_tile(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int v0,
-                                           int t0, int rows, int d, v4u* As, v4u* Bs, f32x16_t acc[4]) {
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31;
-  const v4u* ga[4];
-  const v4u* gb[4];
-  int so[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
-    ga[i] = reinterpret_cast<const v4u*>(W + (int64_t)(v0 + row) * d) + kc;
-    gb[i] = reinterpret_cast<const v4u*>(X + (int64_t)min(t0 + row, rows - 1) * d) + kc;
-    so[i] = row * 8 + (kc ^ (row & 7));
-  }
+                                           int t0, int d, v4u* As, v4u* Bs, f32x16_t acc[4]) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, l32 = lane & 31;
+  TileSrc sw, sx;
+  sw.init(W + (int64_t)v0 * d, d, w, lane);
+  sx.init(X + (int64_t)t0 * d, d, w, lane);
 #pragma unroll
   for (int vb = 0; vb < 4; ++vb)
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[vb][i] = 0.f;
-  const int nk = d / 64;
-  v4u ra[4], rb[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) { ra[i] = ga[i][0]; rb[i] = gb[i][0]; }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) { As[so[i]] = ra[i]; Bs[so[i]] = rb[i]; }
+  const int nk = d / kBK;
+  sw.load<128>(0, As, w);
+  sx.load<128>(0, Bs, w);
+  wait_vmem();
   __syncthreads();
-  const int trow = w * 32 + l32;
   for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
+    const int cur = kt & 1;
     if (kt + 1 < nk) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) { ra[i] = ga[i][(kt + 1) * 8]; rb[i] = gb[i][(kt + 1) * 8]; }
+      sw.load<128>(kt + 1, As + (cur ^ 1) * 1024, w);
+      sx.load<128>(kt + 1, Bs + (cur ^ 1) * 1024, w);
     }
-    const v4u* Ab = As + buf * 1024;
-    const v4u* Bb = Bs + buf * 1024;
+    const v4u* At = As + cur * 1024;
+    const v4u* Bt = Bs + cur * 1024;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      const int ch = ks * 2 + (lane >> 5);
-      const bf16x8_t bx = __builtin_bit_cast(bf16x8_t, Bb[trow * 8 + (ch ^ (trow & 7))]);
+      const bf16x8_t bx = frag(Bt, w * 32 + l32, ks, lane);
 #pragma unroll
-      for (int vb = 0; vb < 4; ++vb) {
-        const int vrow = vb * 32 + l32;
-        const bf16x8_t aw = __builtin_bit_cast(bf16x8_t, Ab[vrow * 8 + (ch ^ (vrow & 7))]);
-        acc[vb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aw, bx, acc[vb], 0, 0, 0);
-      }
+      for (int vb = 0; vb < 4; ++vb)
+        acc[vb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag(At, vb * 32 + l32, ks, lane), bx, acc[vb], 0, 0, 0);
     }
-    if (kt + 1 < nk) {
-      const int nb = (kt + 1) & 1;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) { As[nb * 1024 + so[i]] = ra[i]; Bs[nb * 1024 + so[i]] = rb[i]; }
-    }
+    wait_vmem();
     __syncthreads();
   }
 }
@@ -106,7 +88,7 @@ __global__ __launch_bounds__(256) void lm_lse_kernel(const bf16_t* __restrict__ 
   float m = -INFINITY, z = 0.f;
   f32x16_t acc[4];
   for (int vt = vt0; vt < vt1; ++vt) {
-    logit_tile(W, X, vt * 128, t0, rows, d, smem, smem + 2048, acc);
+    logit_tile(W, X, vt * 128, t0, d, smem, smem + 2048, acc);
     float mx = -INFINITY;
 #pragma unroll
     for (int vb = 0; vb < 4; ++vb)
@@ -143,65 +125,74 @@ __global__ void lse_merge_kernel(const float2* __restrict__ part, int n_chunks, 
 }
 
 // --------------------------------------------------------------------------- fused KL
+// Per (token t, pass g): T1 = sum_v p_v delta_v and S = sum_v p_v (e^{-delta_v} - 1)
+// with p_v = exp(a_v - A_t), so KL_t = T1 + log1p(S) (= sum p (a - b) - A + B
+// without forming A and B).  delta = 0 gives exactly T1 = S = 0.  p is recomputed
+// per pass instead of being held, which keeps the kernel at two waves per SIMD.
+constexpr float kLog2e = 1.4426950408889634f;
+
 template <int GMAX>
-__global__ __launch_bounds__(256) void lm_kl_kernel(const bf16_t* __restrict__ Xc, const bf16_t* __restrict__ Xp,
-                                                    int64_t pass_stride, int G, const bf16_t* __restrict__ W,
-                                                    int rows, int d, int n_vt, int vt_per_chunk,
-                                                    const float* __restrict__ lse, float2* __restrict__ part) {
+__global__ __launch_bounds__(256, 2) void lm_kl_kernel(const bf16_t* __restrict__ Xc, const bf16_t* __restrict__ Xp,
+                                                       int64_t pass_stride, int G, const bf16_t* __restrict__ W,
+                                                       int rows, int d, int n_vt, int vt_per_chunk,
+                                                       const float* __restrict__ lse, float2* __restrict__ part) {
   __shared__ __attribute__((aligned(16))) v4u smem[4096];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int t0 = blockIdx.x * 128, chunk = blockIdx.y;
   const int vt0 = chunk * vt_per_chunk, vt1 = min(n_vt, vt0 + vt_per_chunk);
   const int token = t0 + w * 32 + (lane & 31);
-  const float A = lse[min(token, rows - 1)];
-  float Fa[GMAX], Sa[GMAX];
+  const float Ac = lse[min(token, rows - 1)] * kLog2e;
+  float T1[GMAX], S[GMAX];
 #pragma unroll
-  for (int g = 0; g < GMAX; ++g) { Fa[g] = 0.f; Sa[g] = 0.f; }
-  f32x16_t a[4], p[4], b[4];
+  for (int g = 0; g < GMAX; ++g) { T1[g] = 0.f; S[g] = 0.f; }
+  f32x16_t a[4], b[4];
   for (int vt = vt0; vt < vt1; ++vt) {
-    logit_tile(W, Xc, vt * 128, t0, rows, d, smem, smem + 2048, a);
+    // g = -1 computes the clean tile (kept in a), then each pass g reuses it
+    for (int g = -1; g < G; ++g) {
+      logit_tile(W, g < 0 ? Xc : Xp + (int64_t)g * pass_stride, vt * 128, t0, d, smem, smem + 2048, b);
+      if (g < 0) {
 #pragma unroll
-    for (int vb = 0; vb < 4; ++vb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) p[vb][i] = expf(a[vb][i] - A);
-    for (int g = 0; g < G; ++g) {
-      logit_tile(W, Xp + (int64_t)g * pass_stride, vt * 128, t0, rows, d, smem, smem + 2048, b);
-      float fs = 0.f, ss = 0.f;
+        for (int vb = 0; vb < 4; ++vb) a[vb] = b[vb];
+        continue;
+      }
+      float t1 = 0.f, s2 = 0.f;
 #pragma unroll
       for (int vb = 0; vb < 4; ++vb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const float dl = a[vb][i] - b[vb][i];
-          const float f = kl_f(dl);
-          fs = fmaf(p[vb][i], f, fs);
-          ss = fmaf(p[vb][i], f - dl, ss);
+          const float av = a[vb][i];
+          const float p = __builtin_amdgcn_exp2f(fmaf(av, kLog2e, -Ac));
+          const float dl = av - b[vb][i];
+          const float e = __builtin_amdgcn_exp2f(-dl * kLog2e) - 1.0f;
+          t1 = fmaf(p, dl, t1);
+          s2 = fmaf(p, e, s2);
         }
 #pragma unroll
       for (int j = 0; j < GMAX; ++j)
-        if (j == g) { Fa[j] += fs; Sa[j] += ss; }
+        if (j == g) { T1[j] += t1; S[j] += s2; }
     }
   }
 #pragma unroll
   for (int g = 0; g < GMAX; ++g) {
     if (g < G) {
-      const float F = Fa[g] + __shfl_xor(Fa[g], 32, 64);
-      const float S = Sa[g] + __shfl_xor(Sa[g], 32, 64);
-      if ((lane >> 5) == 0 && token < rows) part[((int64_t)chunk * G + g) * rows + token] = make_float2(F, S);
+      const float x = T1[g] + __shfl_xor(T1[g], 32, 64);
+      const float y = S[g] + __shfl_xor(S[g], 32, 64);
+      if ((lane >> 5) == 0 && token < rows) part[((int64_t)chunk * G + g) * rows + token] = make_float2(x, y);
     }
   }
 }
 
-// kl[g * rows + r] = sum_c F - g(sum_c S), fixed chunk order, double.
+// kl[g * rows + r] = sum_c T1 + log1p(sum_c S), fixed chunk order, double.
 __global__ void kl_merge_kernel(const float2* __restrict__ part, int n_chunks, int G, int rows, float* __restrict__ kl) {
   const int r = blockIdx.x * blockDim.x + threadIdx.x, g = blockIdx.y;
   if (r >= rows) return;
-  double F = 0.0, S = 0.0;
+  double t1 = 0.0, s = 0.0;
   for (int c = 0; c < n_chunks; ++c) {
     const float2 v = part[((int64_t)c * G + g) * rows + r];
-    F += v.x;
-    S += v.y;
+    t1 += v.x;
+    s += v.y;
   }
-  kl[(int64_t)g * rows + r] = (float)(F - (S - log1p(S)));
+  kl[(int64_t)g * rows + r] = (float)(t1 + log1p(s));
 }
 
 int lm_chunks(int rows, int vocab) {

@@ -1,0 +1,78 @@
+// Block-tile machinery shared by the bf16 GEMM-shaped kernels (projections and
+// the LM head): tiles of A[M, K] and B[N, K] (K contiguous) are streamed straight
+// from global memory into LDS with global_load_lds_dwordx4 (no staging registers)
+// and consumed by v_mfma_f32_32x32x16_bf16.
+//
+// LDS tile layout: a BR x 64 bf16 tile is BR rows of eight 16-byte chunks; chunk
+// kc of row r sits at slot r*8 + (kc ^ (r & 7)), so the 32 lanes that read one
+// k-chunk of 32 consecutive rows hit 8 distinct slots per row group.  One wave
+// instruction fills 64 consecutive slots (lane l -> slot base + l, as the
+// hardware places them), i.e. 8 rows; lane l therefore reads row (l >> 3) of its
+// 8-row group at logical chunk (l & 7) ^ (l >> 3).
+//
+// Callers guarantee that all BR rows of every tile are readable (activation
+// buffers are padded to a multiple of 256 rows; weight row counts are multiples
+// of the tile), so the loads need no clamping.
+#pragma once
+
+#include "rk_internal.h"
+
+namespace rk {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int kBK = 64;  // K elements per pipeline stage
+
+__device__ __forceinline__ void lds_dma16(const void* src, v4u* lds_base) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void*)lds_base, 16, 0, 0);
+}
+
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Per-lane source of a BR x 64 tile whose rows start at `rows0` (row stride ld
+// elements).  Round j of wave w covers rows 32 j + 8 w .. +7.
+struct TileSrc {
+  const char* p;      // this lane's address for round 0, k = 0
+  int64_t round_step; // bytes between rounds (32 rows)
+  __device__ __forceinline__ void init(const bf16_t* rows0, int64_t ld, int w, int lane) {
+    const int r = w * 8 + (lane >> 3);
+    const int kc = (lane & 7) ^ (lane >> 3);
+    p = reinterpret_cast<const char*>(rows0 + (int64_t)r * ld + kc * 8);
+    round_step = (int64_t)32 * ld * 2;
+  }
+  // issue the BR/32 rounds of k-step kt into the LDS tile at `dst`
+  template <int BR>
+  __device__ __forceinline__ void load(int kt, v4u* dst, int w) const {
+    const char* q = p + (int64_t)kt * (kBK * 2);
+#pragma unroll
+    for (int j = 0; j < BR / 32; ++j) lds_dma16(q + j * round_step, dst + (j * 4 + w) * 64);
+  }
+};
+
+// One 32x16 (or 16x32) bf16 fragment of row `row`, k-step ks, from a swizzled tile.
+__device__ __forceinline__ bf16x8_t frag(const v4u* tile, int row, int ks, int lane) {
+  const int ch = ks * 2 + (lane >> 5);
+  return __builtin_bit_cast(bf16x8_t, tile[row * 8 + (ch ^ (row & 7))]);
+}
+
+// Tile order for a 1-D grid of n_m x n_n tiles on 8 XCDs.  The dispatcher hands
+// workgroup g to XCD g % 8, so g is first renumbered to make each XCD's
+// workgroups a contiguous run of tile ids, and tile ids are then laid out in
+// groups of `group_m` tile-rows (column-major inside a group): the tiles one XCD
+// runs at the same time share a few A row-panels and B column-panels in its L2.
+__device__ __forceinline__ void xcd_tile(int g, int n_m, int n_n, int group_m, int* bm, int* bn) {
+  const int total = n_m * n_n;
+  const int q = total >> 3, r = total & 7;
+  const int xcd = g & 7, local = g >> 3;
+  const int t = xcd < r ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
+  const int per_group = group_m * n_n;
+  const int first = (t / per_group) * group_m;
+  const int gm = min(group_m, n_m - first);
+  const int in = t - (t / per_group) * per_group;
+  *bm = first + in % gm;
+  *bn = in / gm;
+}
+
+}  // namespace rk

@@ -34,13 +34,8 @@ struct AttnWork {
 #if defined(__HIPCC__)
 __device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
-// fp32 -> bf16, round to nearest even (NaN -> quiet NaN).
-__device__ __forceinline__ bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)0x7fc0;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
+// fp32 -> bf16, round to nearest even (gfx950 v_cvt_pk_bf16_f32; NaN stays NaN).
+__device__ __forceinline__ bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 
 __device__ __forceinline__ int seq_of_row(const SeqTable& st, int r) {
   int lo = 0, hi = st.n - 1;
@@ -70,7 +65,9 @@ hipError_t launch_embed(const void* emb, bool emb_bf16, const int32_t* tokens, f
                         hipStream_t s);
 hipError_t launch_rmsnorm(const float* h, const float* g, void* out, bool out_bf16, int rows, int d,
                           float eps, hipStream_t s);
-hipError_t launch_rope_table(float2* tab, int max_len, int head_dim, float theta, hipStream_t s);
+// Rotary table of a batch: tab[t * head_dim/2 + j] = (cos, sin)(t * theta^(-2j/head_dim)) for
+// t < max_len, and pos[r] = position of row r inside its sequence.
+hipError_t launch_rope_table(float2* tab, int32_t* pos, const SeqTable& st, int head_dim, float theta, hipStream_t s);
 hipError_t launch_value_noise(void* v, bool bf16, int64_t row_stride, const SeqTable& st, int n_kv_heads,
                               int head_dim, int layer, float alpha, uint64_t seed, int protect_head,
                               int protect_tail, hipStream_t s);
@@ -84,9 +81,12 @@ struct GemmArgs {
   Epi epi;
   void* out; int64_t ldo;         // output (act type, or fp32 for kResidual/kStoreF32)
   const float* res; int64_t ldr;  // kResidual: out = res + C (res may alias out)
-  // kStoreRope: columns < rope_cols are rotated with the table (pairs j, j + head_dim/2)
-  int rope_cols; int head_dim; const float2* rope_tab; SeqTable seq;
+  // kStoreRope: columns < rope_cols are rotated (pairs j, j + head_dim/2) with
+  // rope_tab[pos * head_dim/2 + j] = (cos, sin), pos = rope_pos[row]
+  int rope_cols; int head_dim; const float2* rope_tab; const int32_t* rope_pos;
   int d_ff;                        // kSwiGLU: gate rows [0, d_ff), up rows [d_ff, 2 d_ff)
+  int tile_m, tile_n;              // 0: automatic tile choice (bf16 path)
+  int group_m;                     // tile-rows per L2 group (0: default)
 };
 hipError_t launch_gemm(const GemmArgs& a, bool bf16, hipStream_t s);
 

@@ -75,7 +75,7 @@ class Runner:
         self.model.reference_forward(batch, cs, ws)
         return cs
 
-    def layer(self, batch, cs, layer, alpha, want_logits=False, want_kl=True, **kw):
+    def layer(self, batch, cs, layer, alpha, want_logits=False, want_kl=True, logits_rows=None, **kw):
         import torch
         import paper_2608_08684_amd as rk
         flags = kw.pop("flags", 0)
@@ -86,6 +86,8 @@ class Runner:
         lg = torch.empty(batch.rows, self.cfg.vocab, dtype=torch.float32, device="cuda") if want_logits else None
         self.model.profile_layer(batch, layer, alpha, cs, d, ws, kl_pos=kl, logits_out=lg, flags=flags, **kw)
         torch.cuda.synchronize()
+        if lg is not None and logits_rows is not None:
+            lg = lg[:logits_rows]
         return (d.cpu().numpy().astype(np.float64), None if kl is None else kl.cpu().numpy().astype(np.float64),
                 None if lg is None else lg.cpu().numpy())
 
