@@ -84,8 +84,8 @@ def cpu_baseline(w, W, toks, prefix: int = 2048):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="gpt2s-bf16")
     ap.add_argument("--max-group", type=int, default=12)
     ap.add_argument("--family", default="gemm_gate_up", help="kernel family for the roofline figure")

@@ -22,6 +22,10 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 
 SOURCES = ["api.cpp", "budgets.cpp", "elementwise.hip", "gemm.hip", "attention.hip", "lm_kl.hip"]
 ARCH = "gfx950"
+# Per-file code-generation options.  Attention keeps its MFMA accumulators in
+# ordinary VGPRs: its softmax reads and rescales them every tile, and the AGPR
+# form would copy them across register files around every MFMA.
+EXTRA = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def hipcc() -> str:
@@ -36,7 +40,7 @@ def _flags(src: str):
               "-Wno-unused-variable", "-Wno-unused-but-set-variable"]
     if src.endswith(".hip"):
         return common + [f"--offload-arch={ARCH}", "-x", "hip", "-Xclang", "-target-feature", "-Xclang",
-                         "-packed-fp32-ops", "-ffp-contract=fast"]
+                         "-packed-fp32-ops", "-ffp-contract=fast"] + EXTRA.get(src, [])
     return common + ["-x", "c++", "-D__HIP_PLATFORM_AMD__"]
 
 

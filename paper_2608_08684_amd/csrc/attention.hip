@@ -36,6 +36,11 @@ typedef uint32_t v2u __attribute__((ext_vector_type(2)));
 // kLazy / c (2^8 headroom in P), so most tiles skip the rescale of O and l.
 constexpr float kLazyLog2 = 8.0f;
 
+// XOR swizzle of the 16-byte chunks of V^T row dd: lanes that write one element of
+// eight rows dd = 8 c + e (c = 0..7) and lanes that read eight consecutive rows both
+// land on distinct chunks.
+__device__ __forceinline__ int vsw(int dd) { return (dd ^ (dd >> 3)) & 7; }
+
 template <int DH>
 __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict__ qkv, int64_t ldq,
                                                         bf16_t* __restrict__ out, int64_t ldo, SeqTable st,
@@ -47,7 +52,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
   constexpr int NLK = BKV * KCH / 256;      // K chunks loaded per thread
   constexpr int NLV = BKV * KCH / 512;      // V key-pair chunks loaded per thread
   __shared__ __attribute__((aligned(16))) v4u Ks[2][BKV * KCH];
-  __shared__ __attribute__((aligned(16))) v4u Vt[2][DH * 8];   // [d][64 keys], 16-byte chunks XOR-swizzled by d
+  __shared__ __attribute__((aligned(16))) v4u Vt[2][DH * 8];   // [d][64 keys], 16-byte chunks XOR-swizzled (vsw)
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31, hf = lane >> 5;
   const int item = wk.total - 1 - (int)blockIdx.x;
@@ -111,7 +116,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
         const uint32_t lo = (rv[2 * i][e >> 1] >> ((e & 1) * 16)) & 0xffffu;
         const uint32_t hi = (rv[2 * i + 1][e >> 1] >> ((e & 1) * 16)) & 0xffffu;
         // word index: row dd (32 words), chunk key/8 swizzled, word (key%8)/2 inside the chunk
-        vt[dd * 32 + (((key >> 3) ^ (dd & 7)) << 2) + ((key & 7) >> 1)] = lo | (hi << 16);
+        vt[dd * 32 + (((key >> 3) ^ vsw(dd)) << 2) + ((key & 7) >> 1)] = lo | (hi << 16);
       }
     }
   };
@@ -194,8 +199,8 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
           for (int db = 0; db < NDB; ++db) {
             const int dd = db * 32 + l32;
             const v2u* row = reinterpret_cast<const v2u*>(Vt[buf]) + dd * 16;
-            const v2u lo = row[(((kb >> 3) ^ (dd & 7)) << 1) + ((kb & 7) >> 2)];
-            const v2u hi = row[((((kb + 8) >> 3) ^ (dd & 7)) << 1) + ((kb & 7) >> 2)];
+            const v2u lo = row[(((kb >> 3) ^ vsw(dd)) << 1) + ((kb & 7) >> 2)];
+            const v2u hi = row[((((kb + 8) >> 3) ^ vsw(dd)) << 1) + ((kb & 7) >> 2)];
             const v4u vv = {lo[0], lo[1], hi[0], hi[1]};
             o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vv), pb, o[db], 0, 0, 0);
           }

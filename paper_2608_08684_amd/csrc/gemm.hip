@@ -127,14 +127,15 @@ __device__ __forceinline__ int b_row(int bn, int n, int d_ff) {
 }
 
 // --------------------------------------------------------------------------- bf16 MFMA kernel
-template <int BM, int BN, class E, bool SWIGLU>
+template <int BM, int BN, int BK, class E, bool SWIGLU>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict__ A, int64_t lda,
                                                         const bf16_t* __restrict__ B, int64_t ldb, int M, int K,
                                                         int d_ff, int n_bn, int group_m, E e) {
   constexpr int MI = BM / 64, NI = BN / 64;       // 32x32 blocks per wave (2x2 waves)
-  constexpr int AS = BM * 8, BS = BN * 8;         // 16-byte slots per stage
-  __shared__ __attribute__((aligned(16))) v4u smem[2 * (AS + BS)];
-  static_assert(64 * (BN + 4) * 4 <= 2 * (AS + BS) * 16, "staging tile must fit");
+  constexpr int CH = BK / 8;                      // 16-byte chunks per tile row
+  constexpr int AS = BM * CH, BS = BN * CH;       // 16-byte slots per stage
+  constexpr int PIPE = 2 * (AS + BS), STAGE_OUT = 64 * (BN + 4) / 4;
+  __shared__ __attribute__((aligned(16))) v4u smem[PIPE > STAGE_OUT ? PIPE : STAGE_OUT];
   v4u* As = smem;
   v4u* Bs = smem + 2 * AS;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31;
@@ -143,7 +144,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict
   xcd_tile((int)blockIdx.x, (M + BM - 1) / BM, n_bn, group_m, &bm_, &bn);
   const int m0 = bm_ * BM;
 
-  TileSrc sa, sb, su;
+  TileSrcT<BK> sa, sb, su;
   sa.init(A + (int64_t)m0 * lda, lda, w, lane);
   if (SWIGLU) {
     sb.init(B + (int64_t)bn * (BN / 2) * ldb, ldb, w, lane);
@@ -155,7 +156,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict
     sa.template load<BM>(kt, As + stage * AS, w);
     if (SWIGLU) {
       sb.template load<BN / 2>(kt, Bs + stage * BS, w);
-      su.template load<BN / 2>(kt, Bs + stage * BS + (BN / 2) * 8, w);
+      su.template load<BN / 2>(kt, Bs + stage * BS + (BN / 2) * CH, w);
     } else {
       sb.template load<BN>(kt, Bs + stage * BS, w);
     }
@@ -169,7 +170,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[mi][ni][i] = 0.f;
 
-  const int nk = K / kBK;
+  const int nk = K / BK;
   issue(0, 0);
   wait_vmem();
   __syncthreads();
@@ -182,17 +183,17 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict
     // while the MFMAs of slice ks run
     bf16x8_t af[2][MI], bfr[2][NI];
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi) af[0][mi] = frag(At, wm * (BM / 2) + mi * 32 + l32, 0, lane);
+    for (int mi = 0; mi < MI; ++mi) af[0][mi] = frag<CH>(At, wm * (BM / 2) + mi * 32 + l32, 0, lane);
 #pragma unroll
-    for (int ni = 0; ni < NI; ++ni) bfr[0][ni] = frag(Bt, wn * (BN / 2) + ni * 32 + l32, 0, lane);
+    for (int ni = 0; ni < NI; ++ni) bfr[0][ni] = frag<CH>(Bt, wn * (BN / 2) + ni * 32 + l32, 0, lane);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int ks = 0; ks < BK / 16; ++ks) {
       const int c = ks & 1;
-      if (ks < 3) {
+      if (ks + 1 < BK / 16) {
 #pragma unroll
-        for (int mi = 0; mi < MI; ++mi) af[c ^ 1][mi] = frag(At, wm * (BM / 2) + mi * 32 + l32, ks + 1, lane);
+        for (int mi = 0; mi < MI; ++mi) af[c ^ 1][mi] = frag<CH>(At, wm * (BM / 2) + mi * 32 + l32, ks + 1, lane);
 #pragma unroll
-        for (int ni = 0; ni < NI; ++ni) bfr[c ^ 1][ni] = frag(Bt, wn * (BN / 2) + ni * 32 + l32, ks + 1, lane);
+        for (int ni = 0; ni < NI; ++ni) bfr[c ^ 1][ni] = frag<CH>(Bt, wn * (BN / 2) + ni * 32 + l32, ks + 1, lane);
       }
       // keep the next slice's LDS reads ahead of this slice's MFMAs
       __builtin_amdgcn_sched_barrier(0);
@@ -298,12 +299,12 @@ static void pick_tile(const GemmArgs& a, bool swiglu, int* bm, int* bn_) {
   *bm = 128; *bn_ = 128;
 }
 
-template <int BM, int BN, class E, bool SWIGLU>
+template <int BM, int BN, int BK, class E, bool SWIGLU>
 static void go_bf16(const GemmArgs& a, const E& e, hipStream_t s) {
   const int nbn = SWIGLU ? a.d_ff / (BN / 2) : a.N / BN;
   const int nbm = (a.M + BM - 1) / BM;
   const int group_m = a.group_m > 0 ? a.group_m : 8;
-  gemm_bf16_kernel<BM, BN, E, SWIGLU><<<nbm * nbn, 256, 0, s>>>((const bf16_t*)a.A, a.lda, (const bf16_t*)a.B,
+  gemm_bf16_kernel<BM, BN, BK, E, SWIGLU><<<nbm * nbn, 256, 0, s>>>((const bf16_t*)a.A, a.lda, (const bf16_t*)a.B,
                                                                 a.ldb, a.M, a.K, a.d_ff, nbn, group_m, e);
 }
 
@@ -312,10 +313,13 @@ static hipError_t go(const GemmArgs& a, bool bf16, const E& e, hipStream_t s) {
   if (bf16) {
     int bm, bn;
     pick_tile(a, SWIGLU, &bm, &bn);
-    if (a.tile_m) { bm = a.tile_m; bn = a.tile_n; }
-    if (bm == 256 && bn == 256) go_bf16<256, 256, E, SWIGLU>(a, e, s);
-    else if (bm == 256 && bn == 128) go_bf16<256, 128, E, SWIGLU>(a, e, s);
-    else if (bm == 128 && bn == 128) go_bf16<128, 128, E, SWIGLU>(a, e, s);
+    int bk = 64;
+    if (a.tile_m) { bm = a.tile_m; bn = a.tile_n; bk = a.tile_k ? a.tile_k : 64; }
+    if (bm == 256 && bn == 256 && bk == 64) go_bf16<256, 256, 64, E, SWIGLU>(a, e, s);
+    else if (bm == 256 && bn == 128 && bk == 32) go_bf16<256, 128, 32, E, SWIGLU>(a, e, s);
+    else if (bm == 128 && bn == 256 && bk == 32) go_bf16<128, 256, 32, E, SWIGLU>(a, e, s);
+    else if (bm == 128 && bn == 128 && bk == 64) go_bf16<128, 128, 64, E, SWIGLU>(a, e, s);
+    else if (bm == 128 && bn == 128 && bk == 32) go_bf16<128, 128, 32, E, SWIGLU>(a, e, s);
     else return hipErrorInvalidValue;
   } else {
     const int nbn = SWIGLU ? a.d_ff / 64 : a.N / 128;

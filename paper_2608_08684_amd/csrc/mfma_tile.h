@@ -23,7 +23,7 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kBK = 64;  // K elements per pipeline stage
+constexpr int kBK = 64;  // default K elements per pipeline stage
 
 __device__ __forceinline__ void lds_dma16(const void* src, v4u* lds_base) {
   __builtin_amdgcn_global_load_lds(src, (lds_void*)lds_base, 16, 0, 0);
@@ -31,30 +31,41 @@ __device__ __forceinline__ void lds_dma16(const void* src, v4u* lds_base) {
 
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// Per-lane source of a BR x 64 tile whose rows start at `rows0` (row stride ld
-// elements).  Round j of wave w covers rows 32 j + 8 w .. +7.
-struct TileSrc {
-  const char* p;      // this lane's address for round 0, k = 0
-  int64_t round_step; // bytes between rounds (32 rows)
+// Chunk swizzle of a tile row with CH 16-byte chunks (CH = BK / 8).
+template <int CH>
+__device__ __forceinline__ int swz(int row) {
+  return CH == 8 ? (row & 7) : ((row >> 1) & 3);
+}
+
+// Per-lane source of a BR x BK tile whose rows start at `rows0` (row stride ld
+// elements).  One wave instruction fills 64 consecutive slots = 64 / CH rows;
+// round j of wave w covers rows (4 j + w) * (64 / CH) ...
+template <int BK = kBK>
+struct TileSrcT {
+  static constexpr int CH = BK / 8;
+  static constexpr int RPI = 64 / CH;  // rows per wave instruction
+  const char* p;
+  int64_t round_step;
   __device__ __forceinline__ void init(const bf16_t* rows0, int64_t ld, int w, int lane) {
-    const int r = w * 8 + (lane >> 3);
-    const int kc = (lane & 7) ^ (lane >> 3);
+    const int r = w * RPI + lane / CH;
+    const int kc = (lane % CH) ^ swz<CH>(lane / CH);
     p = reinterpret_cast<const char*>(rows0 + (int64_t)r * ld + kc * 8);
-    round_step = (int64_t)32 * ld * 2;
+    round_step = (int64_t)4 * RPI * ld * 2;
   }
-  // issue the BR/32 rounds of k-step kt into the LDS tile at `dst`
   template <int BR>
   __device__ __forceinline__ void load(int kt, v4u* dst, int w) const {
-    const char* q = p + (int64_t)kt * (kBK * 2);
+    const char* q = p + (int64_t)kt * (BK * 2);
 #pragma unroll
-    for (int j = 0; j < BR / 32; ++j) lds_dma16(q + j * round_step, dst + (j * 4 + w) * 64);
+    for (int j = 0; j < BR * CH / 256; ++j) lds_dma16(q + j * round_step, dst + (j * 4 + w) * 64);
   }
 };
+typedef TileSrcT<kBK> TileSrc;
 
-// One 32x16 (or 16x32) bf16 fragment of row `row`, k-step ks, from a swizzled tile.
+// One 32x16 (or 16x32) bf16 fragment of row `row`, k-slice ks, from a swizzled tile.
+template <int CH = 8>
 __device__ __forceinline__ bf16x8_t frag(const v4u* tile, int row, int ks, int lane) {
   const int ch = ks * 2 + (lane >> 5);
-  return __builtin_bit_cast(bf16x8_t, tile[row * 8 + (ch ^ (row & 7))]);
+  return __builtin_bit_cast(bf16x8_t, tile[row * CH + (ch ^ swz<CH>(row))]);
 }
 
 // Tile order for a 1-D grid of n_m x n_n tiles on 8 XCDs.  The dispatcher hands
