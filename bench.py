@@ -33,6 +33,53 @@ if ROOT not in sys.path:
 BF16_PEAK_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 HBM_PEAK_GBS = 8000.0         # MI355X HBM3E
 
+# HBM bytes per launch of a kernel family, from rocprofv3 FETCH_SIZE / WRITE_SIZE
+# counter runs of this benchmark scaled by a 1 GiB copy (see --derive-traffic and
+# profiles/).  Keyed by (family, workload); valid only while the kernel sources
+# hash to the recorded value, so a changed kernel reports null until re-measured.
+TRAFFIC = {
+    ("gemm_gate_up", "gpt2s-bf16"): {"bytes_per_launch": 327062709, "fetch_bytes": 226399413, "write_bytes": 100663296,
+                                     "sources": "97bd8a31f98a41ad"},
+}
+KERNEL_SOURCES = ["paper_2608_08684_amd/csrc/gemm.hip", "paper_2608_08684_amd/csrc/mfma_tile.h",
+                  "paper_2608_08684_amd/csrc/rk_internal.h"]
+FAMILY_KERNEL = {"gemm_gate_up": "EpiSwiGLU", "gemm_qkv": "EpiRope", "lm_kl": "lm_kl_kernel",
+                 "attention": "attn_bf16_kernel"}
+
+
+def sources_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def derive_traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, family):
+    """Per-launch HBM bytes of `family` from four rocprofv3 --pmc csv directories:
+    FETCH_SIZE and WRITE_SIZE of this benchmark, and of the --copy-calibration run
+    (1 GiB read and 1 GiB written per copy)."""
+    import csv
+    import glob
+
+    def per_dispatch(d, key):
+        vals = []
+        for f in glob.glob(os.path.join(d, "*counter_collection.csv")):
+            for r in csv.DictReader(open(f)):
+                if key in r["Kernel_Name"]:
+                    vals.append(float(r["Counter_Value"]) * 1024.0)
+        return sum(vals) / len(vals) if vals else float("nan")
+
+    copy_bytes = float(1 << 30)
+    f_scale = copy_bytes / per_dispatch(copy_fetch_dir, "copyBuffer")
+    w_scale = copy_bytes / per_dispatch(copy_write_dir, "copyBuffer")
+    key = FAMILY_KERNEL[family]
+    fetch = per_dispatch(fetch_dir, key) * f_scale
+    write = per_dispatch(write_dir, key) * w_scale
+    return {"kernel": family, "fetch_bytes": fetch, "write_bytes": write, "bytes_per_launch": fetch + write,
+            "fetch_scale": f_scale, "write_scale": w_scale, "sources": sources_hash()}
+
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
@@ -90,7 +137,14 @@ def main():
     ap.add_argument("--max-group", type=int, default=12)
     ap.add_argument("--family", default="gemm_gate_up", help="kernel family for the roofline figure")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy (calibrates HBM byte counters)")
+    ap.add_argument("--derive-traffic", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
+                    help="print the per-launch HBM bytes of --family from rocprofv3 --pmc csv directories")
     args = ap.parse_args()
+    if args.derive_traffic:
+        print(json.dumps(derive_traffic(*args.derive_traffic, args.family)))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the profile's passes are independent and "
               "would shard by sequence or layer, which this build does not implement", file=sys.stderr)
@@ -99,6 +153,15 @@ def main():
     import torch
     if not torch.cuda.is_available():
         raise SystemExit("no GPU visible: the benchmark needs an MI355X")
+    if args.copy_calibration:
+        n = 1 << 30
+        x = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        y = torch.empty_like(x)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        log(f"copied {n} bytes 3 times")
+        return
     import fixtures as F
     import paper_2608_08684_amd as rk
     from tests.gpu_helpers import make_batch, upload_weights
@@ -151,8 +214,12 @@ def main():
     n_pass_lm = G  # perturbed passes scored per LM-head launch (algorithmic: pert logits only)
     flops = family_flops(args.family, cfg, rows, n_pass_lm)
     achieved = flops / (fam_avg_ms / 1e3) / 1e12
+    traffic = None
+    rec = TRAFFIC.get((args.family, w.name))
+    if rec is not None and rec["sources"] == sources_hash():
+        traffic = rec["bytes_per_launch"]
     roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None,
+            "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": traffic,
             "kernel": args.family, "launches": launches, "avg_ms": round(fam_avg_ms, 4),
             "flop_per_launch": flops}
     log(f"{args.family}: {launches} launches, avg {fam_avg_ms:.4f} ms, {achieved:.1f} TFLOP/s")

@@ -87,11 +87,14 @@ struct EpiSwiGLU {
   O* out; int64_t ldo;
   template <int BN>
   __device__ void apply(int row, int bn, int c0, const float* cs) const {
+    // silu(g) = g / (1 + e^-g) with the hardware exp2 and reciprocal (about 1 ulp
+    // each); the product is rounded to bf16 (or stored fp32 on the fp32 path).
     float v[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const float g = cs[c0 + j], u = cs[BN / 2 + c0 + j];
-      v[j] = g / (1.0f + expf(-g)) * u;
+      const float sig = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-g * 1.4426950408889634f));
+      v[j] = g * sig * u;
     }
     store8(out + (int64_t)row * ldo + (int64_t)bn * (BN / 2) + c0, v);
   }
@@ -106,11 +109,11 @@ struct EpiStoreF32 {
   }
 };
 
-// Run the epilogue over 64 staged rows (row stride BN + 4 floats).
-template <int BN, class E>
+// Run the epilogue over 64 staged rows (row stride BN + 4 floats) with NT threads.
+template <int BN, class E, int NT = 256>
 __device__ __forceinline__ void run_epilogue(const E& e, const float* Cs, int row0, int M, int bn) {
   constexpr int TPR = E::out_cols(BN) / 8;
-  constexpr int RPP = 256 / TPR;
+  constexpr int RPP = NT / TPR;
   const int t = threadIdx.x;
   const int c0 = (t % TPR) * 8;
   for (int r = t / TPR; r < 64; r += RPP) {
@@ -127,24 +130,27 @@ __device__ __forceinline__ int b_row(int bn, int n, int d_ff) {
 }
 
 // --------------------------------------------------------------------------- bf16 MFMA kernel
-template <int BM, int BN, int BK, class E, bool SWIGLU>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict__ A, int64_t lda,
-                                                        const bf16_t* __restrict__ B, int64_t ldb, int M, int K,
-                                                        int d_ff, int n_bn, int group_m, E e) {
-  constexpr int MI = BM / 64, NI = BN / 64;       // 32x32 blocks per wave (2x2 waves)
+template <int BM, int BN, int BK, int NWM, int NWN, class E, bool SWIGLU>
+__global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t* __restrict__ A, int64_t lda,
+                                                                  const bf16_t* __restrict__ B, int64_t ldb, int M,
+                                                                  int K, int d_ff, int n_bn, int group_m, E e) {
+  constexpr int NW = NWM * NWN, NT = 64 * NW;
+  constexpr int WTM = BM / NWM, WTN = BN / NWN;   // wave tile
+  constexpr int MI = WTM / 32, NI = WTN / 32;     // 32x32 blocks per wave
   constexpr int CH = BK / 8;                      // 16-byte chunks per tile row
   constexpr int AS = BM * CH, BS = BN * CH;       // 16-byte slots per stage
   constexpr int PIPE = 2 * (AS + BS), STAGE_OUT = 64 * (BN + 4) / 4;
+  static_assert(WTM >= 64 && WTM % 64 == 0, "a 64-row staging slice must lie inside one wave row");
   __shared__ __attribute__((aligned(16))) v4u smem[PIPE > STAGE_OUT ? PIPE : STAGE_OUT];
   v4u* As = smem;
   v4u* Bs = smem + 2 * AS;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31;
-  const int wm = w >> 1, wn = w & 1;
+  const int wm = w / NWN, wn = w % NWN;
   int bm_, bn;
   xcd_tile((int)blockIdx.x, (M + BM - 1) / BM, n_bn, group_m, &bm_, &bn);
   const int m0 = bm_ * BM;
 
-  TileSrcT<BK> sa, sb, su;
+  TileSrcT<BK, NW> sa, sb, su;
   sa.init(A + (int64_t)m0 * lda, lda, w, lane);
   if (SWIGLU) {
     sb.init(B + (int64_t)bn * (BN / 2) * ldb, ldb, w, lane);
@@ -183,17 +189,17 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict
     // while the MFMAs of slice ks run
     bf16x8_t af[2][MI], bfr[2][NI];
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi) af[0][mi] = frag<CH>(At, wm * (BM / 2) + mi * 32 + l32, 0, lane);
+    for (int mi = 0; mi < MI; ++mi) af[0][mi] = frag<CH>(At, wm * WTM + mi * 32 + l32, 0, lane);
 #pragma unroll
-    for (int ni = 0; ni < NI; ++ni) bfr[0][ni] = frag<CH>(Bt, wn * (BN / 2) + ni * 32 + l32, 0, lane);
+    for (int ni = 0; ni < NI; ++ni) bfr[0][ni] = frag<CH>(Bt, wn * WTN + ni * 32 + l32, 0, lane);
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       const int c = ks & 1;
       if (ks + 1 < BK / 16) {
 #pragma unroll
-        for (int mi = 0; mi < MI; ++mi) af[c ^ 1][mi] = frag<CH>(At, wm * (BM / 2) + mi * 32 + l32, ks + 1, lane);
+        for (int mi = 0; mi < MI; ++mi) af[c ^ 1][mi] = frag<CH>(At, wm * WTM + mi * 32 + l32, ks + 1, lane);
 #pragma unroll
-        for (int ni = 0; ni < NI; ++ni) bfr[c ^ 1][ni] = frag<CH>(Bt, wn * (BN / 2) + ni * 32 + l32, ks + 1, lane);
+        for (int ni = 0; ni < NI; ++ni) bfr[c ^ 1][ni] = frag<CH>(Bt, wn * WTN + ni * 32 + l32, ks + 1, lane);
       }
       // keep the next slice's LDS reads ahead of this slice's MFMAs
       __builtin_amdgcn_sched_barrier(0);
@@ -213,8 +219,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict
   constexpr int CSS = BN + 4;
 #pragma unroll
   for (int slice = 0; slice < BM / 64; ++slice) {
-    const int owner = (slice * 64) / (BM / 2);
-    const int mi0 = (slice * 64 - owner * (BM / 2)) / 32;
+    const int owner = (slice * 64) / WTM;
+    const int mi0 = (slice * 64 - owner * WTM) / 32;
     if (wm == owner) {
 #pragma unroll
       for (int mm = 0; mm < 2; ++mm)
@@ -223,12 +229,12 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
             const int r = mm * 32 + (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
-            const int c = wn * (BN / 2) + ni * 32 + l32;
+            const int c = wn * WTN + ni * 32 + l32;
             Cs[r * CSS + c] = acc[mi0 + mm][ni][i];
           }
     }
     __syncthreads();
-    run_epilogue<BN>(e, Cs, m0 + slice * 64, M, bn);
+    run_epilogue<BN, E, NT>(e, Cs, m0 + slice * 64, M, bn);
     __syncthreads();
   }
 }
@@ -289,33 +295,34 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 }
 
 // --------------------------------------------------------------------------- dispatch
-// Tile choice (measured on MI355X): 256x256 pays off only with a long K loop and
-// enough tiles to fill the CUs; otherwise 128x128 at two workgroups per CU.
-static void pick_tile(const GemmArgs& a, bool swiglu, int* bm, int* bn_) {
-  const int n_cols = swiglu ? 2 * a.d_ff : a.N;
-  const int64_t tiles256 = (int64_t)(a.M + 255) / 256 * (n_cols / 256);
+// Tile choice (measured on MI355X over the decoder's projection shapes): a
+// 256x256 tile on 8 waves (2x4, 128x64 per wave) is the best or within a few
+// percent of the best everywhere it divides N; otherwise 128x128 on 4 waves.
+static void pick_tile(const GemmArgs& a, bool swiglu, int* bm, int* bn_, int* bk, int* waves) {
   const bool fits256 = swiglu ? (a.d_ff % 128 == 0) : (a.N % 256 == 0);
-  if (fits256 && a.K >= 2048 && tiles256 >= 512) { *bm = 256; *bn_ = 256; return; }
-  *bm = 128; *bn_ = 128;
+  if (fits256 && a.K % 64 == 0) { *bm = 256; *bn_ = 256; *bk = 64; *waves = 8; return; }
+  *bm = 128; *bn_ = 128; *bk = 64; *waves = 4;
 }
 
-template <int BM, int BN, int BK, class E, bool SWIGLU>
+template <int BM, int BN, int BK, class E, bool SWIGLU, int NWM = 2, int NWN = 2>
 static void go_bf16(const GemmArgs& a, const E& e, hipStream_t s) {
   const int nbn = SWIGLU ? a.d_ff / (BN / 2) : a.N / BN;
   const int nbm = (a.M + BM - 1) / BM;
   const int group_m = a.group_m > 0 ? a.group_m : 8;
-  gemm_bf16_kernel<BM, BN, BK, E, SWIGLU><<<nbm * nbn, 256, 0, s>>>((const bf16_t*)a.A, a.lda, (const bf16_t*)a.B,
-                                                                a.ldb, a.M, a.K, a.d_ff, nbn, group_m, e);
+  gemm_bf16_kernel<BM, BN, BK, NWM, NWN, E, SWIGLU><<<nbm * nbn, 64 * NWM * NWN, 0, s>>>(
+      (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.K, a.d_ff, nbn, group_m, e);
 }
 
 template <class E, bool SWIGLU>
 static hipError_t go(const GemmArgs& a, bool bf16, const E& e, hipStream_t s) {
   if (bf16) {
-    int bm, bn;
-    pick_tile(a, SWIGLU, &bm, &bn);
-    int bk = 64;
-    if (a.tile_m) { bm = a.tile_m; bn = a.tile_n; bk = a.tile_k ? a.tile_k : 64; }
-    if (bm == 256 && bn == 256 && bk == 64) go_bf16<256, 256, 64, E, SWIGLU>(a, e, s);
+    int bm, bn, bk, waves;
+    pick_tile(a, SWIGLU, &bm, &bn, &bk, &waves);
+    if (a.tile_m) { bm = a.tile_m; bn = a.tile_n; bk = a.tile_k ? a.tile_k : 64; waves = a.tile_waves ? a.tile_waves : 4; }
+    if (bm == 256 && bn == 256 && bk == 64 && waves == 8) go_bf16<256, 256, 64, E, SWIGLU, 2, 4>(a, e, s);
+    else if (bm == 256 && bn == 256 && bk == 32 && waves == 8) go_bf16<256, 256, 32, E, SWIGLU, 2, 4>(a, e, s);
+    else if (bm == 256 && bn == 128 && bk == 64 && waves == 8) go_bf16<256, 128, 64, E, SWIGLU, 2, 4>(a, e, s);
+    else if (bm == 256 && bn == 256 && bk == 64) go_bf16<256, 256, 64, E, SWIGLU>(a, e, s);
     else if (bm == 256 && bn == 128 && bk == 32) go_bf16<256, 128, 32, E, SWIGLU>(a, e, s);
     else if (bm == 128 && bn == 256 && bk == 32) go_bf16<128, 256, 32, E, SWIGLU>(a, e, s);
     else if (bm == 128 && bn == 128 && bk == 64) go_bf16<128, 128, 64, E, SWIGLU>(a, e, s);

@@ -40,7 +40,7 @@ __device__ __forceinline__ int swz(int row) {
 // Per-lane source of a BR x BK tile whose rows start at `rows0` (row stride ld
 // elements).  One wave instruction fills 64 consecutive slots = 64 / CH rows;
 // round j of wave w covers rows (4 j + w) * (64 / CH) ...
-template <int BK = kBK>
+template <int BK = kBK, int NW = 4>
 struct TileSrcT {
   static constexpr int CH = BK / 8;
   static constexpr int RPI = 64 / CH;  // rows per wave instruction
@@ -50,16 +50,18 @@ struct TileSrcT {
     const int r = w * RPI + lane / CH;
     const int kc = (lane % CH) ^ swz<CH>(lane / CH);
     p = reinterpret_cast<const char*>(rows0 + (int64_t)r * ld + kc * 8);
-    round_step = (int64_t)4 * RPI * ld * 2;
+    round_step = (int64_t)NW * RPI * ld * 2;
   }
+  // issue the k-step kt of a BR-row tile (NW waves, BR * CH / (64 NW) rounds)
   template <int BR>
   __device__ __forceinline__ void load(int kt, v4u* dst, int w) const {
+    static_assert(BR * CH % (64 * NW) == 0, "tile rows must fill whole rounds");
     const char* q = p + (int64_t)kt * (BK * 2);
 #pragma unroll
-    for (int j = 0; j < BR * CH / 256; ++j) lds_dma16(q + j * round_step, dst + (j * 4 + w) * 64);
+    for (int j = 0; j < BR * CH / (64 * NW); ++j) lds_dma16(q + j * round_step, dst + (j * NW + w) * 64);
   }
 };
-typedef TileSrcT<kBK> TileSrc;
+typedef TileSrcT<kBK, 4> TileSrc;
 
 // One 32x16 (or 16x32) bf16 fragment of row `row`, k-slice ks, from a swizzled tile.
 template <int CH = 8>

@@ -86,6 +86,7 @@ struct GemmArgs {
   int rope_cols; int head_dim; const float2* rope_tab; const int32_t* rope_pos;
   int d_ff;                        // kSwiGLU: gate rows [0, d_ff), up rows [d_ff, 2 d_ff)
   int tile_m, tile_n, tile_k;      // 0: automatic tile choice (bf16 path)
+  int tile_waves;                  // waves per workgroup of an explicit tile (4 or 8)
   int group_m;                     // tile-rows per L2 group (0: default)
 };
 hipError_t launch_gemm(const GemmArgs& a, bool bf16, hipStream_t s);
