@@ -24,8 +24,9 @@ SOURCES = ["api.cpp", "budgets.cpp", "elementwise.hip", "gemm.hip", "attention.h
 ARCH = "gfx950"
 # Per-file code-generation options.  Attention keeps its MFMA accumulators in
 # ordinary VGPRs: its softmax reads and rescales them every tile, and the AGPR
-# form would copy them across register files around every MFMA.
-EXTRA = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+# form would copy them across register files around every MFMA.  Its scores are
+# never NaN (masked keys are -inf), so max reductions need no NaN canonicalising.
+EXTRA = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-fno-honor-nans"]}
 
 
 def hipcc() -> str:

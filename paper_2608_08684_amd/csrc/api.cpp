@@ -204,6 +204,10 @@ static rk_status run_block(const rk_model* m, int l, const float* h_in, float* h
   g.epi = Epi::kStoreRope; g.out = b.qkv; g.ldo = m->qkv_cols;
   g.rope_cols = (c.n_heads + c.n_kv_heads) * c.head_dim; g.head_dim = c.head_dim; g.rope_tab = b.rope;
   g.rope_pos = b.rope_pos;
+  if (m->bf16) {  // the bf16 attention kernel takes queries pre-scaled to base-2 softmax units
+    g.q_cols = c.n_heads * c.head_dim;
+    g.q_scale = (float)(1.4426950408889634 / sqrt((double)c.head_dim));
+  }
   { Timed t("gemm_qkv", s); RK_TRY(launch_gemm(g, m->bf16, s)); }
   if (noise) {
     char* v = (char*)b.qkv + (size_t)(c.n_heads + c.n_kv_heads) * c.head_dim * act_bytes(m);

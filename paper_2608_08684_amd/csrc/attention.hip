@@ -4,19 +4,25 @@
 // hq / (H / H_kv).  With the Keys fixed the attention weights of the perturbed
 // layer equal the clean ones (Section 4.3); only the aggregated Values change.
 //
-// bf16 kernel (flash attention, fp32 online softmax):
-//   * one workgroup = 128 queries of one head (4 waves x 32 queries), keys in
-//     tiles of 64 staged in LDS (K row-major, V transposed), double-buffered;
-//   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16, so each lane owns one query
-//     column: the row max and row sum of the softmax are lane-local plus one
-//     exchange with the partner half-wave;
-//   * O^T = V^T P^T: the P^T operand is the lane's own S^T registers rounded to
-//     bf16 (keys 4h..4h+3 and 8+4h..8+4h+3 of each 16-key step); V^T is written
-//     to LDS as key pairs and read as two 8-byte pieces that match those keys;
-//   * masks only on diagonal / ragged tiles; the softmax scale is folded into
-//     one FMA before exp2; the running max is raised lazily (rescaling O only
-//     when a tile's max grows by more than 2^8);
-//   * work items run heaviest (latest q-block) first.
+// bf16 kernel (flash attention, fp32 online softmax in base 2):
+//   * the queries arrive pre-multiplied by log2(e) / sqrt(d_h) (the q|k|v
+//     projection's epilogue does it before rounding), so a score is already
+//     the exponent of 2;
+//   * one workgroup = 4 waves x 32 queries of one head; it runs a pair of
+//     128-query blocks (nqb - 1 - x, then x) so all pairs of a sequence cost the
+//     same, longest sequences first;
+//   * 64-key tiles of K and V go global -> LDS by buffer_load ... lds (no
+//     staging registers; rows past the sequence read as zero), double-buffered;
+//   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 with the accumulator started at
+//     -m (the running max), so each lane owns one query column and exp2 is
+//     applied to the MFMA result directly; m is raised lazily (only when a
+//     tile's max exceeds it by 2^8), with one exchange with the partner
+//     half-wave;
+//   * O^T = V^T P^T: P^T is the lane's own S^T registers rounded to bf16, and
+//     the V^T operand comes from the row-major V tile through ds_read_b64_tr_b16
+//     in the same key order; the softmax denominator is summed from the rounded
+//     P with v_dot2_f32_bf16, so the weights applied to V sum to one;
+//   * masks only on diagonal / ragged tiles.
 // fp32 kernel: one thread per (row, head), streaming keys; for the small fp32
 // model only.
 #include <math.h>
@@ -26,203 +32,247 @@
 namespace rk {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
-
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t v2u __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4;
 
-// Raw scores are kept unscaled; p = 2^((s - m) * c) with c = log2(e) / sqrt(d_h).
-// The running max m is only raised when a tile's max exceeds it by more than
-// kLazy / c (2^8 headroom in P), so most tiles skip the rescale of O and l.
-constexpr float kLazyLog2 = 8.0f;
+// A score may exceed the running max by up to 2^kLazy before m is raised.
+constexpr float kLazy = 8.0f;
 
-// XOR swizzle of the 16-byte chunks of V^T row dd: lanes that write one element of
-// eight rows dd = 8 c + e (c = 0..7) and lanes that read eight consecutive rows both
-// land on distinct chunks.
-__device__ __forceinline__ int vsw(int dd) { return (dd ^ (dd >> 3)) & 7; }
+typedef int32_t i32x4_t __attribute__((ext_vector_type(4)));
+
+// 16-byte global -> LDS copy of one wave (lane l lands at lds_base + 16 l); rows
+// past the descriptor's range read as zero.  Issued as inline assembly so the
+// compiler does not tie later LDS reads of the other buffer to it: the caller
+// waits with s_waitcnt vmcnt(0) and a barrier before the data is read.
+__device__ __forceinline__ void dma16(i32x4_t rsrc, uint32_t lds_base, uint32_t voff, int32_t soff) {
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+               :
+               : "v"(voff), "s"(rsrc), "s"(soff), "{m0}"(lds_base)
+               : "memory");
+}
+
+// s_waitcnt vmcnt(0) (gfx9 encoding: expcnt and lgkmcnt fields at their maximum)
+// as a builtin, so the compiler also knows that its own earlier loads are done
+__device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// 16-byte chunk swizzles of the K tile (read as 32 rows x one chunk) and of the
+// V tile (read by ds_read_b64_tr_b16 as 4 rows x 4 chunks per half-wave).
+__device__ __forceinline__ int k_swz(int row) { return row & 7; }
+template <int DH>
+__device__ __forceinline__ int v_swz(int row) { return DH == 128 ? ((row & 3) << 2) : 0; }
 
 template <int DH>
 __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict__ qkv, int64_t ldq,
                                                         bf16_t* __restrict__ out, int64_t ldo, SeqTable st,
-                                                        AttnWork wk, int H, int Hkv, float c_log2) {
+                                                        AttnWork wk, int H, int Hkv, int n_items) {
   constexpr int BQ = 128, BKV = 64;
-  constexpr int KCH = DH / 8;               // 16-byte chunks per K row
+  constexpr int CH = DH / 8;                // 16-byte chunks per row
   constexpr int NKS = DH / 16;              // k-steps of S^T
   constexpr int NDB = DH / 32;              // 32-row blocks of O^T
-  constexpr int NLK = BKV * KCH / 256;      // K chunks loaded per thread
-  constexpr int NLV = BKV * KCH / 512;      // V key-pair chunks loaded per thread
-  __shared__ __attribute__((aligned(16))) v4u Ks[2][BKV * KCH];
-  __shared__ __attribute__((aligned(16))) v4u Vt[2][DH * 8];   // [d][64 keys], 16-byte chunks XOR-swizzled (vsw)
+  constexpr int SLOTS = BKV * CH;           // 16-byte slots per tile
+  constexpr int NLD = SLOTS / 256;          // DMA instructions per thread, per tile and matrix
+  constexpr int ROWB = DH * 2;              // bytes per tile row
+  __shared__ __attribute__((aligned(16))) v4u Ks[2][SLOTS];
+  __shared__ __attribute__((aligned(16))) v4u Vs[2][SLOTS];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31, hf = lane >> 5;
-  const int item = wk.total - 1 - (int)blockIdx.x;
-  int k = 0;
+  const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // ---- work item: XCD-grouped so the query heads of one KV head share an L2
+  const int grp = H / Hkv;
+  int t_item;
+  {
+    const int g = blockIdx.x, x = g & 7, n = g >> 3;
+    t_item = (n / grp) * (8 * grp) + x * grp + n % grp;
+  }
+  if (t_item >= n_items) return;
+  const int item = t_item / H, hq = t_item - item * H, hk = hq / grp;
+  int j = 0;
   {
     int lo = 0, hi = st.n - 1;
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
       if (wk.cum[mid] <= item) lo = mid; else hi = mid - 1;
     }
-    k = lo;
+    j = lo;
   }
-  const int qb = item - wk.cum[k];
+  const int k = wk.order[j], x = item - wk.cum[j];
   const int row0 = st.off[k], T = st.off[k + 1] - row0;
-  const int q0 = qb * BQ;
-  const int hq = blockIdx.y, hk = hq / (H / Hkv);
-  const int64_t kcol = (int64_t)H * DH + (int64_t)hk * DH;
-  const int64_t vcol = (int64_t)(H + Hkv) * DH + (int64_t)hk * DH;
-  const int my_q = q0 + w * 32 + l32;
+  const int nqb = (T + BQ - 1) / BQ;
 
-  bf16x8_t qf[NKS];
+  // buffer descriptor over this sequence's rows (raw, stride 0): reads past row T - 1 return zero
+  i32x4_t rsrc;
   {
-    const bf16_t* qp = qkv + (int64_t)(row0 + min(my_q, T - 1)) * ldq + (int64_t)hq * DH + hf * 8;
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) qf[ks] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const v4u*>(qp + ks * 16));
+    const uint64_t base = (uint64_t)(qkv + (int64_t)row0 * ldq);
+    rsrc[0] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)base);
+    rsrc[1] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)(base >> 32));
+    rsrc[2] = __builtin_amdgcn_readfirstlane((int32_t)((int64_t)T * ldq * 2));
+    rsrc[3] = 0x00020000;
   }
-
-  const int kv_end = min(T, q0 + BQ);
-  const int n_tiles = (kv_end + BKV - 1) / BKV;
-
-  v4u rk[NLK], rv[2 * NLV];
-  auto gload = [&](int k0) {
+  const int kcol = (H + hk) * DH, vcol = (H + Hkv + hk) * DH;
+  uint32_t koff[NLD], voff[NLD];
 #pragma unroll
-    for (int i = 0; i < NLK; ++i) {
-      const int c = tid + 256 * i, key = c / KCH, ch = c % KCH;
-      const int64_t r = row0 + min(k0 + key, T - 1);
-      rk[i] = *reinterpret_cast<const v4u*>(qkv + r * ldq + kcol + ch * 8);
-    }
+  for (int i = 0; i < NLD; ++i) {
+    const int slot = (i * 4 + w) * 64 + lane, r = slot / CH, ph = slot % CH;
+    koff[i] = (uint32_t)(r * ldq * 2 + (kcol + (ph ^ k_swz(r)) * 8) * 2);
+    voff[i] = (uint32_t)(r * ldq * 2 + (vcol + (ph ^ v_swz<DH>(r)) * 8) * 2);
+  }
+  const uint32_t ks_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) v4u*)&Ks[0][0];
+  const uint32_t vs_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) v4u*)&Vs[0][0];
+  auto issue = [&](int k0, int b) {
+    const int so = __builtin_amdgcn_readfirstlane(k0 * (int)ldq * 2);
 #pragma unroll
-    for (int i = 0; i < NLV; ++i) {
-      const int c = tid + 256 * i, kp = c / KCH, ch = c % KCH;   // key pair kp: keys 2kp, 2kp+1
-      const int64_t r0 = row0 + min(k0 + 2 * kp, T - 1), r1 = row0 + min(k0 + 2 * kp + 1, T - 1);
-      rv[2 * i] = *reinterpret_cast<const v4u*>(qkv + r0 * ldq + vcol + ch * 8);
-      rv[2 * i + 1] = *reinterpret_cast<const v4u*>(qkv + r1 * ldq + vcol + ch * 8);
-    }
-  };
-  auto lstore = [&](int b) {
-#pragma unroll
-    for (int i = 0; i < NLK; ++i) {
-      const int c = tid + 256 * i, key = c / KCH, ch = c % KCH;
-      Ks[b][key * KCH + (ch ^ (key & 7))] = rk[i];
-    }
-    uint32_t* vt = reinterpret_cast<uint32_t*>(Vt[b]);
-#pragma unroll
-    for (int i = 0; i < NLV; ++i) {
-      const int c = tid + 256 * i, kp = c / KCH, ch = c % KCH;
-      const int key = 2 * kp;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int dd = ch * 8 + e;
-        const uint32_t lo = (rv[2 * i][e >> 1] >> ((e & 1) * 16)) & 0xffffu;
-        const uint32_t hi = (rv[2 * i + 1][e >> 1] >> ((e & 1) * 16)) & 0xffffu;
-        // word index: row dd (32 words), chunk key/8 swizzled, word (key%8)/2 inside the chunk
-        vt[dd * 32 + (((key >> 3) ^ vsw(dd)) << 2) + ((key & 7) >> 1)] = lo | (hi << 16);
-      }
+    for (int i = 0; i < NLD; ++i) {
+      const uint32_t o = (uint32_t)((b * SLOTS + (i * 4 + w) * 64) * 16);
+      dma16(rsrc, __builtin_amdgcn_readfirstlane(ks_lds + o), koff[i], so);
+      dma16(rsrc, __builtin_amdgcn_readfirstlane(vs_lds + o), voff[i], so);
     }
   };
 
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x16_t o[NDB];
+  // per-lane LDS byte offsets of the K fragments (row l32 of a 32-row block, chunk 2 ks + hf)
+  // and of the V^T fragments (ds_read_b64_tr_b16: lane (G, jj) reads row 4 (G / 2) + jj / 4
+  // of an 8-row group, columns db * 32 + 16 (G % 2) + 4 (jj % 4))
+  int kfo[NKS];
 #pragma unroll
-  for (int db = 0; db < NDB; ++db)
+  for (int ks = 0; ks < NKS; ++ks) kfo[ks] = l32 * ROWB + (((2 * ks + hf) ^ k_swz(l32)) << 4);
+  int vfo[NDB];
+  {
+    const int G = lane >> 4, jj = lane & 15, r = 4 * (G >> 1) + (jj >> 2);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
-
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  const int wave_qmin = q0 + w * 32, wave_qmax = wave_qmin + 31;
-  const float lazy = kLazyLog2 / c_log2;
-  for (int t = 0; t < n_tiles; ++t) {
-    const int buf = t & 1, k0 = t * BKV;
-    if (t + 1 < n_tiles) gload(k0 + BKV);
-    if (k0 <= wave_qmax) {
-      f32x16_t s[2];
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) s[rb][i] = 0.f;
-        const int key = rb * 32 + l32;
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, Ks[buf][key * KCH + ((2 * ks + hf) ^ (key & 7))]);
-          s[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s[rb], 0, 0, 0);
-        }
-      }
-      // masks only where a key can exceed the query or the sequence (wave-uniform test)
-      if (k0 + BKV - 1 > wave_qmin || k0 + BKV > T) {
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int key = k0 + rb * 32 + (i >> 2) * 8 + hf * 4 + (i & 3);
-            if (key > my_q || key >= T) s[rb][i] = -INFINITY;
-          }
-      }
-      float mx = s[0][0];
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[rb][i]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      if (__any(mx > m_run + lazy)) {
-        const float m_new = fmaxf(m_run, mx);
-        const float corr = __builtin_amdgcn_exp2f((m_run - m_new) * c_log2);
-        l_run *= corr;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) o[db][i] *= corr;
-        m_run = m_new;
-      }
-      const float mc = m_run * c_log2;
-      float rs = 0.f;
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[rb][i], c_log2, -mc));
-          s[rb][i] = p;
-          rs += p;
-        }
-      l_run += rs;
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-        for (int ss = 0; ss < 2; ++ss) {
-          bf16x8_t pb;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) pb[e] = (__bf16)s[rb][8 * ss + e];
-          // this lane's k-slots: keys 16*(2rb+ss) + 4hf + {0..3} and the same + 8
-          const int kb = rb * 32 + ss * 16 + hf * 4;
-#pragma unroll
-          for (int db = 0; db < NDB; ++db) {
-            const int dd = db * 32 + l32;
-            const v2u* row = reinterpret_cast<const v2u*>(Vt[buf]) + dd * 16;
-            const v2u lo = row[(((kb >> 3) ^ vsw(dd)) << 1) + ((kb & 7) >> 2)];
-            const v2u hi = row[((((kb + 8) >> 3) ^ vsw(dd)) << 1) + ((kb & 7) >> 2)];
-            const v4u vv = {lo[0], lo[1], hi[0], hi[1]};
-            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vv), pb, o[db], 0, 0, 0);
-          }
-        }
+    for (int db = 0; db < NDB; ++db) {
+      const int ch = 4 * db + 2 * (G & 1) + ((jj & 3) >> 1);
+      vfo[db] = r * ROWB + ((ch ^ v_swz<DH>(r)) << 4) + (jj & 1) * 8;
     }
-    if (t + 1 < n_tiles) lstore(buf ^ 1);
-    __syncthreads();
   }
 
-  const float l = l_run + __shfl_xor(l_run, 32, 64);
-  const float inv = 1.0f / l;
-  if (my_q < T) {
-    bf16_t* op = out + (int64_t)(row0 + my_q) * ldo + (int64_t)hq * DH;
+  const bf16x2_t ones = {(__bf16)1.0f, (__bf16)1.0f};
+  const int n_blocks = (x == nqb - 1 - x) ? 1 : 2;
+  for (int bi = 0; bi < n_blocks; ++bi) {
+    const int qb = bi == 0 ? nqb - 1 - x : x;
+    const int q0 = qb * BQ;
+    const int my_q = min(q0 + w * 32 + l32, T - 1);   // rows past T duplicate row T - 1
+    bf16x8_t qf[NKS];
+    {
+      const bf16_t* qp = qkv + (int64_t)(row0 + my_q) * ldq + (int64_t)hq * DH + hf * 8;
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks)
+        qf[ks] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const v4u*>(qp + ks * 16));
+    }
+    const int kv_end = min(T, q0 + BQ);
+    const int n_tiles = (kv_end + BKV - 1) / BKV;
+    const int wave_qmin = q0 + w * 32, wave_qmax = wave_qmin + 31;
+
+    f32x16_t o[NDB], negm;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) negm[i] = 0.f;
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        bf16x4_t u;
+      for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
+    float l_run = 0.f;
+
+    issue(0, 0);
+    wait_vm0();
+    __syncthreads();
+    for (int t = 0; t < n_tiles; ++t) {
+      const int buf = t & 1, k0 = t * BKV;
+      if (t + 1 < n_tiles) issue(k0 + BKV, buf ^ 1);
+      if (k0 <= wave_qmax) {
+        const char* kt = reinterpret_cast<const char*>(Ks[buf]);
+        f32x16_t s[2];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) u[e] = (__bf16)(o[db][g * 4 + e] * inv);
-        *reinterpret_cast<bf16x4_t*>(op + db * 32 + g * 8 + hf * 4) = u;
+        for (int rb = 0; rb < 2; ++rb) {
+          bf16x8_t a[NKS];
+#pragma unroll
+          for (int ks = 0; ks < NKS; ++ks)
+            a[ks] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const v4u*>(kt + rb * 32 * ROWB + kfo[ks]));
+          s[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], qf[0], negm, 0, 0, 0);
+#pragma unroll
+          for (int ks = 1; ks < NKS; ++ks) s[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks], qf[ks], s[rb], 0, 0, 0);
+        }
+        // masks only where a key can exceed the query or the sequence (wave-uniform test)
+        if (k0 + BKV - 1 > wave_qmin || k0 + BKV > T) {
+#pragma unroll
+          for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+              const int key = k0 + rb * 32 + (i >> 2) * 8 + hf * 4 + (i & 3);
+              if (key > my_q || key >= T) s[rb][i] = -INFINITY;
+            }
+        }
+        float mx = fmaxf(s[0][0], s[0][1]);
+#pragma unroll
+        for (int i = 2; i < 16; i += 2) mx = fmaxf(mx, fmaxf(s[0][i], s[0][i + 1]));
+#pragma unroll
+        for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(s[1][i], s[1][i + 1]));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        if (t == 0 || __any(mx > kLazy)) {
+          // raise the running max: by the tile max on the first tile, else where it grew past 2^kLazy
+          const float dm = (t == 0 || mx > kLazy) ? mx : 0.f;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            s[0][i] -= dm;
+            s[1][i] -= dm;
+            negm[i] -= dm;
+          }
+          if (t != 0) {
+            const float corr = __builtin_amdgcn_exp2f(-dm);
+            l_run *= corr;
+#pragma unroll
+            for (int db = 0; db < NDB; ++db)
+#pragma unroll
+              for (int i = 0; i < 16; ++i) o[db][i] *= corr;
+          }
+        }
+        const char* vt = reinterpret_cast<const char*>(Vs[buf]);
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int ss = 0; ss < 2; ++ss) {
+            bf16x8_t pb;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pb[e] = (__bf16)__builtin_amdgcn_exp2f(s[rb][8 * ss + e]);
+#pragma unroll
+            for (int e = 0; e < 8; e += 2) {
+              const bf16x2_t pr = {pb[e], pb[e + 1]};
+              l_run = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, l_run, false);
+            }
+            // k-slot hf * 8 + e of this MFMA is key rb*32 + ss*16 + 8 (e / 4) + 4 hf + e % 4
+            const int kr = (rb * 32 + ss * 16) * ROWB;
+#pragma unroll
+            for (int db = 0; db < NDB; ++db) {
+              const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vt + kr + vfo[db]));
+              const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vt + kr + 8 * ROWB + vfo[db]));
+              const v4u vv = {__builtin_bit_cast(v2u, lo)[0], __builtin_bit_cast(v2u, lo)[1],
+                              __builtin_bit_cast(v2u, hi)[0], __builtin_bit_cast(v2u, hi)[1]};
+              o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vv), pb, o[db], 0, 0, 0);
+            }
+          }
       }
+      wait_vm0();
+      __syncthreads();
+    }
+
+    const float l = l_run + __shfl_xor(l_run, 32, 64);
+    const float inv = 1.0f / l;
+    const int q_out = q0 + w * 32 + l32;
+    if (q_out < T) {
+      bf16_t* op = out + (int64_t)(row0 + q_out) * ldo + (int64_t)hq * DH;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          bf16x4_t u;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) u[e] = (__bf16)(o[db][g * 4 + e] * inv);
+          *reinterpret_cast<bf16x4_t*>(op + db * 32 + g * 8 + hf * 4) = u;
+        }
+    }
   }
 }
 
@@ -263,19 +313,36 @@ hipError_t launch_attention(const void* qkv, int64_t ldq, void* out, int64_t ldo
                             int n_kv_heads, int head_dim, bool bf16, hipStream_t s) {
   if (st.rows <= 0) return hipSuccess;
   if (bf16) {
+    // sequences by decreasing length; items = pairs of q-blocks
     AttnWork wk;
+    for (int k = 0; k < st.n; ++k) wk.order[k] = k;
+    for (int a = 1; a < st.n; ++a) {  // insertion sort, stable
+      const int v = wk.order[a], len = st.off[v + 1] - st.off[v];
+      int b = a;
+      while (b > 0 && st.off[wk.order[b - 1] + 1] - st.off[wk.order[b - 1]] < len) {
+        wk.order[b] = wk.order[b - 1];
+        --b;
+      }
+      wk.order[b] = v;
+    }
     wk.cum[0] = 0;
-    for (int k = 0; k < st.n; ++k) wk.cum[k + 1] = wk.cum[k] + (st.off[k + 1] - st.off[k] + 127) / 128;
+    for (int j = 0; j < st.n; ++j) {
+      const int k = wk.order[j], nqb = (st.off[k + 1] - st.off[k] + 127) / 128;
+      wk.cum[j + 1] = wk.cum[j] + (nqb + 1) / 2;
+    }
     wk.total = wk.cum[st.n];
     if (wk.total == 0) return hipSuccess;
-    const float c_log2 = (float)(1.4426950408889634 / sqrt((double)head_dim));
-    dim3 grid(wk.total, n_heads);
+    // the buffer descriptor covers one sequence's rows with 32-bit byte offsets
+    if ((int64_t)st.max_len * ldq * 2 >= ((int64_t)1 << 31) || n_heads % n_kv_heads != 0) return hipErrorInvalidValue;
+    const int grp = n_heads / n_kv_heads;
+    const int n_items = wk.total * n_heads;
+    const int grid = (n_items + 8 * grp - 1) / (8 * grp) * (8 * grp);
     if (head_dim == 128)
       attn_bf16_kernel<128><<<grid, 256, 0, s>>>((const bf16_t*)qkv, ldq, (bf16_t*)out, ldo, st, wk, n_heads,
-                                                 n_kv_heads, c_log2);
+                                                 n_kv_heads, n_items);
     else if (head_dim == 64)
       attn_bf16_kernel<64><<<grid, 256, 0, s>>>((const bf16_t*)qkv, ldq, (bf16_t*)out, ldo, st, wk, n_heads,
-                                                n_kv_heads, c_log2);
+                                                n_kv_heads, n_items);
     else
       return hipErrorInvalidValue;
   } else {

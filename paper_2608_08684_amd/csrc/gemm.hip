@@ -38,7 +38,7 @@ template <typename O>
 struct EpiRope {
   static constexpr int out_cols(int BN) { return BN; }
   // tab[pos * head_dim/2 + j] = (cos, sin) of position pos, pair j; pos[row] = position of the row
-  O* out; int64_t ldo; int rope_cols; int head_dim; const float2* tab; const int32_t* pos;
+  O* out; int64_t ldo; int rope_cols; int head_dim; const float2* tab; const int32_t* pos; int q_cols; float q_scale;
   template <int BN>
   __device__ void apply(int row, int bn, int c0, const float* cs) const {
     const int gc0 = bn * BN + c0;
@@ -56,12 +56,13 @@ struct EpiRope {
     const float* x = cs + c0;
     const float* y = cs + c0 + (lo ? half : -half);
     const float sg = lo ? -1.0f : 1.0f;
+    const float sc = gc0 < q_cols ? q_scale : 1.0f;
     float v[8];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const float4 t = t4[q];  // (cos, sin) of pairs 2q and 2q+1
-      v[2 * q] = fmaf(sg * y[2 * q], t.y, x[2 * q] * t.x);
-      v[2 * q + 1] = fmaf(sg * y[2 * q + 1], t.w, x[2 * q + 1] * t.z);
+      v[2 * q] = fmaf(sg * y[2 * q], t.y, x[2 * q] * t.x) * sc;
+      v[2 * q + 1] = fmaf(sg * y[2 * q + 1], t.w, x[2 * q + 1] * t.z) * sc;
     }
     store8(dst, v);
   }
@@ -342,10 +343,10 @@ hipError_t launch_gemm(const GemmArgs& a, bool bf16, hipStream_t s) {
   switch (a.epi) {
     case Epi::kStoreRope:
       if (bf16) {
-        EpiRope<bf16_t> e{(bf16_t*)a.out, a.ldo, a.rope_cols, a.head_dim, a.rope_tab, a.rope_pos};
+        EpiRope<bf16_t> e{(bf16_t*)a.out, a.ldo, a.rope_cols, a.head_dim, a.rope_tab, a.rope_pos, a.q_cols, a.q_scale};
         return go<EpiRope<bf16_t>, false>(a, true, e, s);
       } else {
-        EpiRope<float> e{(float*)a.out, a.ldo, a.rope_cols, a.head_dim, a.rope_tab, a.rope_pos};
+        EpiRope<float> e{(float*)a.out, a.ldo, a.rope_cols, a.head_dim, a.rope_tab, a.rope_pos, a.q_cols, a.q_scale};
         return go<EpiRope<float>, false>(a, false, e, s);
       }
     case Epi::kResidual: {

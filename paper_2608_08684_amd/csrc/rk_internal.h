@@ -24,10 +24,13 @@ struct SeqTable {
   int32_t off[RK_MAX_BATCH_SEQS + 1];
 };
 
-// Work list of the attention kernel: q-blocks of all sequences, flattened.
+// Work list of the bf16 attention kernel.  A work item is a pair of q-blocks of
+// one sequence, (nqb - 1 - x, x), so every item of a sequence costs about the
+// same; sequences are visited longest first.
 struct AttnWork {
-  int32_t total;                         // number of (sequence, q-block) items
-  int32_t cum[RK_MAX_BATCH_SEQS + 1];    // cum[k] = q-blocks of sequences < k
+  int32_t total;                          // work items (pairs) over all sequences
+  int32_t order[RK_MAX_BATCH_SEQS];       // sequence indices by decreasing length
+  int32_t cum[RK_MAX_BATCH_SEQS + 1];     // cum[j] = pairs of sequences order[0..j)
 };
 
 // --------------------------------------------------------------------------- device helpers
@@ -84,6 +87,9 @@ struct GemmArgs {
   // kStoreRope: columns < rope_cols are rotated (pairs j, j + head_dim/2) with
   // rope_tab[pos * head_dim/2 + j] = (cos, sin), pos = rope_pos[row]
   int rope_cols; int head_dim; const float2* rope_tab; const int32_t* rope_pos;
+  // kStoreRope: columns < q_cols (the queries) are multiplied by q_scale after the
+  // rotation, before rounding (q_cols = 0: no scaling)
+  int q_cols; float q_scale;
   int d_ff;                        // kSwiGLU: gate rows [0, d_ff), up rows [d_ff, 2 d_ff)
   int tile_m, tile_n, tile_k;      // 0: automatic tile choice (bf16 path)
   int tile_waves;                  // waves per workgroup of an explicit tile (4 or 8)
