@@ -12,7 +12,8 @@
 //     128-query blocks (nqb - 1 - x, then x) so all pairs of a sequence cost the
 //     same, longest sequences first;
 //   * 64-key tiles of K and V go global -> LDS by buffer_load ... lds (no
-//     staging registers; rows past the sequence read as zero), double-buffered;
+//     staging registers; rows past the sequence read as zero) through a
+//     ring of 2-3 stages;
 //   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 with the accumulator started at
 //     -m (the running max), so each lane owns one query column and exp2 is
 //     applied to the MFMA result directly; m is raised lazily (only when a
@@ -59,15 +60,31 @@ __device__ __forceinline__ void dma16(i32x4_t rsrc, uint32_t lds_base, uint32_t 
 // s_waitcnt vmcnt(0) (gfx9 encoding: expcnt and lgkmcnt fields at their maximum)
 // as a builtin, so the compiler also knows that its own earlier loads are done
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// s_waitcnt vmcnt(N), N < 16
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
 
-// 16-byte chunk swizzles of the K tile (read as 32 rows x one chunk) and of the
-// V tile (read by ds_read_b64_tr_b16 as 4 rows x 4 chunks per half-wave).
-__device__ __forceinline__ int k_swz(int row) { return row & 7; }
+// 16-byte chunk swizzles that keep the LDS reads free of bank conflicts (64
+// banks of 4 bytes): the K tile is read as 16 rows x one chunk per quarter-wave,
+// the V tile by ds_read_b64_tr_b16 as 4 rows x 4 chunks per half-wave.
 template <int DH>
-__device__ __forceinline__ int v_swz(int row) { return DH == 128 ? ((row & 3) << 2) : 0; }
+__device__ __forceinline__ int k_swz(int row) { return DH == 128 ? (row & 15) : ((row >> 1) & 7); }
+template <int DH>
+__device__ __forceinline__ int v_swz(int row) { return DH == 128 ? ((row & 3) << 2) : (((row >> 1) & 1) << 2); }
+
+// K/V tile ring depth: three stages (prefetch two tiles ahead) where the LDS
+// allows three workgroups per CU, two for d_h = 128.
+template <int DH>
+struct AttnTraits {
+  static constexpr int kStages = DH == 64 ? 3 : 2;
+  static constexpr int kMinBlocks = DH == 64 ? 3 : 2;
+};
 
 template <int DH>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict__ qkv, int64_t ldq,
+__global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_kernel(const bf16_t* __restrict__ qkv, int64_t ldq,
                                                         bf16_t* __restrict__ out, int64_t ldo, SeqTable st,
                                                         AttnWork wk, int H, int Hkv, int n_items) {
   constexpr int BQ = 128, BKV = 64;
@@ -77,8 +94,9 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
   constexpr int SLOTS = BKV * CH;           // 16-byte slots per tile
   constexpr int NLD = SLOTS / 256;          // DMA instructions per thread, per tile and matrix
   constexpr int ROWB = DH * 2;              // bytes per tile row
-  __shared__ __attribute__((aligned(16))) v4u Ks[2][SLOTS];
-  __shared__ __attribute__((aligned(16))) v4u Vs[2][SLOTS];
+  constexpr int S = AttnTraits<DH>::kStages;
+  __shared__ __attribute__((aligned(16))) v4u Ks[S][SLOTS];
+  __shared__ __attribute__((aligned(16))) v4u Vs[S][SLOTS];
 
   const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -119,7 +137,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
 #pragma unroll
   for (int i = 0; i < NLD; ++i) {
     const int slot = (i * 4 + w) * 64 + lane, r = slot / CH, ph = slot % CH;
-    koff[i] = (uint32_t)(r * ldq * 2 + (kcol + (ph ^ k_swz(r)) * 8) * 2);
+    koff[i] = (uint32_t)(r * ldq * 2 + (kcol + (ph ^ k_swz<DH>(r)) * 8) * 2);
     voff[i] = (uint32_t)(r * ldq * 2 + (vcol + (ph ^ v_swz<DH>(r)) * 8) * 2);
   }
   const uint32_t ks_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) v4u*)&Ks[0][0];
@@ -139,7 +157,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
   // of an 8-row group, columns db * 32 + 16 (G % 2) + 4 (jj % 4))
   int kfo[NKS];
 #pragma unroll
-  for (int ks = 0; ks < NKS; ++ks) kfo[ks] = l32 * ROWB + (((2 * ks + hf) ^ k_swz(l32)) << 4);
+  for (int ks = 0; ks < NKS; ++ks) kfo[ks] = l32 * ROWB + (((2 * ks + hf) ^ k_swz<DH>(l32)) << 4);
   int vfo[NDB];
   {
     const int G = lane >> 4, jj = lane & 15, r = 4 * (G >> 1) + (jj >> 2);
@@ -176,12 +194,17 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
       for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
     float l_run = 0.f;
 
-    issue(0, 0);
-    wait_vm0();
-    __syncthreads();
+    wait_vm0();   // the query fragments are in registers before the ring starts
+#pragma unroll
+    for (int p = 0; p < S - 1; ++p)
+      if (p < n_tiles) issue(p * BKV, p);
+    int buf = 0, nbuf = S - 1;   // ring slots of tile t and of tile t + S - 1
     for (int t = 0; t < n_tiles; ++t) {
-      const int buf = t & 1, k0 = t * BKV;
-      if (t + 1 < n_tiles) issue(k0 + BKV, buf ^ 1);
+      const int k0 = t * BKV;
+      // tile t has landed once at most the S - 2 later tiles are in flight
+      if (t + S - 2 < n_tiles) wait_vm<(S - 2) * 2 * NLD>(); else wait_vm0();
+      __syncthreads();   // ... for every wave; and tile t - 1's slot is free again
+      if (t + S - 1 < n_tiles) issue(k0 + (S - 1) * BKV, nbuf);
       if (k0 <= wave_qmax) {
         const char* kt = reinterpret_cast<const char*>(Ks[buf]);
         f32x16_t s[2];
@@ -254,9 +277,10 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
             }
           }
       }
-      wait_vm0();
-      __syncthreads();
+      buf = buf == S - 1 ? 0 : buf + 1;
+      nbuf = nbuf == S - 1 ? 0 : nbuf + 1;
     }
+    __syncthreads();   // the next q-block refills the ring
 
     const float l = l_run + __shfl_xor(l_run, 32, 64);
     const float inv = 1.0f / l;

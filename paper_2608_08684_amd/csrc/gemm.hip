@@ -131,7 +131,7 @@ __device__ __forceinline__ int b_row(int bn, int n, int d_ff) {
 }
 
 // --------------------------------------------------------------------------- bf16 MFMA kernel
-template <int BM, int BN, int BK, int NWM, int NWN, class E, bool SWIGLU>
+template <int BM, int BN, int BK, int NWM, int NWN, int STAGES, class E, bool SWIGLU>
 __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t* __restrict__ A, int64_t lda,
                                                                   const bf16_t* __restrict__ B, int64_t ldb, int M,
                                                                   int K, int d_ff, int n_bn, int group_m, E e) {
@@ -140,11 +140,14 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t*
   constexpr int MI = WTM / 32, NI = WTN / 32;     // 32x32 blocks per wave
   constexpr int CH = BK / 8;                      // 16-byte chunks per tile row
   constexpr int AS = BM * CH, BS = BN * CH;       // 16-byte slots per stage
-  constexpr int PIPE = 2 * (AS + BS), STAGE_OUT = 64 * (BN + 4) / 4;
+  constexpr int PIPE = STAGES * (AS + BS), STAGE_OUT = 64 * (BN + 4) / 4;
+  // DMA instructions per thread and stage (A tile, then B tile or its gate and up halves)
+  constexpr int NL = (BM * CH + BN * CH) / (64 * NW);
+  static_assert(STAGES >= 2 && (STAGES - 2) * NL < 16, "ring depth");
   static_assert(WTM >= 64 && WTM % 64 == 0, "a 64-row staging slice must lie inside one wave row");
   __shared__ __attribute__((aligned(16))) v4u smem[PIPE > STAGE_OUT ? PIPE : STAGE_OUT];
   v4u* As = smem;
-  v4u* Bs = smem + 2 * AS;
+  v4u* Bs = smem + STAGES * AS;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31;
   const int wm = w / NWN, wn = w % NWN;
   int bm_, bn;
@@ -159,15 +162,27 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t*
   } else {
     sb.init(B + (int64_t)bn * BN * ldb, ldb, w, lane);
   }
-  auto issue = [&](int kt, int stage) {
-    sa.template load<BM>(kt, As + stage * AS, w);
-    if (SWIGLU) {
-      sb.template load<BN / 2>(kt, Bs + stage * BS, w);
-      su.template load<BN / 2>(kt, Bs + stage * BS + (BN / 2) * CH, w);
+  // The NL copy instructions of one stage, numbered: A rounds, then B rounds (for
+  // SwiGLU: gate rounds, then up rounds).  They are spread over the k-slices of
+  // the previous k-step so the vector memory pipe never holds a wave back for long.
+  constexpr int NA = BM * CH / (64 * NW), NB = BN * CH / (64 * NW);
+  auto issue_one = [&](int kt, int stage, int j) {
+    if (j < NA) {
+      sa.load_round(kt, j, As + stage * AS, w);
+    } else if (SWIGLU) {
+      const int jb = j - NA;
+      if (jb < NB / 2) sb.load_round(kt, jb, Bs + stage * BS, w);
+      else su.load_round(kt, jb - NB / 2, Bs + stage * BS + (BN / 2) * CH, w);
     } else {
-      sb.template load<BN>(kt, Bs + stage * BS, w);
+      sb.load_round(kt, j - NA, Bs + stage * BS, w);
     }
   };
+  auto issue = [&](int kt, int stage) {
+#pragma unroll
+    for (int j = 0; j < NL; ++j) issue_one(kt, stage, j);
+  };
+  constexpr int NKS = BK / 16;                       // k-slices per k-step
+  constexpr int PER = (NL + NKS - 1) / NKS;          // copies issued per k-slice
 
   f32x16_t acc[MI][NI];
 #pragma unroll
@@ -177,32 +192,39 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t*
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[mi][ni][i] = 0.f;
 
+  // Ring of STAGES LDS stages: k-step kt + STAGES - 1 is in flight while kt is consumed.
   const int nk = K / BK;
-  issue(0, 0);
-  wait_vmem();
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) issue(kt + 1, cur ^ 1);
+#pragma unroll
+  for (int p = 0; p < STAGES - 1; ++p)
+    if (p < nk) issue(p, p);
+  // One k-step.  Fragments are double-buffered in registers: the LDS reads of
+  // k-slice ks+1 and this k-step's share of the copies for k-step kt + STAGES - 1
+  // are issued ahead of the MFMAs of slice ks.
+  auto kstep = [&](int kt, int cur, int nxt, bool copy, bool tail) {
+    if (!tail) wait_vmem_le<(STAGES - 2) * NL>(); else wait_vmem();
+    __syncthreads();   // k-step kt is in LDS for every wave; the slot of kt - 1 is free
     const v4u* At = As + cur * AS;
     const v4u* Bt = Bs + cur * BS;
-    // fragments double-buffered in registers: k-slice ks+1 is read from LDS
-    // while the MFMAs of slice ks run
     bf16x8_t af[2][MI], bfr[2][NI];
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi) af[0][mi] = frag<CH>(At, wm * WTM + mi * 32 + l32, 0, lane);
 #pragma unroll
     for (int ni = 0; ni < NI; ++ni) bfr[0][ni] = frag<CH>(Bt, wn * WTN + ni * 32 + l32, 0, lane);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
+    for (int ks = 0; ks < NKS; ++ks) {
       const int c = ks & 1;
-      if (ks + 1 < BK / 16) {
+      if (ks + 1 < NKS) {
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) af[c ^ 1][mi] = frag<CH>(At, wm * WTM + mi * 32 + l32, ks + 1, lane);
 #pragma unroll
         for (int ni = 0; ni < NI; ++ni) bfr[c ^ 1][ni] = frag<CH>(Bt, wn * WTN + ni * 32 + l32, ks + 1, lane);
       }
-      // keep the next slice's LDS reads ahead of this slice's MFMAs
+      if (copy) {
+#pragma unroll
+        for (int j = ks * PER; j < (ks + 1) * PER; ++j)
+          if (j < NL) issue_one(kt + STAGES - 1, nxt, j);
+      }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi)
@@ -211,9 +233,18 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t*
           acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[c][mi], bfr[c][ni], acc[mi][ni], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
-    wait_vmem();
-    __syncthreads();
+  };
+  int cur = 0, nxt = STAGES - 1, kt = 0;
+  for (; kt + STAGES - 1 < nk; ++kt) {
+    kstep(kt, cur, nxt, true, false);
+    cur = cur == STAGES - 1 ? 0 : cur + 1;
+    nxt = nxt == STAGES - 1 ? 0 : nxt + 1;
   }
+  for (; kt < nk; ++kt) {
+    kstep(kt, cur, nxt, false, true);
+    cur = cur == STAGES - 1 ? 0 : cur + 1;
+  }
+  __syncthreads();   // the staging area below overlaps the ring
 
   // Stage 64 rows at a time and run the epilogue on whole rows.
   float* Cs = reinterpret_cast<float*>(smem);
@@ -297,38 +328,47 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 
 // --------------------------------------------------------------------------- dispatch
 // Tile choice (measured on MI355X over the decoder's projection shapes): a
-// 256x256 tile on 8 waves (2x4, 128x64 per wave) is the best or within a few
-// percent of the best everywhere it divides N; otherwise 128x128 on 4 waves.
-static void pick_tile(const GemmArgs& a, bool swiglu, int* bm, int* bn_, int* bk, int* waves) {
+// 256x256 tile on 8 waves (2x4, 128x64 per wave) wherever it divides N;
+// otherwise 128x128 on 4 waves.
+static void pick_tile(const GemmArgs& a, bool swiglu, int* bm, int* bn_, int* bk, int* waves, int* stages) {
   const bool fits256 = swiglu ? (a.d_ff % 128 == 0) : (a.N % 256 == 0);
-  if (fits256 && a.K % 64 == 0) { *bm = 256; *bn_ = 256; *bk = 64; *waves = 8; return; }
-  *bm = 128; *bn_ = 128; *bk = 64; *waves = 4;
+  if (fits256 && a.K % 64 == 0) { *bm = 256; *bn_ = 256; *bk = 64; *waves = 8; *stages = 2; return; }
+  *bm = 128; *bn_ = 128; *bk = 64; *waves = 4; *stages = 2;
 }
 
-template <int BM, int BN, int BK, class E, bool SWIGLU, int NWM = 2, int NWN = 2>
+template <int BM, int BN, int BK, int ST, class E, bool SWIGLU, int NWM = 2, int NWN = 2>
 static void go_bf16(const GemmArgs& a, const E& e, hipStream_t s) {
   const int nbn = SWIGLU ? a.d_ff / (BN / 2) : a.N / BN;
   const int nbm = (a.M + BM - 1) / BM;
   const int group_m = a.group_m > 0 ? a.group_m : 8;
-  gemm_bf16_kernel<BM, BN, BK, NWM, NWN, E, SWIGLU><<<nbm * nbn, 64 * NWM * NWN, 0, s>>>(
+  gemm_bf16_kernel<BM, BN, BK, NWM, NWN, ST, E, SWIGLU><<<nbm * nbn, 64 * NWM * NWN, 0, s>>>(
       (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.K, a.d_ff, nbn, group_m, e);
 }
 
 template <class E, bool SWIGLU>
 static hipError_t go(const GemmArgs& a, bool bf16, const E& e, hipStream_t s) {
   if (bf16) {
-    int bm, bn, bk, waves;
-    pick_tile(a, SWIGLU, &bm, &bn, &bk, &waves);
-    if (a.tile_m) { bm = a.tile_m; bn = a.tile_n; bk = a.tile_k ? a.tile_k : 64; waves = a.tile_waves ? a.tile_waves : 4; }
-    if (bm == 256 && bn == 256 && bk == 64 && waves == 8) go_bf16<256, 256, 64, E, SWIGLU, 2, 4>(a, e, s);
-    else if (bm == 256 && bn == 256 && bk == 32 && waves == 8) go_bf16<256, 256, 32, E, SWIGLU, 2, 4>(a, e, s);
-    else if (bm == 256 && bn == 128 && bk == 64 && waves == 8) go_bf16<256, 128, 64, E, SWIGLU, 2, 4>(a, e, s);
-    else if (bm == 256 && bn == 256 && bk == 64) go_bf16<256, 256, 64, E, SWIGLU>(a, e, s);
-    else if (bm == 256 && bn == 128 && bk == 32) go_bf16<256, 128, 32, E, SWIGLU>(a, e, s);
-    else if (bm == 128 && bn == 256 && bk == 32) go_bf16<128, 256, 32, E, SWIGLU>(a, e, s);
-    else if (bm == 128 && bn == 128 && bk == 64) go_bf16<128, 128, 64, E, SWIGLU>(a, e, s);
-    else if (bm == 128 && bn == 128 && bk == 32) go_bf16<128, 128, 32, E, SWIGLU>(a, e, s);
-    else return hipErrorInvalidValue;
+    int bm, bn, bk, waves, st;
+    pick_tile(a, SWIGLU, &bm, &bn, &bk, &waves, &st);
+    if (a.tile_m) {
+      bm = a.tile_m; bn = a.tile_n; bk = a.tile_k ? a.tile_k : 64; waves = a.tile_waves ? a.tile_waves : 4;
+      st = a.tile_stages ? a.tile_stages : 2;
+    }
+#define RK_TILE(BM_, BN_, BK_, W_, ST_, NWM_, NWN_)                                     \
+  if (bm == BM_ && bn == BN_ && bk == BK_ && waves == W_ && st == ST_) {                \
+    go_bf16<BM_, BN_, BK_, ST_, E, SWIGLU, NWM_, NWN_>(a, e, s);                        \
+    return hipGetLastError();                                                          \
+  }
+    RK_TILE(256, 256, 64, 8, 2, 2, 4)
+    RK_TILE(256, 256, 32, 8, 3, 2, 4)
+    RK_TILE(256, 256, 32, 8, 4, 2, 4)
+    RK_TILE(256, 128, 64, 8, 3, 2, 4)
+    RK_TILE(256, 256, 64, 4, 2, 2, 2)
+    RK_TILE(128, 128, 64, 4, 2, 2, 2)
+    RK_TILE(128, 128, 64, 4, 3, 2, 2)
+    RK_TILE(128, 256, 32, 4, 4, 2, 2)
+#undef RK_TILE
+    return hipErrorInvalidValue;
   } else {
     const int nbn = SWIGLU ? a.d_ff / 64 : a.N / 128;
     dim3 grid(nbn, (a.M + 63) / 64);

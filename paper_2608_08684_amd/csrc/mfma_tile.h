@@ -3,12 +3,14 @@
 // from global memory into LDS with global_load_lds_dwordx4 (no staging registers)
 // and consumed by v_mfma_f32_32x32x16_bf16.
 //
-// LDS tile layout: a BR x 64 bf16 tile is BR rows of eight 16-byte chunks; chunk
-// kc of row r sits at slot r*8 + (kc ^ (r & 7)), so the 32 lanes that read one
-// k-chunk of 32 consecutive rows hit 8 distinct slots per row group.  One wave
-// instruction fills 64 consecutive slots (lane l -> slot base + l, as the
-// hardware places them), i.e. 8 rows; lane l therefore reads row (l >> 3) of its
-// 8-row group at logical chunk (l & 7) ^ (l >> 3).
+// LDS tile layout: a BR x BK bf16 tile is BR rows of CH = BK / 8 16-byte chunks;
+// chunk kc of row r sits at slot r*CH + (kc ^ swz<CH>(r)).  A fragment read
+// (32 lanes reading one k-chunk of 32 consecutive rows) is serviced 16 lanes at
+// a time by 64 banks of 4 bytes, so the 16 rows of a quarter-wave must cover
+// all 16 bank quads: with 128-byte rows (CH = 8) two rows share a bank line and
+// the chunk is XORed with bits 1-3 of the row, with 64-byte rows (CH = 4) four
+// rows share it and bits 2-3 are used.  One wave instruction fills 64
+// consecutive slots (lane l -> slot base + l, as the hardware places them).
 //
 // Callers guarantee that all BR rows of every tile are readable (activation
 // buffers are padded to a multiple of 256 rows; weight row counts are multiples
@@ -31,15 +33,22 @@ __device__ __forceinline__ void lds_dma16(const void* src, v4u* lds_base) {
 
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// s_waitcnt vmcnt(N) for N < 16 (gfx9 encoding; expcnt and lgkmcnt left at their maximum)
+template <int N>
+__device__ __forceinline__ void wait_vmem_le() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
+
 // Chunk swizzle of a tile row with CH 16-byte chunks (CH = BK / 8).
 template <int CH>
 __device__ __forceinline__ int swz(int row) {
-  return CH == 8 ? (row & 7) : ((row >> 1) & 3);
+  return CH == 8 ? ((row >> 1) & 7) : ((row >> 2) & 3);
 }
 
 // Per-lane source of a BR x BK tile whose rows start at `rows0` (row stride ld
 // elements).  One wave instruction fills 64 consecutive slots = 64 / CH rows;
-// round j of wave w covers rows (4 j + w) * (64 / CH) ...
+// round j of wave w covers rows (NW j + w) * (64 / CH) ...
 template <int BK = kBK, int NW = 4>
 struct TileSrcT {
   static constexpr int CH = BK / 8;
@@ -48,7 +57,7 @@ struct TileSrcT {
   int64_t round_step;
   __device__ __forceinline__ void init(const bf16_t* rows0, int64_t ld, int w, int lane) {
     const int r = w * RPI + lane / CH;
-    const int kc = (lane % CH) ^ swz<CH>(lane / CH);
+    const int kc = (lane % CH) ^ swz<CH>(r);   // rounds add multiples of 16 rows: same swizzle
     p = reinterpret_cast<const char*>(rows0 + (int64_t)r * ld + kc * 8);
     round_step = (int64_t)NW * RPI * ld * 2;
   }
@@ -59,6 +68,10 @@ struct TileSrcT {
     const char* q = p + (int64_t)kt * (BK * 2);
 #pragma unroll
     for (int j = 0; j < BR * CH / (64 * NW); ++j) lds_dma16(q + j * round_step, dst + (j * NW + w) * 64);
+  }
+  // round j only (j < BR * CH / (64 NW))
+  __device__ __forceinline__ void load_round(int kt, int j, v4u* dst, int w) const {
+    lds_dma16(p + (int64_t)kt * (BK * 2) + j * round_step, dst + (j * NW + w) * 64);
   }
 };
 typedef TileSrcT<kBK, 4> TileSrc;

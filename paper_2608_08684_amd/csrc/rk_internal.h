@@ -93,6 +93,7 @@ struct GemmArgs {
   int d_ff;                        // kSwiGLU: gate rows [0, d_ff), up rows [d_ff, 2 d_ff)
   int tile_m, tile_n, tile_k;      // 0: automatic tile choice (bf16 path)
   int tile_waves;                  // waves per workgroup of an explicit tile (4 or 8)
+  int tile_stages;                 // LDS pipeline stages of an explicit tile (0: 2)
   int group_m;                     // tile-rows per L2 group (0: default)
 };
 hipError_t launch_gemm(const GemmArgs& a, bool bf16, hipStream_t s);
