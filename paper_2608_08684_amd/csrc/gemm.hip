@@ -4,9 +4,9 @@
 //   output / down     -> residual add into the fp32 stream,
 //   gate|up           -> SwiGLU (silu(gate) * up), written as one [M, d_ff] tile,
 //   LM head (unfused) -> plain fp32 logits.
-// bf16 path: BM x BN block tile (128x128, 256x128 or 256x256), 2x2 waves,
-// v_mfma_f32_32x32x16_bf16, K-step 64 streamed global -> LDS by
-// global_load_lds_dwordx4 into two stages (see mfma_tile.h).
+// bf16 path: BM x BN block tile (256x256 on 8 waves where it divides N, else
+// 128x128 on 4), v_mfma_f32_32x32x16_bf16, K-steps streamed global -> LDS by
+// buffer loads into a ring of LDS stages (see mfma_tile.h).
 // fp32 path: a VALU kernel with the same epilogues (64x128 tile).
 // Both stage the finished tile through LDS 64 rows at a time so each epilogue
 // sees whole rows (a rotary pair j, j + d_h/2 or a gate/up pair lies inside one

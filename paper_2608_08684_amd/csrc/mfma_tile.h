@@ -1,6 +1,6 @@
 // Block-tile machinery shared by the bf16 GEMM-shaped kernels (projections and
 // the LM head): tiles of A[M, K] and B[N, K] (K contiguous) are streamed straight
-// from global memory into LDS with global_load_lds_dwordx4 (no staging registers)
+// from global memory into LDS with buffer_load_dwordx4 ... lds (no staging registers)
 // and consumed by v_mfma_f32_32x32x16_bf16.
 //
 // LDS tile layout: a BR x BK bf16 tile is BR rows of CH = BK / 8 16-byte chunks;
@@ -24,12 +24,10 @@ namespace rk {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void;
+typedef int32_t i32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kBK = 64;  // default K elements per pipeline stage
 
-__device__ __forceinline__ void lds_dma16(const void* src, v4u* lds_base) {
-  __builtin_amdgcn_global_load_lds(src, (lds_void*)lds_base, 16, 0, 0);
-}
 
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
@@ -48,30 +46,46 @@ __device__ __forceinline__ int swz(int row) {
 
 // Per-lane source of a BR x BK tile whose rows start at `rows0` (row stride ld
 // elements).  One wave instruction fills 64 consecutive slots = 64 / CH rows;
-// round j of wave w covers rows (NW j + w) * (64 / CH) ...
+// round j of wave w covers rows (NW j + w) * (64 / CH) ...  The copies are
+// buffer_load_dwordx4 ... lds with the tile's base in an SGPR descriptor, a
+// per-lane 32-bit offset fixed at init, and the k-step and round in the scalar
+// offset, so issuing one costs no vector ALU work.  They are inline assembly:
+// the compiler neither counts them in its own waits nor orders later LDS reads
+// behind them, so callers wait with s_waitcnt vmcnt and a barrier themselves.
 template <int BK = kBK, int NW = 4>
 struct TileSrcT {
   static constexpr int CH = BK / 8;
   static constexpr int RPI = 64 / CH;  // rows per wave instruction
-  const char* p;
-  int64_t round_step;
+  i32x4_t rsrc;
+  uint32_t voff;
+  int32_t round_bytes;
   __device__ __forceinline__ void init(const bf16_t* rows0, int64_t ld, int w, int lane) {
     const int r = w * RPI + lane / CH;
     const int kc = (lane % CH) ^ swz<CH>(r);   // rounds add multiples of 16 rows: same swizzle
-    p = reinterpret_cast<const char*>(rows0 + (int64_t)r * ld + kc * 8);
-    round_step = (int64_t)NW * RPI * ld * 2;
+    const uint64_t base = (uint64_t)rows0;
+    rsrc[0] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)base);
+    rsrc[1] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)(base >> 32));
+    rsrc[2] = -1;            // no range limit: callers keep every row readable
+    rsrc[3] = 0x00020000;    // raw buffer, 32-bit data format (gfx9 word 3)
+    voff = (uint32_t)(r * ld * 2 + kc * 16);
+    round_bytes = __builtin_amdgcn_readfirstlane((int32_t)(NW * RPI * ld * 2));
+  }
+  // round j (j < BR * CH / (64 NW)) of k-step kt into the tile at dst
+  __device__ __forceinline__ void load_round(int kt, int j, v4u* dst, int w) const {
+    const uint32_t lds = __builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) v4u*)(dst + (j * NW + w) * 64));
+    const int32_t soff = __builtin_amdgcn_readfirstlane(kt * (BK * 2) + j * round_bytes);
+    asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+                 :
+                 : "v"(voff), "s"(rsrc), "s"(soff), "{m0}"(lds)
+                 : "memory");
   }
   // issue the k-step kt of a BR-row tile (NW waves, BR * CH / (64 NW) rounds)
   template <int BR>
   __device__ __forceinline__ void load(int kt, v4u* dst, int w) const {
     static_assert(BR * CH % (64 * NW) == 0, "tile rows must fill whole rounds");
-    const char* q = p + (int64_t)kt * (BK * 2);
 #pragma unroll
-    for (int j = 0; j < BR * CH / (64 * NW); ++j) lds_dma16(q + j * round_step, dst + (j * NW + w) * 64);
-  }
-  // round j only (j < BR * CH / (64 NW))
-  __device__ __forceinline__ void load_round(int kt, int j, v4u* dst, int w) const {
-    lds_dma16(p + (int64_t)kt * (BK * 2) + j * round_step, dst + (j * NW + w) * 64);
+    for (int j = 0; j < BR * CH / (64 * NW); ++j) load_round(kt, j, dst, w);
   }
 };
 typedef TileSrcT<kBK, 4> TileSrc;
