@@ -90,10 +90,41 @@ def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_chunk: int =
     return o
 
 
+def cached_attention(q: np.ndarray, k_prefix: np.ndarray, v_prefix: np.ndarray, k: np.ndarray, v: np.ndarray,
+                     q_chunk: int = 1024) -> np.ndarray:
+    """Attention of W new positions over a cache of P earlier ones.
+
+    q, k, v [W, ., d_h] belong to positions P..P+W-1; k_prefix, v_prefix
+    [P, H_kv, d_h] are the cached states of positions 0..P-1.  New position
+    P + j sees every cached position and the new positions P + j' with j' <= j.
+    """
+    W, H, dh = q.shape
+    P = k_prefix.shape[0]
+    Hkv = k.shape[1]
+    group = H // Hkv
+    scale = q.dtype.type(1.0 / np.sqrt(dh))
+    kk = np.concatenate([k_prefix, k], axis=0)
+    vv = np.concatenate([v_prefix, v], axis=0)
+    o = np.empty_like(q)
+    for hq in range(H):
+        hk = hq // group
+        for t0 in range(0, W, q_chunk):
+            t1 = min(W, t0 + q_chunk)
+            s = (q[t0:t1, hq, :] @ kk[:P + t1, hk, :].T) * scale      # [tq, P + t1]
+            mask = np.arange(P + t1)[None, :] > (P + np.arange(t0, t1))[:, None]
+            s = np.where(mask, -np.inf, s)
+            o[t0:t1, hq, :] = softmax(s, axis=-1) @ vv[:P + t1, hk, :]
+    return o
+
+
 def block(m: Model, l: int, h: np.ndarray, positions: np.ndarray,
-          v_hook: Optional[Callable[[np.ndarray], np.ndarray]] = None) -> np.ndarray:
+          v_hook: Optional[Callable[[np.ndarray], np.ndarray]] = None, kv_out: Optional[list] = None,
+          prefix_kv: Optional[tuple] = None) -> np.ndarray:
     """One decoder block.  ``v_hook`` (if given) replaces the layer's Value states
-    [T, H_kv, d_h] before attention; Q and K are untouched."""
+    [T, H_kv, d_h] before attention; Q and K are untouched.  ``kv_out`` (a list)
+    receives the block's rotated Keys and its Values.  ``prefix_kv`` = (K, V) of
+    cached earlier positions makes the rows of h new positions attending to that
+    cache as well (``cached_attention``); the hook does not touch the cache."""
     c = m.cfg
     H, Hkv, dh = c.n_heads, c.n_kv_heads, c.head_dim
     T = h.shape[0]
@@ -106,7 +137,13 @@ def block(m: Model, l: int, h: np.ndarray, positions: np.ndarray,
     k = rope(k, positions, c.rope_theta)
     if v_hook is not None:
         v = v_hook(v)
-    o = causal_attention(q, k, v).reshape(T, H * dh)
+    if kv_out is not None:
+        kv_out.append((k, v))
+    if prefix_kv is None:
+        o = causal_attention(q, k, v)
+    else:
+        o = cached_attention(q, prefix_kv[0], prefix_kv[1], k, v)
+    o = o.reshape(T, H * dh)
     h = h + o @ m.w_o[l].T
     x = rmsnorm(h, m.mlp_norm[l], c.rms_eps)
     gu = x @ m.w_gate_up[l].T
@@ -128,21 +165,24 @@ def logits(m: Model, xf: np.ndarray) -> np.ndarray:
 
 class CleanState:
     """What ReferencePredict leaves behind: h_l (input of block l) for every l, and
-    the final normalised hidden state of the clean pass."""
+    the final normalised hidden state of the clean pass; with ``keep_kv`` also the
+    KV cache, (rotated K, V) of every block."""
 
-    def __init__(self, hs: List[np.ndarray], xfinal: np.ndarray):
+    def __init__(self, hs: List[np.ndarray], xfinal: np.ndarray, kv: Optional[list] = None):
         self.hs = hs
         self.xfinal = xfinal
+        self.kv = kv
 
 
-def clean_pass(m: Model, tokens: np.ndarray) -> CleanState:
+def clean_pass(m: Model, tokens: np.ndarray, keep_kv: bool = False) -> CleanState:
     pos = np.arange(len(tokens))
     h = embed(m, tokens)
     hs = []
+    kv = [] if keep_kv else None
     for l in range(m.cfg.n_layers):
         hs.append(h)
-        h = block(m, l, h, pos)
-    return CleanState(hs, final_hidden(m, h))
+        h = block(m, l, h, pos, kv_out=kv)
+    return CleanState(hs, final_hidden(m, h), kv)
 
 
 def resume(m: Model, h_l: np.ndarray, l: int, v_hook) -> np.ndarray:

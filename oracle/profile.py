@@ -121,3 +121,78 @@ def sensitivity_profile(m: M.Model, token_seqs: Sequence[np.ndarray], layers: Se
                 d[a, n, j], _ = profile_layer(m, st, toks, seq_indices[n], l, p)
     s = d.sum(axis=1) / N
     return {"s": s, "d": d}
+
+
+# --------------------------------------------------------------------------- cached-window mode
+# The literal reading of Section 4.3: each example is a prefix [0, P) that builds
+# the KV cache and an evaluation window [P, T), P = window_start.  The reference
+# (ReferencePredict) evaluates the window against the intact cache.  Perturbing
+# layer l changes only the eligible prefix Values of layer l's cache (positions
+# [protect_head, P - protect_tail)); its Keys and the caches of all other layers
+# stay as they are, and no cached position is removed.  The window is evaluated
+# again against that cache: its rows resume from their input to block l (nothing
+# below l sees the change), attend at every block to the cached prefix plus the
+# window's own freshly computed states, and d_{i,l} is the mean KL over the window
+# (Eq. sample-response).  The same noise counter as the resumed mode keys epsilon.
+
+class WindowState:
+    """Prefix KV cache of every block, and the window's reference pass: the input
+    of every block for the window rows and their final normalised hidden state."""
+
+    def __init__(self, P: int, kv: list, hs: list, xfinal: np.ndarray):
+        self.P, self.kv, self.hs, self.xfinal = P, kv, hs, xfinal
+
+
+def window_clean_state(m: M.Model, tokens: np.ndarray, P: int) -> WindowState:
+    T = len(tokens)
+    if not (0 < P < T):
+        raise ValueError("window_start must split the sequence into a non-empty prefix and window")
+    prefix = M.clean_pass(m, tokens[:P], keep_kv=True)
+    pos = np.arange(P, T)
+    h = M.embed(m, tokens[P:])
+    hs = []
+    for l in range(m.cfg.n_layers):
+        hs.append(h)
+        h = M.block(m, l, h, pos, prefix_kv=prefix.kv[l])
+    return WindowState(P, prefix.kv, hs, M.final_hidden(m, h))
+
+
+def window_perturbed_final(m: M.Model, ws: WindowState, seq: int, layer: int, p: PerturbParams) -> np.ndarray:
+    """Final normalised hidden state of the window rows [P, T) with layer ``layer``'s
+    prefix Values perturbed in the cache."""
+    c = m.cfg
+    P = ws.P
+    T = P + ws.hs[0].shape[0]
+    pos = np.arange(P, T)
+    k_l, v_l = ws.kv[layer]
+    eps = value_noise(p.seed, seq, layer, c.n_kv_heads, np.arange(P), c.head_dim)
+    v_pert = perturb_values(v_l, p.alpha, eps, p.protect_head, P - p.protect_tail)
+    h = M.block(m, layer, ws.hs[layer], pos, prefix_kv=(k_l, v_pert))
+    for lp in range(layer + 1, c.n_layers):
+        h = M.block(m, lp, h, pos, prefix_kv=ws.kv[lp])
+    return M.final_hidden(m, h)
+
+
+def window_profile_layer(m: M.Model, ws: WindowState, seq: int, layer: int, p: PerturbParams):
+    """(d_{i,l}, KL_t for t in [P, T)) in the cached-window mode."""
+    xp = window_perturbed_final(m, ws, seq, layer, p)
+    kl = kl_per_position(m, ws.xfinal, xp)
+    return float(np.mean(kl)), kl
+
+
+def window_sensitivity_profile(m: M.Model, token_seqs: Sequence[np.ndarray], layers: Sequence[int],
+                               alphas: Sequence[float], p: PerturbParams,
+                               seq_indices: Optional[Sequence[int]] = None) -> Dict[str, np.ndarray]:
+    """s_l (Eq. layer-sensitivity) in the cached-window mode; the same shapes as
+    ``sensitivity_profile``.  Every sequence needs T_i > window_start."""
+    N, nA = len(token_seqs), len(layers)
+    if seq_indices is None:
+        seq_indices = list(range(N))
+    d = np.zeros((len(alphas), N, nA), dtype=np.float64)
+    for n, toks in enumerate(token_seqs):
+        ws = window_clean_state(m, toks, p.window_start)
+        for a, alpha in enumerate(alphas):
+            q = dataclasses.replace(p, alpha=float(alpha))
+            for j, l in enumerate(layers):
+                d[a, n, j] = window_profile_layer(m, ws, seq_indices[n], l, q)[0]
+    return {"s": d.sum(axis=1) / N, "d": d}
