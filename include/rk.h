@@ -71,6 +71,13 @@ typedef enum {
 #define RK_FLAG_UNFUSED_KL     0x2u  /* materialise fp32 logits and run the separate
                                         log-softmax + KL kernel instead of the fused
                                         LM-head + KL kernel                          */
+#define RK_FLAG_CACHED_WINDOW  0x4u  /* the literal reading of Section 4.3: each
+                                        sequence is a cached prefix [0, P) and an
+                                        evaluation window [P, T_i), P = window_start;
+                                        only layer l's cached prefix Values are
+                                        perturbed, every other cache stays frozen,
+                                        and only the window is recomputed (see
+                                        rk_window_reference).  bf16 models only.     */
 
 /* Most sequences one batch (one call's rows) may hold. */
 #define RK_MAX_BATCH_SEQS 64
@@ -121,7 +128,9 @@ typedef struct {
  * with protect_head <= u < T_i - protect_tail are perturbed (the paper excludes
  * positions the base compressor protects); the evaluation window is
  * W_i = [window_start, T_i).  seed keys the Philox4x32-10 noise; the same noise
- * serves every alpha.                                                          */
+ * serves every alpha.  With RK_FLAG_CACHED_WINDOW the perturbed positions are
+ * the cached prefix positions protect_head <= u < window_start - protect_tail
+ * and every sequence must be longer than window_start > 0.                    */
 typedef struct {
   uint64_t seed;
   int32_t window_start;
@@ -145,8 +154,16 @@ void rk_model_destroy(rk_model *m);
  * and the final normalised hidden state ([n_rows, d_model] in the model dtype).  */
 size_t rk_clean_state_size(const rk_model *m, int64_t n_rows);
 
+/* Bytes of the state of the cached-window mode for a batch of at most n_rows
+ * rows (rk_window_reference): the KV cache of every layer for the prefix rows
+ * ([L, prefix rows, 2 * n_kv_heads * head_dim] bf16, K then V), and for the
+ * window rows the fp32 input of every block, the final normalised hidden state
+ * and the clean log-sum-exp of the LM head.  0 for invalid arguments.          */
+size_t rk_window_state_size(const rk_model *m, int64_t n_rows);
+
 /* Flag of rk_workspace_size: the workspace also holds one clean state
- * (rk_sensitivity_profile keeps its clean state there).                        */
+ * (rk_sensitivity_profile keeps its clean state there; with
+ * RK_FLAG_CACHED_WINDOW also set, a cached-window state).                      */
 #define RK_WS_CLEAN_STATE 0x100u
 
 /* Workspace bytes for batches of at most max_rows rows, scoring at most
@@ -155,6 +172,8 @@ size_t rk_clean_state_size(const rk_model *m, int64_t n_rows);
  * and/or RK_FLAG_UNFUSED_KL (room for materialised fp32 logits; implied for
  * RK_F32 models).  Returns 0 for invalid arguments.                            */
 size_t rk_workspace_size(const rk_model *m, int64_t max_rows, int32_t max_group, uint32_t flags);
+/* (flags may also hold RK_FLAG_CACHED_WINDOW: room for one layer's perturbed
+ * prefix Values, and, with RK_WS_CLEAN_STATE, a cached-window state.)          */
 
 /* ---------------------------------------------------------------- profiling */
 
@@ -162,6 +181,16 @@ size_t rk_workspace_size(const rk_model *m, int64_t max_rows, int32_t max_group,
  * per-layer inputs h_l and the final normalised hidden state in clean_state.    */
 rk_status rk_reference_forward(const rk_model *m, const rk_batch *batch, void *clean_state,
                                size_t clean_bytes, void *workspace, size_t ws_bytes, void *stream);
+
+/* ReferencePredict of the cached-window mode (Section 4.3) for one batch: the
+ * prefix [0, window_start) of every sequence runs through all layers once and
+ * leaves its KV cache; the window [window_start, T_i) is then evaluated against
+ * the intact cache (its block inputs, final hidden state and log-sum-exp are
+ * kept).  Every sequence must be longer than window_start > 0; bf16 models only.
+ * state: at least rk_window_state_size(m, rows) bytes; workspace: at least
+ * rk_workspace_size(m, rows, 1, RK_FLAG_CACHED_WINDOW).                        */
+rk_status rk_window_reference(const rk_model *m, const rk_batch *batch, int32_t window_start, void *state,
+                              size_t state_bytes, void *workspace, size_t ws_bytes, void *stream);
 
 /* PerturbedPredict + WindowKL (Algorithm 1; Eqs. value-perturbation and
  * sample-response) for one batch, one layer and one alpha, resumed from a clean
@@ -172,7 +201,11 @@ rk_status rk_reference_forward(const rk_model *m, const rk_batch *batch, void *c
  *               (selects the unfused LM-head path; for verification).
  * workspace must be at least rk_workspace_size(m, rows, 1, f) with f =
  * RK_FLAG_UNFUSED_KL when logits_out is given, the flag is set or the model is
- * fp32, else 0.                                                                 */
+ * fp32, else 0 (plus RK_FLAG_CACHED_WINDOW in that mode).
+ * With RK_FLAG_CACHED_WINDOW in p->flags, clean_state is a state from
+ * rk_window_reference with the same window_start, and kl_pos / logits_out hold
+ * the window rows only (sum_i (T_i - window_start) rows, sequence by sequence);
+ * RK_FLAG_FULL_RECOMPUTE is not available in that mode.                         */
 rk_status rk_profile_layer(const rk_model *m, const rk_batch *batch, int32_t layer, float alpha,
                            const rk_perturb_params *p, const void *clean_state, size_t clean_bytes,
                            float *d_out, float *kl_pos, float *logits_out,
@@ -188,8 +221,9 @@ rk_status rk_profile_layer(const rk_model *m, const rk_batch *batch, int32_t lay
  *   finite and >= 0.  s_out: DEVICE fp32 [n_alpha, n_A].  d_out: DEVICE fp32
  *   [n_alpha, N, n_A] or NULL.  One clean pass per batch serves every alpha.
  * max_group: passes scored per LM-head launch (1..16).
+ * With RK_FLAG_CACHED_WINDOW the profile is that of the cached-window mode.
  * workspace must be at least rk_workspace_size(m, max_rows, max_group,
- * RK_WS_CLEAN_STATE | (p->flags & RK_FLAG_UNFUSED_KL)).                         */
+ * RK_WS_CLEAN_STATE | (p->flags & (RK_FLAG_UNFUSED_KL | RK_FLAG_CACHED_WINDOW))). */
 rk_status rk_sensitivity_profile(const rk_model *m, const rk_batch *calib, const int32_t *layers,
                                  int32_t n_A, const float *alphas, int32_t n_alpha,
                                  const rk_perturb_params *p, int64_t max_rows, int32_t max_group,

@@ -26,7 +26,7 @@ from typing import Optional, Sequence
 import numpy as np
 
 __all__ = ["RKError", "load", "Model", "Batch", "layer_budgets", "timing_begin", "timing_end", "LIB_PATH", "RK_FLAG_FULL_RECOMPUTE",
-           "RK_FLAG_UNFUSED_KL", "RK_WS_CLEAN_STATE", "RK_MAX_BATCH_SEQS", "RK_MAX_GROUP"]
+           "RK_FLAG_UNFUSED_KL", "RK_FLAG_CACHED_WINDOW", "RK_WS_CLEAN_STATE", "RK_MAX_BATCH_SEQS", "RK_MAX_GROUP"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librk.so")
 
@@ -35,6 +35,7 @@ RK_F32, RK_BF16 = 0, 1
 RK_ROUND_LARGEST_REMAINDER, RK_ROUND_NEAREST_EVEN = 0, 1
 RK_FLAG_FULL_RECOMPUTE = 0x1
 RK_FLAG_UNFUSED_KL = 0x2
+RK_FLAG_CACHED_WINDOW = 0x4
 RK_WS_CLEAN_STATE = 0x100
 RK_MAX_BATCH_SEQS = 64
 RK_MAX_GROUP = 16
@@ -93,6 +94,8 @@ def load() -> ctypes.CDLL:
         "rk_model_create": (st, [ctypes.POINTER(_Config), ctypes.POINTER(_Weights), ctypes.POINTER(vp)]),
         "rk_model_destroy": (None, [vp]),
         "rk_clean_state_size": (sz, [vp, i64]),
+        "rk_window_state_size": (sz, [vp, i64]),
+        "rk_window_reference": (st, [vp, ctypes.POINTER(_Batch), i32, vp, sz, vp, sz, vp]),
         "rk_workspace_size": (sz, [vp, i64, i32, u32]),
         "rk_reference_forward": (st, [vp, ctypes.POINTER(_Batch), vp, sz, vp, sz, vp]),
         "rk_profile_layer": (st, [vp, ctypes.POINTER(_Batch), i32, f32, ctypes.POINTER(_Params), vp, sz, vp, vp, vp,
@@ -200,11 +203,19 @@ class Model:
     def workspace_size(self, max_rows: int, max_group: int = 1, flags: int = 0) -> int:
         return int(load().rk_workspace_size(self._h, int(max_rows), int(max_group), int(flags)))
 
+    def window_state_size(self, rows: int) -> int:
+        return int(load().rk_window_state_size(self._h, int(rows)))
+
     # -- entry points
     def reference_forward(self, batch: Batch, clean_state, workspace, stream=None):
         _check(load().rk_reference_forward(self._h, ctypes.byref(batch._c), _ptr(clean_state),
                                            clean_state.numel() * clean_state.element_size(), _ptr(workspace),
                                            workspace.numel() * workspace.element_size(), _stream(stream)))
+
+    def window_reference(self, batch: Batch, window_start: int, state, workspace, stream=None):
+        _check(load().rk_window_reference(self._h, ctypes.byref(batch._c), int(window_start), _ptr(state),
+                                          state.numel() * state.element_size(), _ptr(workspace),
+                                          workspace.numel() * workspace.element_size(), _stream(stream)))
 
     def profile_layer(self, batch: Batch, layer: int, alpha: float, clean_state, d_out, workspace, kl_pos=None,
                       logits_out=None, seed: int = 2, window_start: int = 0, protect_head: int = 0,

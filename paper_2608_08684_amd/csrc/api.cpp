@@ -73,8 +73,30 @@ static CleanPlan clean_plan(const rk_model* m, int64_t R) {
   return p;
 }
 
+// State of the cached-window mode, sized for a batch of R rows (prefix plus
+// window rows <= R): the prefix KV cache of every layer (K then V columns), and
+// for the window rows the input of every block, the final hidden state and the
+// clean log-sum-exp.
+struct WinPlan {
+  size_t kv, h, xf, lse, total;
+};
+
+static int64_t kv_cols(const rk_model* m) { return 2 * (int64_t)m->cfg.n_kv_heads * m->cfg.head_dim; }
+
+static WinPlan win_plan(const rk_model* m, int64_t R) {
+  const int64_t d = m->cfg.d_model, L = m->cfg.n_layers;
+  WinPlan p;
+  size_t o = 0;
+  p.kv = o;  o += align256((size_t)L * R * kv_cols(m) * act_bytes(m));
+  p.h = o;   o += align256((size_t)L * R * d * 4);
+  p.xf = o;  o += align256((size_t)pad_rows(R) * d * act_bytes(m));
+  p.lse = o; o += align256((size_t)R * 4);
+  p.total = o;
+  return p;
+}
+
 struct WsPlan {
-  size_t h, x, qkv, att, ff, xp, part, logits_c, logits_p, kl, rope, rope_pos, dbatch, sacc, clean, total;
+  size_t h, x, qkv, att, ff, xp, part, logits_c, logits_p, kl, rope, rope_pos, dbatch, sacc, vpert, clean, total;
   bool unfused;
 };
 
@@ -109,8 +131,11 @@ static WsPlan ws_plan(const rk_model* m, int64_t R, int G, uint32_t flags) {
   p.rope_pos = o; o += align256((size_t)R * 4);
   p.dbatch = o;   o += align256((size_t)G * RK_MAX_BATCH_SEQS * 4);
   p.sacc = o;     o += align256((size_t)kMaxSAcc * 8);
+  p.vpert = o;
+  if (flags & RK_FLAG_CACHED_WINDOW) o += align256((size_t)R * (kv_cols(m) / 2) * a);
   p.clean = o;
-  if (flags & RK_WS_CLEAN_STATE) o += clean_plan(m, R).total;
+  if (flags & RK_WS_CLEAN_STATE)
+    o += (flags & RK_FLAG_CACHED_WINDOW) ? win_plan(m, R).total : clean_plan(m, R).total;
   p.total = o;
   return p;
 }
@@ -120,6 +145,7 @@ struct Bufs {
   float* h; void* x; void* qkv; void* att; void* ff; void* xp;
   float2* part; float* logits_c; float* logits_p; float* kl; float2* rope; int32_t* rope_pos; float* dbatch;
   double* sacc;
+  void* vpert;
   char* clean;
 };
 
@@ -130,7 +156,7 @@ static Bufs carve(const WsPlan& p, void* ws) {
   u.xp = b + p.xp; u.part = (float2*)(b + p.part); u.logits_c = (float*)(b + p.logits_c);
   u.logits_p = (float*)(b + p.logits_p); u.kl = (float*)(b + p.kl); u.rope = (float2*)(b + p.rope);
   u.rope_pos = (int32_t*)(b + p.rope_pos);
-  u.dbatch = (float*)(b + p.dbatch); u.sacc = (double*)(b + p.sacc); u.clean = b + p.clean;
+  u.dbatch = (float*)(b + p.dbatch); u.sacc = (double*)(b + p.sacc); u.vpert = b + p.vpert; u.clean = b + p.clean;
   return u;
 }
 
@@ -142,6 +168,19 @@ static Clean clean_view(const rk_model* m, int64_t R, const void* base) {
   const CleanPlan p = clean_plan(m, R);
   char* b = (char*)base;
   return Clean{(float*)(b + p.h), b + p.xf, (float*)(b + p.lse)};
+}
+
+// Cached-window state: the window rows' part has the shape of a clean state
+// (inputs h_l [L][Rw][d], final hidden, lse) plus the prefix KV cache.
+struct Win {
+  void* kv;   // [L][Rp][kv_cols], K columns then V columns
+  Clean w;    // window rows
+};
+
+static Win win_view(const rk_model* m, int64_t R, const void* base) {
+  const WinPlan p = win_plan(m, R);
+  char* b = (char*)base;
+  return Win{b + p.kv, Clean{(float*)(b + p.h), b + p.xf, (float*)(b + p.lse)}};
 }
 
 // ----------------------------------------------------------------------------- timing
@@ -194,8 +233,12 @@ struct Noise {
 
 // One decoder block from h_in to h_out (h_out may equal h_in); `noise` perturbs
 // the block's Values between the q|k|v projection and attention.
+// With `pre`, the block's rows are the window rows of a cached-window batch and
+// attention also reads the cached prefix; `kv_out` (if given) receives the
+// block's K and V columns, row by row.
 static rk_status run_block(const rk_model* m, int l, const float* h_in, float* h_out, const Bufs& b,
-                           const SeqTable& st, const Noise* noise, hipStream_t s) {
+                           const SeqTable& st, const Noise* noise, hipStream_t s, const KvPrefix* pre = nullptr,
+                           void* kv_out = nullptr) {
   const rk_model_config& c = m->cfg;
   const int R = st.rows, d = c.d_model;
   { Timed t("rmsnorm", s); RK_TRY(launch_rmsnorm(h_in, m->attn_norm[l], b.x, m->bf16, R, d, c.rms_eps, s)); }
@@ -209,6 +252,11 @@ static rk_status run_block(const rk_model* m, int l, const float* h_in, float* h
     g.q_scale = (float)(1.4426950408889634 / sqrt((double)c.head_dim));
   }
   { Timed t("gemm_qkv", s); RK_TRY(launch_gemm(g, m->bf16, s)); }
+  if (kv_out) {
+    const int64_t a = act_bytes(m);
+    RK_TRY(launch_copy_cols(b.qkv, m->qkv_cols * a, (int64_t)c.n_heads * c.head_dim * a, kv_out, kv_cols(m) * a,
+                            kv_cols(m) * a, R, s));
+  }
   if (noise) {
     char* v = (char*)b.qkv + (size_t)(c.n_heads + c.n_kv_heads) * c.head_dim * act_bytes(m);
     Timed t("noise", s);
@@ -218,7 +266,7 @@ static rk_status run_block(const rk_model* m, int l, const float* h_in, float* h
   {
     Timed t("attention", s);
     RK_TRY(launch_attention(b.qkv, m->qkv_cols, b.att, m->attn_cols, st, c.n_heads, c.n_kv_heads, c.head_dim,
-                            m->bf16, s));
+                            m->bf16, s, pre));
   }
   g = GemmArgs{};
   g.A = b.att; g.lda = m->attn_cols; g.B = m->w_o[l]; g.ldb = m->attn_cols; g.M = R; g.N = d; g.K = m->attn_cols;
@@ -315,6 +363,106 @@ static rk_status clean_logits(const rk_model* m, const SeqTable& st, const Clean
   return RK_OK;
 }
 
+// ----------------------------------------------------------------------------- cached-window mode
+// Row tables of a cached-window batch: the prefix rows (P per sequence, in
+// sequence order) and the window rows (T_k - P per sequence).
+static rk_status window_tables(const SeqTable& st, int P, SeqTable* pst, SeqTable* wst) {
+  if (P < 1) { set_error("the cached-window mode needs window_start >= 1"); return RK_ERR_ARG; }
+  *pst = st;
+  *wst = st;
+  pst->max_len = P;
+  wst->max_len = 0;
+  for (int k = 0; k <= st.n; ++k) {
+    pst->off[k] = k * P;
+    wst->off[k] = st.off[k] - k * P;
+    if (k > 0) {
+      const int len = st.off[k] - st.off[k - 1];
+      if (len <= P) {
+        set_error("sequence %d (%d tokens) is not longer than window_start %d", k, len, P);
+        return RK_ERR_SHAPE;
+      }
+      wst->max_len = std::max(wst->max_len, len - P);
+    }
+  }
+  pst->rows = st.n * P;
+  wst->rows = st.off[st.n] - st.n * P;
+  return RK_OK;
+}
+
+// The cached prefix of layer l: K from the cache, V from the cache or from vpert.
+static KvPrefix cache_prefix(const rk_model* m, const Win& wn, const SeqTable& pst, int l, const void* vpert) {
+  const int64_t kc = kv_cols(m);
+  const bf16_t* kv = (const bf16_t*)wn.kv + (size_t)l * pst.rows * kc;
+  KvPrefix pk;
+  pk.k = kv;
+  pk.ldk = kc;
+  pk.P = pst.max_len;
+  if (vpert) {
+    pk.v = (const bf16_t*)vpert;
+    pk.ldv = kc / 2;
+  } else {
+    pk.v = kv + kc / 2;
+    pk.ldv = kc;
+  }
+  return pk;
+}
+
+// ReferencePredict of the cached-window mode: the prefixes run through every
+// layer once and leave their K and V; the windows are then evaluated against the
+// intact cache, keeping each block's input, the final hidden state and A_t.
+static rk_status window_reference(const rk_model* m, const int32_t* tokens, const SeqTable& st, const SeqTable& pst,
+                                  const SeqTable& wst, const Win& wn, const Bufs& b, hipStream_t s) {
+  const rk_model_config& c = m->cfg;
+  const int64_t d = c.d_model, Rp = pst.rows, Rw = wst.rows, kvb = kv_cols(m) * act_bytes(m);
+  const int P = pst.max_len;
+  RK_TRY(launch_rope_table(b.rope, b.rope_pos, pst, c.head_dim, c.rope_theta, s, 0));
+  RK_TRY(launch_embed_gather(m->tok_emb, m->bf16, tokens, st, pst, 0, b.h, (int)d, s));
+  for (int l = 0; l < c.n_layers; ++l) {
+    rk_status e = run_block(m, l, b.h, b.h, b, pst, nullptr, s, nullptr, (char*)wn.kv + (size_t)l * Rp * kvb);
+    if (e != RK_OK) return e;
+  }
+  RK_TRY(launch_rope_table(b.rope, b.rope_pos, wst, c.head_dim, c.rope_theta, s, P));
+  RK_TRY(launch_embed_gather(m->tok_emb, m->bf16, tokens, st, wst, P, wn.w.h, (int)d, s));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const KvPrefix pk = cache_prefix(m, wn, pst, l, nullptr);
+    float* out = (l + 1 < c.n_layers) ? wn.w.h + (size_t)(l + 1) * Rw * d : b.h;
+    rk_status e = run_block(m, l, wn.w.h + (size_t)l * Rw * d, out, b, wst, nullptr, s, &pk);
+    if (e != RK_OK) return e;
+  }
+  RK_TRY(launch_rmsnorm(b.h, m->final_norm, wn.w.xf, m->bf16, (int)Rw, (int)d, c.rms_eps, s));
+  Timed t("lm_lse", s);
+  RK_TRY(launch_lm_lse((const bf16_t*)wn.w.xf, (const bf16_t*)m->lm_head, (int)Rw, (int)d, c.vocab, b.part,
+                       wn.w.lse, s));
+  return RK_OK;
+}
+
+// PerturbedPredict of the cached-window mode: layer `layer`'s cached prefix
+// Values get the noise (a copy: the cache itself stays clean), the window rows
+// resume from their input to that block and read the frozen caches above it.
+// The rotary table must hold the window positions.
+static rk_status window_perturbed_final(const rk_model* m, const SeqTable& pst, const SeqTable& wst, const Win& wn,
+                                        int layer, float alpha, const rk_perturb_params* p, void* xf_out,
+                                        const Bufs& b, hipStream_t s) {
+  const rk_model_config& c = m->cfg;
+  const int64_t d = c.d_model, Rp = pst.rows, Rw = wst.rows, a = act_bytes(m), kc = kv_cols(m);
+  const char* kv_l = (const char*)wn.kv + (size_t)layer * Rp * kc * a;
+  RK_TRY(launch_copy_cols(kv_l, kc * a, (kc / 2) * a, b.vpert, (kc / 2) * a, (kc / 2) * a, (int)Rp, s));
+  {
+    Timed t("noise", s);
+    RK_TRY(launch_value_noise(b.vpert, m->bf16, kc / 2, pst, c.n_kv_heads, c.head_dim, layer, alpha, p->seed,
+                              p->protect_head, p->protect_tail, s));
+  }
+  KvPrefix pk = cache_prefix(m, wn, pst, layer, b.vpert);
+  rk_status e = run_block(m, layer, wn.w.h + (size_t)layer * Rw * d, b.h, b, wst, nullptr, s, &pk);
+  if (e != RK_OK) return e;
+  for (int l = layer + 1; l < c.n_layers; ++l) {
+    pk = cache_prefix(m, wn, pst, l, nullptr);
+    if ((e = run_block(m, l, b.h, b.h, b, wst, nullptr, s, &pk)) != RK_OK) return e;
+  }
+  RK_TRY(launch_rmsnorm(b.h, m->final_norm, xf_out, m->bf16, (int)Rw, (int)d, c.rms_eps, s));
+  return RK_OK;
+}
+
 // ----------------------------------------------------------------------------- validation
 static rk_status make_table(const rk_batch* bt, int first, int count, SeqTable* st) {
   if (count < 1 || count > RK_MAX_BATCH_SEQS) {
@@ -354,7 +502,19 @@ static rk_status check_params(const rk_perturb_params* p) {
     set_error("window_start / protect_head / protect_tail must be >= 0");
     return RK_ERR_ARG;
   }
-  if (p->flags & ~(RK_FLAG_FULL_RECOMPUTE | RK_FLAG_UNFUSED_KL)) { set_error("unknown flags"); return RK_ERR_ARG; }
+  if (p->flags & ~(RK_FLAG_FULL_RECOMPUTE | RK_FLAG_UNFUSED_KL | RK_FLAG_CACHED_WINDOW)) {
+    set_error("unknown flags");
+    return RK_ERR_ARG;
+  }
+  if ((p->flags & RK_FLAG_CACHED_WINDOW) && (p->flags & RK_FLAG_FULL_RECOMPUTE)) {
+    set_error("RK_FLAG_FULL_RECOMPUTE is not available in the cached-window mode");
+    return RK_ERR_ARG;
+  }
+  return RK_OK;
+}
+
+static rk_status check_window_model(const rk_model* m) {
+  if (!m->bf16) { set_error("the cached-window mode needs a bf16 model"); return RK_ERR_UNSUPPORTED; }
   return RK_OK;
 }
 
@@ -451,6 +611,27 @@ size_t rk_clean_state_size(const rk_model* m, int64_t n_rows) {
   return clean_plan(m, n_rows).total;
 }
 
+size_t rk_window_state_size(const rk_model* m, int64_t n_rows) {
+  if (!m || n_rows < 1 || !m->bf16) return 0;
+  return win_plan(m, n_rows).total;
+}
+
+rk_status rk_window_reference(const rk_model* m, const rk_batch* batch, int32_t window_start, void* state,
+                              size_t state_bytes, void* workspace, size_t ws_bytes, void* stream) {
+  rk_status e = check_batch(m, batch);
+  if (e != RK_OK) return e;
+  if ((e = check_window_model(m)) != RK_OK) return e;
+  if (!state || !workspace) { set_error("null state or workspace"); return RK_ERR_ARG; }
+  SeqTable st, pst, wst;
+  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  if ((e = window_tables(st, window_start, &pst, &wst)) != RK_OK) return e;
+  if (state_bytes < win_plan(m, st.rows).total) { set_error("window state too small"); return RK_ERR_WORKSPACE; }
+  const WsPlan wp = ws_plan(m, st.rows, 1, RK_FLAG_CACHED_WINDOW);
+  if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
+  const Bufs b = carve(wp, workspace);
+  return window_reference(m, batch->tokens, st, pst, wst, win_view(m, st.rows, state), b, (hipStream_t)stream);
+}
+
 size_t rk_workspace_size(const rk_model* m, int64_t max_rows, int32_t max_group, uint32_t flags) {
   if (!m || max_rows < 1 || max_group < 1 || max_group > RK_MAX_GROUP) return 0;
   return ws_plan(m, max_rows, max_group, flags).total;
@@ -481,8 +662,27 @@ rk_status rk_profile_layer(const rk_model* m, const rk_batch* batch, int32_t lay
   if (!(alpha >= 0.0f) || !isfinite(alpha)) { set_error("alpha must be finite and >= 0"); return RK_ERR_ARG; }
   SeqTable st;
   if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
-  if (clean_bytes < clean_plan(m, st.rows).total) { set_error("clean state too small"); return RK_ERR_WORKSPACE; }
   const bool unfused = !m->bf16 || logits_out || (p->flags & RK_FLAG_UNFUSED_KL);
+  if (p->flags & RK_FLAG_CACHED_WINDOW) {
+    if ((e = check_window_model(m)) != RK_OK) return e;
+    SeqTable pst, wst;
+    if ((e = window_tables(st, p->window_start, &pst, &wst)) != RK_OK) return e;
+    if (clean_bytes < win_plan(m, st.rows).total) { set_error("window state too small"); return RK_ERR_WORKSPACE; }
+    const WsPlan wp = ws_plan(m, st.rows, 1, (unfused ? RK_FLAG_UNFUSED_KL : 0) | RK_FLAG_CACHED_WINDOW);
+    if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
+    const Bufs b = carve(wp, workspace);
+    const Win wn = win_view(m, st.rows, clean_state);
+    hipStream_t s = (hipStream_t)stream;
+    RK_TRY(launch_rope_table(b.rope, b.rope_pos, wst, m->cfg.head_dim, m->cfg.rope_theta, s, p->window_start));
+    if ((e = window_perturbed_final(m, pst, wst, wn, layer, alpha, p, b.xp, b, s)) != RK_OK) return e;
+    float* kl = kl_pos ? kl_pos : b.kl;
+    if (unfused && (e = clean_logits(m, wst, wn.w, b.logits_c, s)) != RK_OK) return e;
+    if ((e = score_group(m, wst, wn.w, b.xp, 1, unfused, logits_out ? logits_out : b.logits_p, kl, b, s)) != RK_OK)
+      return e;
+    RK_TRY(launch_window_mean(kl, wst.rows, 1, wst, 0, d_out, s));
+    return RK_OK;
+  }
+  if (clean_bytes < clean_plan(m, st.rows).total) { set_error("clean state too small"); return RK_ERR_WORKSPACE; }
   const WsPlan wp = ws_plan(m, st.rows, 1, unfused ? RK_FLAG_UNFUSED_KL : 0);
   if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
   const Bufs b = carve(wp, workspace);
@@ -524,9 +724,16 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
     if (len < 0) { set_error("offsets must be non-decreasing"); return RK_ERR_SHAPE; }
     if (len > max_rows) { set_error("sequence %d (%lld tokens) exceeds max_rows", i, (long long)len); return RK_ERR_SHAPE; }
     if (len == 0) { set_error("sequence %d is empty", i); return RK_ERR_SHAPE; }
+    if ((p->flags & RK_FLAG_CACHED_WINDOW) && (p->window_start < 1 || len <= p->window_start)) {
+      set_error("sequence %d (%lld tokens) needs a non-empty prefix and window around window_start %d", i,
+                (long long)len, p->window_start);
+      return RK_ERR_SHAPE;
+    }
   }
   const bool unfused = !m->bf16 || (p->flags & RK_FLAG_UNFUSED_KL);
-  const uint32_t wflags = RK_WS_CLEAN_STATE | (unfused ? RK_FLAG_UNFUSED_KL : 0);
+  const bool cw = (p->flags & RK_FLAG_CACHED_WINDOW) != 0;
+  if (cw && (e = check_window_model(m)) != RK_OK) return e;
+  const uint32_t wflags = RK_WS_CLEAN_STATE | (unfused ? RK_FLAG_UNFUSED_KL : 0) | (cw ? RK_FLAG_CACHED_WINDOW : 0);
   const WsPlan wp = ws_plan(m, max_rows, max_group, wflags);
   if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
 
@@ -549,6 +756,34 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
     if ((e = make_table(calib, first, count, &st)) != RK_OK) return e;
     const int32_t* tokens = calib->tokens + calib->offsets[first];
     const int64_t R = st.rows;
+    if (cw) {
+      // cached-window mode: the same grouping over the window rows of the batch
+      SeqTable pst, wst;
+      if ((e = window_tables(st, p->window_start, &pst, &wst)) != RK_OK) return e;
+      const Win wn = win_view(m, R, b.clean);
+      if ((e = window_reference(m, tokens, st, pst, wst, wn, b, s)) != RK_OK) return e;
+      if (unfused && (e = clean_logits(m, wst, wn.w, b.logits_c, s)) != RK_OK) return e;
+      const int64_t Rw = wst.rows;
+      for (int g0 = 0; g0 < n_pass; g0 += max_group) {
+        const int G = (n_pass - g0 < max_group) ? n_pass - g0 : max_group;
+        PassMap pm{};
+        pm.G = G;
+        pm.seq_index0 = first;
+        pm.d_seq_stride = n_A;
+        for (int k = 0; k < G; ++k) {
+          const int idx = g0 + k, a = idx / n_A, j = idx % n_A;
+          void* xf = (char*)b.xp + (size_t)k * pad_rows(Rw) * m->cfg.d_model * act_bytes(m);
+          if ((e = window_perturbed_final(m, pst, wst, wn, layers[j], alphas[a], p, xf, b, s)) != RK_OK) return e;
+          pm.d_base[k] = (int64_t)a * N * n_A + j;
+          pm.s_index[k] = a * n_A + j;
+        }
+        if ((e = score_group(m, wst, wn.w, b.xp, G, unfused, b.logits_p, b.kl, b, s)) != RK_OK) return e;
+        RK_TRY(launch_window_mean(b.kl, Rw, G, wst, 0, b.dbatch, s));
+        RK_TRY(launch_accumulate(b.dbatch, st.n, pm, d_out, b.sacc, s));
+      }
+      first += count;
+      continue;
+    }
     const Clean cl = clean_view(m, R, b.clean);
     if ((e = reference_forward(m, tokens, st, cl, b, s)) != RK_OK) return e;
     if (unfused && (e = clean_logits(m, st, cl, b.logits_c, s)) != RK_OK) return e;

@@ -28,6 +28,8 @@
 // model only.
 #include <math.h>
 
+#include <algorithm>
+
 #include "rk_internal.h"
 
 namespace rk {
@@ -83,10 +85,10 @@ struct AttnTraits {
   static constexpr int kMinBlocks = DH == 64 ? 3 : 2;
 };
 
-template <int DH>
+template <int DH, bool PREFIX>
 __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_kernel(const bf16_t* __restrict__ qkv, int64_t ldq,
                                                         bf16_t* __restrict__ out, int64_t ldo, SeqTable st,
-                                                        AttnWork wk, int H, int Hkv, int n_items) {
+                                                        AttnWork wk, int H, int Hkv, int n_items, KvPrefix pk) {
   constexpr int BQ = 128, BKV = 64;
   constexpr int CH = DH / 8;                // 16-byte chunks per row
   constexpr int NKS = DH / 16;              // k-steps of S^T
@@ -124,14 +126,16 @@ __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_ker
   const int nqb = (T + BQ - 1) / BQ;
 
   // buffer descriptor over this sequence's rows (raw, stride 0): reads past row T - 1 return zero
-  i32x4_t rsrc;
-  {
-    const uint64_t base = (uint64_t)(qkv + (int64_t)row0 * ldq);
-    rsrc[0] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)base);
-    rsrc[1] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)(base >> 32));
-    rsrc[2] = __builtin_amdgcn_readfirstlane((int32_t)((int64_t)T * ldq * 2));
-    rsrc[3] = 0x00020000;
-  }
+  auto make_rsrc = [](const bf16_t* base_ptr, int64_t bytes) {
+    i32x4_t r;
+    const uint64_t base = (uint64_t)base_ptr;
+    r[0] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)base);
+    r[1] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)(base >> 32));
+    r[2] = __builtin_amdgcn_readfirstlane((int32_t)bytes);
+    r[3] = 0x00020000;
+    return r;
+  };
+  const i32x4_t rsrc = make_rsrc(qkv + (int64_t)row0 * ldq, (int64_t)T * ldq * 2);
   const int kcol = (H + hk) * DH, vcol = (H + Hkv + hk) * DH;
   uint32_t koff[NLD], voff[NLD];
 #pragma unroll
@@ -140,15 +144,42 @@ __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_ker
     koff[i] = (uint32_t)(r * ldq * 2 + (kcol + (ph ^ k_swz<DH>(r)) * 8) * 2);
     voff[i] = (uint32_t)(r * ldq * 2 + (vcol + (ph ^ v_swz<DH>(r)) * 8) * 2);
   }
-  const uint32_t ks_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) v4u*)&Ks[0][0];
-  const uint32_t vs_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) v4u*)&Vs[0][0];
-  auto issue = [&](int k0, int b) {
-    const int so = __builtin_amdgcn_readfirstlane(k0 * (int)ldq * 2);
+  // cached prefix of this sequence (PREFIX): rows k * P .. k * P + P - 1 of the K and V caches
+  const int P = PREFIX ? pk.P : 0;
+  i32x4_t rk_p = rsrc, rv_p = rsrc;
+  uint32_t koff_p[PREFIX ? NLD : 1], voff_p[PREFIX ? NLD : 1];
+  if constexpr (PREFIX) {
+    rk_p = make_rsrc(pk.k + (int64_t)k * P * pk.ldk, (int64_t)P * pk.ldk * 2);
+    rv_p = make_rsrc(pk.v + (int64_t)k * P * pk.ldv, (int64_t)P * pk.ldv * 2);
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
-      const uint32_t o = (uint32_t)((b * SLOTS + (i * 4 + w) * 64) * 16);
-      dma16(rsrc, __builtin_amdgcn_readfirstlane(ks_lds + o), koff[i], so);
-      dma16(rsrc, __builtin_amdgcn_readfirstlane(vs_lds + o), voff[i], so);
+      const int slot = (i * 4 + w) * 64 + lane, r = slot / CH, ph = slot % CH;
+      koff_p[i] = (uint32_t)(r * pk.ldk * 2 + (hk * DH + (ph ^ k_swz<DH>(r)) * 8) * 2);
+      voff_p[i] = (uint32_t)(r * pk.ldv * 2 + (hk * DH + (ph ^ v_swz<DH>(r)) * 8) * 2);
+    }
+  }
+  const int n_pre = (P + BKV - 1) / BKV;   // prefix tiles, visited before the window's own
+  const uint32_t ks_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) v4u*)&Ks[0][0];
+  const uint32_t vs_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) v4u*)&Vs[0][0];
+  // tile t: prefix tile t (t < n_pre), else the sequence's own tile t - n_pre
+  auto issue = [&](int t, int b) {
+    if (PREFIX && t < n_pre) {
+      const int sk = __builtin_amdgcn_readfirstlane(t * BKV * (int)pk.ldk * 2);
+      const int sv = __builtin_amdgcn_readfirstlane(t * BKV * (int)pk.ldv * 2);
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
+        const uint32_t o = (uint32_t)((b * SLOTS + (i * 4 + w) * 64) * 16);
+        dma16(rk_p, __builtin_amdgcn_readfirstlane(ks_lds + o), koff_p[i], sk);
+        dma16(rv_p, __builtin_amdgcn_readfirstlane(vs_lds + o), voff_p[i], sv);
+      }
+    } else {
+      const int so = __builtin_amdgcn_readfirstlane((t - n_pre) * BKV * (int)ldq * 2);
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
+        const uint32_t o = (uint32_t)((b * SLOTS + (i * 4 + w) * 64) * 16);
+        dma16(rsrc, __builtin_amdgcn_readfirstlane(ks_lds + o), koff[i], so);
+        dma16(rsrc, __builtin_amdgcn_readfirstlane(vs_lds + o), voff[i], so);
+      }
     }
   };
 
@@ -182,7 +213,7 @@ __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_ker
         qf[ks] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const v4u*>(qp + ks * 16));
     }
     const int kv_end = min(T, q0 + BQ);
-    const int n_tiles = (kv_end + BKV - 1) / BKV;
+    const int n_tiles = n_pre + (kv_end + BKV - 1) / BKV;
     const int wave_qmin = q0 + w * 32, wave_qmax = wave_qmin + 31;
 
     f32x16_t o[NDB], negm;
@@ -197,15 +228,16 @@ __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_ker
     wait_vm0();   // the query fragments are in registers before the ring starts
 #pragma unroll
     for (int p = 0; p < S - 1; ++p)
-      if (p < n_tiles) issue(p * BKV, p);
+      if (p < n_tiles) issue(p, p);
     int buf = 0, nbuf = S - 1;   // ring slots of tile t and of tile t + S - 1
     for (int t = 0; t < n_tiles; ++t) {
-      const int k0 = t * BKV;
+      const bool pre = PREFIX && t < n_pre;
+      const int k0 = (pre ? t : t - n_pre) * BKV;   // first key of the tile within its segment
       // tile t has landed once at most the S - 2 later tiles are in flight
       if (t + S - 2 < n_tiles) wait_vm<(S - 2) * 2 * NLD>(); else wait_vm0();
       __syncthreads();   // ... for every wave; and tile t - 1's slot is free again
-      if (t + S - 1 < n_tiles) issue(k0 + (S - 1) * BKV, nbuf);
-      if (k0 <= wave_qmax) {
+      if (t + S - 1 < n_tiles) issue(t + S - 1, nbuf);
+      if (pre || k0 <= wave_qmax) {
         const char* kt = reinterpret_cast<const char*>(Ks[buf]);
         f32x16_t s[2];
 #pragma unroll
@@ -218,14 +250,16 @@ __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_ker
 #pragma unroll
           for (int ks = 1; ks < NKS; ++ks) s[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks], qf[ks], s[rb], 0, 0, 0);
         }
-        // masks only where a key can exceed the query or the sequence (wave-uniform test)
-        if (k0 + BKV - 1 > wave_qmin || k0 + BKV > T) {
+        // masks only where a key can exceed the query or the segment (wave-uniform test);
+        // every cached prefix key precedes every query of the sequence's own rows
+        if (pre ? (k0 + BKV > P) : (k0 + BKV - 1 > wave_qmin || k0 + BKV > T)) {
+          const int qlim = pre ? P - 1 : my_q, klim = pre ? P : T;
 #pragma unroll
           for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
               const int key = k0 + rb * 32 + (i >> 2) * 8 + hf * 4 + (i & 3);
-              if (key > my_q || key >= T) s[rb][i] = -INFINITY;
+              if (key > qlim || key >= klim) s[rb][i] = -INFINITY;
             }
         }
         float mx = fmaxf(s[0][0], s[0][1]);
@@ -334,7 +368,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 }
 
 hipError_t launch_attention(const void* qkv, int64_t ldq, void* out, int64_t ldo, const SeqTable& st, int n_heads,
-                            int n_kv_heads, int head_dim, bool bf16, hipStream_t s) {
+                            int n_kv_heads, int head_dim, bool bf16, hipStream_t s, const KvPrefix* prefix) {
   if (st.rows <= 0) return hipSuccess;
   if (bf16) {
     // sequences by decreasing length; items = pairs of q-blocks
@@ -361,15 +395,21 @@ hipError_t launch_attention(const void* qkv, int64_t ldq, void* out, int64_t ldo
     const int grp = n_heads / n_kv_heads;
     const int n_items = wk.total * n_heads;
     const int grid = (n_items + 8 * grp - 1) / (8 * grp) * (8 * grp);
-    if (head_dim == 128)
-      attn_bf16_kernel<128><<<grid, 256, 0, s>>>((const bf16_t*)qkv, ldq, (bf16_t*)out, ldo, st, wk, n_heads,
-                                                 n_kv_heads, n_items);
-    else if (head_dim == 64)
-      attn_bf16_kernel<64><<<grid, 256, 0, s>>>((const bf16_t*)qkv, ldq, (bf16_t*)out, ldo, st, wk, n_heads,
-                                                n_kv_heads, n_items);
-    else
-      return hipErrorInvalidValue;
+    KvPrefix pk{};
+    const bool pre = prefix && prefix->P > 0;
+    if (pre) {
+      pk = *prefix;
+      if ((int64_t)st.n * pk.P * std::max(pk.ldk, pk.ldv) * 2 >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+    }
+#define RK_ATTN(D, PRE)                                                                                      \
+  attn_bf16_kernel<D, PRE><<<grid, 256, 0, s>>>((const bf16_t*)qkv, ldq, (bf16_t*)out, ldo, st, wk, n_heads, \
+                                                n_kv_heads, n_items, pk)
+    if (head_dim == 128) { if (pre) RK_ATTN(128, true); else RK_ATTN(128, false); }
+    else if (head_dim == 64) { if (pre) RK_ATTN(64, true); else RK_ATTN(64, false); }
+    else return hipErrorInvalidValue;
+#undef RK_ATTN
   } else {
+    if (prefix && prefix->P > 0) return hipErrorInvalidValue;   // cached prefixes: bf16 path only
     const float scale = (float)(1.0 / sqrt((double)head_dim));
     dim3 grid((st.rows + 63) / 64, n_heads);
     if (head_dim == 32)

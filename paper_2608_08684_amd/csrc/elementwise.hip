@@ -31,6 +31,51 @@ hipError_t launch_embed(const void* emb, bool emb_bf16, const int32_t* tokens, f
   return hipGetLastError();
 }
 
+// Row r of table dst (sequence k, local index j) takes token src.off[k] + pos0 + j.
+template <typename E>
+__global__ void embed_gather_kernel(const E* __restrict__ emb, const int32_t* __restrict__ tok, SeqTable src,
+                                    SeqTable dst, int pos0, float* __restrict__ h, int d) {
+  for (int r = blockIdx.x; r < dst.rows; r += gridDim.x) {
+    const int k = seq_of_row(dst, r);
+    const int64_t t = tok[src.off[k] + pos0 + (r - dst.off[k])];
+    for (int c = threadIdx.x; c < d; c += blockDim.x) h[(int64_t)r * d + c] = Act<E>::load(emb + t * d + c);
+  }
+}
+
+hipError_t launch_embed_gather(const void* emb, bool emb_bf16, const int32_t* tokens, const SeqTable& src,
+                               const SeqTable& dst, int pos0, float* h, int d, hipStream_t s) {
+  if (dst.rows <= 0) return hipSuccess;
+  const int blocks = std::min(dst.rows, 65536);
+  if (emb_bf16)
+    embed_gather_kernel<bf16_t><<<blocks, 256, 0, s>>>((const bf16_t*)emb, tokens, src, dst, pos0, h, d);
+  else
+    embed_gather_kernel<float><<<blocks, 256, 0, s>>>((const float*)emb, tokens, src, dst, pos0, h, d);
+  return hipGetLastError();
+}
+
+// dst[r][0 .. nbytes) = src[r][off .. off + nbytes), rows of ld_src / ld_dst bytes;
+// all byte counts multiples of 16.
+__global__ void copy_cols_kernel(const char* __restrict__ src, int64_t ld_src, int64_t off, char* __restrict__ dst,
+                                 int64_t ld_dst, int nvec, int rows) {
+  const int64_t total = (int64_t)rows * nvec;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / nvec, c = i - r * nvec;
+    reinterpret_cast<v4u*>(dst + r * ld_dst)[c] = reinterpret_cast<const v4u*>(src + r * ld_src + off)[c];
+  }
+}
+
+hipError_t launch_copy_cols(const void* src, int64_t ld_src_bytes, int64_t off_bytes, void* dst, int64_t ld_dst_bytes,
+                            int64_t nbytes, int rows, hipStream_t s) {
+  if (rows <= 0 || nbytes <= 0) return hipSuccess;
+  if ((ld_src_bytes | off_bytes | ld_dst_bytes | nbytes) & 15) return hipErrorInvalidValue;
+  const int nvec = (int)(nbytes / 16);
+  const int64_t total = (int64_t)rows * nvec;
+  int blocks = (int)std::min<int64_t>((total + 255) / 256, 16384);
+  copy_cols_kernel<<<blocks, 256, 0, s>>>((const char*)src, ld_src_bytes, off_bytes, (char*)dst, ld_dst_bytes, nvec,
+                                          rows);
+  return hipGetLastError();
+}
+
 // --------------------------------------------------------------------------- RMSNorm
 // One wave per row: out = h / sqrt(mean(h^2) + eps) * g.  fp32 in, act out.
 template <typename O>
@@ -75,8 +120,9 @@ hipError_t launch_rmsnorm(const float* h, const float* g, void* out, bool out_bf
 // tab[t * (dh/2) + j] = (cos, sin)(t * theta^(-2j/dh)) for t < max_len; the angle is
 // formed and reduced modulo 2*pi in double precision before the fp32 rounding.
 // pos[r] = position of row r inside its sequence.
-__global__ void rope_table_kernel(float2* tab, int32_t* pos, SeqTable st, int half, int dh, double log2_theta) {
-  const int64_t total = (int64_t)st.max_len * half;
+__global__ void rope_table_kernel(float2* tab, int32_t* pos, SeqTable st, int half, int dh, double log2_theta,
+                                  int pos0) {
+  const int64_t total = (int64_t)(pos0 + st.max_len) * half;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
     const int t = (int)(i / half), j = (int)(i - (int64_t)t * half);
@@ -89,16 +135,17 @@ __global__ void rope_table_kernel(float2* tab, int32_t* pos, SeqTable st, int ha
     tab[i] = make_float2((float)cv, (float)sv);
   }
   for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < st.rows; r += stride)
-    pos[r] = (int32_t)(r - st.off[seq_of_row(st, (int)r)]);
+    pos[r] = (int32_t)(pos0 + r - st.off[seq_of_row(st, (int)r)]);
 }
 
-hipError_t launch_rope_table(float2* tab, int32_t* pos, const SeqTable& st, int head_dim, float theta, hipStream_t s) {
+hipError_t launch_rope_table(float2* tab, int32_t* pos, const SeqTable& st, int head_dim, float theta, hipStream_t s,
+                             int pos0) {
   const int half = head_dim / 2;
-  const int64_t total = std::max((int64_t)st.max_len * half, (int64_t)st.rows);
+  const int64_t total = std::max((int64_t)(pos0 + st.max_len) * half, (int64_t)st.rows);
   int blocks = (int)((total + 255) / 256);
   if (blocks > 16384) blocks = 16384;
   if (blocks < 1) blocks = 1;
-  rope_table_kernel<<<blocks, 256, 0, s>>>(tab, pos, st, half, head_dim, log2((double)theta));
+  rope_table_kernel<<<blocks, 256, 0, s>>>(tab, pos, st, half, head_dim, log2((double)theta), pos0);
   return hipGetLastError();
 }
 

@@ -70,7 +70,14 @@ hipError_t launch_rmsnorm(const float* h, const float* g, void* out, bool out_bf
                           float eps, hipStream_t s);
 // Rotary table of a batch: tab[t * head_dim/2 + j] = (cos, sin)(t * theta^(-2j/head_dim)) for
 // t < max_len, and pos[r] = position of row r inside its sequence.
-hipError_t launch_rope_table(float2* tab, int32_t* pos, const SeqTable& st, int head_dim, float theta, hipStream_t s);
+// Rotary table for positions [0, pos0 + max_len) and the position of every row:
+// pos0 + its index within its sequence.
+hipError_t launch_rope_table(float2* tab, int32_t* pos, const SeqTable& st, int head_dim, float theta, hipStream_t s,
+                             int pos0 = 0);
+hipError_t launch_embed_gather(const void* emb, bool emb_bf16, const int32_t* tokens, const SeqTable& src,
+                               const SeqTable& dst, int pos0, float* h, int d, hipStream_t s);
+hipError_t launch_copy_cols(const void* src, int64_t ld_src_bytes, int64_t off_bytes, void* dst, int64_t ld_dst_bytes,
+                            int64_t nbytes, int rows, hipStream_t s);
 hipError_t launch_value_noise(void* v, bool bf16, int64_t row_stride, const SeqTable& st, int n_kv_heads,
                               int head_dim, int layer, float alpha, uint64_t seed, int protect_head,
                               int protect_tail, hipStream_t s);
@@ -98,8 +105,21 @@ struct GemmArgs {
 };
 hipError_t launch_gemm(const GemmArgs& a, bool bf16, hipStream_t s);
 
+// Cached prefix of the cached-window mode: every sequence k of the batch has P
+// cached positions, rows k * P .. k * P + P - 1 of the K cache (row stride ldk,
+// KV head h at columns h * d_h) and of the V cache (row stride ldv, same columns);
+// the attention rows of the batch are the positions P.. of each sequence and see
+// every cached position before their own causal keys.
+struct KvPrefix {
+  const bf16_t* k;
+  const bf16_t* v;
+  int64_t ldk, ldv;
+  int32_t P;
+};
+
 hipError_t launch_attention(const void* qkv, int64_t ldq, void* out, int64_t ldo, const SeqTable& st,
-                            int n_heads, int n_kv_heads, int head_dim, bool bf16, hipStream_t s);
+                            int n_heads, int n_kv_heads, int head_dim, bool bf16, hipStream_t s,
+                            const KvPrefix* prefix = nullptr);
 
 // Clean log-sum-exp of the LM head, fused (bf16): lse[r] = logsumexp_v (x[r] . W[v]).
 int lm_chunks(int rows, int vocab);

@@ -96,7 +96,8 @@ class Runner:
         import paper_2608_08684_amd as rk
         max_rows = max_rows or batch.rows
         flags = kw.get("flags", 0)
-        ws = empty_bytes(self.model.workspace_size(max_rows, max_group, rk.RK_WS_CLEAN_STATE | (flags & rk.RK_FLAG_UNFUSED_KL)))
+        ws = empty_bytes(self.model.workspace_size(
+            max_rows, max_group, rk.RK_WS_CLEAN_STATE | (flags & (rk.RK_FLAG_UNFUSED_KL | rk.RK_FLAG_CACHED_WINDOW))))
         s = torch.empty(len(alphas), len(layers), dtype=torch.float32, device="cuda")
         d = torch.empty(len(alphas), batch.n_seqs, len(layers), dtype=torch.float32, device="cuda") if want_d else None
         self.model.sensitivity_profile(batch, layers, alphas, s, ws, max_rows, max_group, d_out=d, **kw)

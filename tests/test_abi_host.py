@@ -202,3 +202,43 @@ def test_binding_fails_loudly_without_library(monkeypatch):
     monkeypatch.setattr(rk, "LIB_PATH", "/nonexistent/librk.so")
     with pytest.raises(RuntimeError):
         rk.load()
+
+
+def test_cached_window_entry_points_validate_before_launching():
+    """Argument checks of the cached-window mode (no kernel runs here)."""
+    lib = rk.load()
+    fake = ctypes.c_void_p(0x1000)
+    offs = np.array([0, 100, 250], dtype=np.int64)
+    batch = rk._Batch(fake, offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 2, 0)
+    big = 1 << 40
+    cw = rk.RK_FLAG_CACHED_WINDOW
+    # fp32 model: the mode is bf16 only
+    st, h32 = _create(_FakeCfg(dtype="f32"))
+    assert st == rk.RK_OK
+    assert lib.rk_window_state_size(h32, 100) == 0
+    assert lib.rk_window_reference(h32, ctypes.byref(batch), 50, fake, big, fake, big, None) == rk.RK_ERR_UNSUPPORTED
+    lib.rk_model_destroy(h32)
+    st, h = _create(_FakeCfg())
+    assert st == rk.RK_OK
+    assert lib.rk_window_state_size(h, 100) > lib.rk_clean_state_size(h, 100)
+    assert lib.rk_workspace_size(h, 100, 1, cw) > lib.rk_workspace_size(h, 100, 1, 0)
+    # window_start must leave a non-empty prefix and window in every sequence
+    for ws in (0, 100, 150):
+        assert lib.rk_window_reference(h, ctypes.byref(batch), ws, fake, big, fake, big, None) in (
+            rk.RK_ERR_ARG, rk.RK_ERR_SHAPE)
+    assert lib.rk_window_reference(h, ctypes.byref(batch), 50, fake, 16, fake, big, None) == rk.RK_ERR_WORKSPACE
+    assert lib.rk_window_reference(h, ctypes.byref(batch), 50, fake, big, fake, 16, None) == rk.RK_ERR_WORKSPACE
+    p = rk._Params(2, 50, 0, 0, cw)
+    assert lib.rk_profile_layer(h, ctypes.byref(batch), 0, 0.1, ctypes.byref(p), fake, 16, fake, None, None,
+                                fake, big, None) == rk.RK_ERR_WORKSPACE
+    p_long = rk._Params(2, 100, 0, 0, cw)
+    assert lib.rk_profile_layer(h, ctypes.byref(batch), 0, 0.1, ctypes.byref(p_long), fake, big, fake, None, None,
+                                fake, big, None) == rk.RK_ERR_SHAPE
+    p_both = rk._Params(2, 50, 0, 0, cw | rk.RK_FLAG_FULL_RECOMPUTE)
+    assert lib.rk_profile_layer(h, ctypes.byref(batch), 0, 0.1, ctypes.byref(p_both), fake, big, fake, None, None,
+                                fake, big, None) == rk.RK_ERR_ARG
+    lay = (ctypes.c_int32 * 1)(0)
+    alp = (ctypes.c_float * 1)(0.1)
+    assert lib.rk_sensitivity_profile(h, ctypes.byref(batch), lay, 1, alp, 1, ctypes.byref(p_long), 1000, 1, fake,
+                                      None, fake, big, None) == rk.RK_ERR_SHAPE
+    lib.rk_model_destroy(h)
