@@ -101,6 +101,33 @@ def family_flops(fam: str, cfg, rows: int, n_vocab_pass: int) -> float:
     raise ValueError(fam)
 
 
+def cpu_baseline_window(w, W, toks, window: int):
+    """Oracle cached-window profile of sequence 0 (prefix prefill and window
+    reference included), every layer, the largest alpha."""
+    from oracle import model as OM
+    from oracle import profile as OPR
+    from tests.gpu_helpers import f32_weights  # noqa: E402
+    cfg = w.model
+    m = OM.Model(cfg, f32_weights(cfg, W), np.float32)
+    t = toks[0]
+    P = len(t) - window
+    alpha = max(w.alphas)
+    t0 = time.perf_counter()
+    ws = OPR.window_clean_state(m, t, P)
+    for l in range(cfg.n_layers):
+        OPR.window_profile_layer(m, ws, 0, l, OPR.PerturbParams(alpha, window_start=P))
+    dt = time.perf_counter() - t0
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max(int(x.get("num_threads", 1)) for x in threadpool_info()) if threadpool_info() else os.cpu_count()
+    except Exception:
+        cores = os.cpu_count()
+    n = window * cfg.n_layers
+    return {"value": n / dt, "unit": "perturbed window token-layers/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"sequence 0 (prefix {P}, window {window}), all {cfg.n_layers} layers, alpha={alpha}, float32 "
+                      f"oracle: {dt:.1f} s for {n} window token-layers (prefix prefill and reference included)"}
+
+
 def cpu_baseline(w, W, toks, prefix: int = 2048):
     """Oracle (as it stands) on a bounded sample: the first `prefix` tokens of
     sequence 0 (a causal prefix computes exactly the same per-position values),
@@ -137,6 +164,9 @@ def main():
     ap.add_argument("--max-group", type=int, default=12)
     ap.add_argument("--family", default="gemm_gate_up", help="kernel family for the roofline figure")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--window", type=int, default=0,
+                    help="cached-window mode: evaluate the last WINDOW tokens of every sequence against the cached "
+                         "prefix (0: the resumed full-sequence profile)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (calibrates HBM byte counters)")
     ap.add_argument("--derive-traffic", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
@@ -180,14 +210,19 @@ def main():
     alphas = list(w.alphas)
     rows = batch.rows
     G = min(args.max_group, rk.RK_MAX_GROUP)
-    ws = torch.empty(model.workspace_size(rows, G, rk.RK_WS_CLEAN_STATE), dtype=torch.uint8, device="cuda")
+    window = int(args.window)
+    flags = rk.RK_FLAG_CACHED_WINDOW if window > 0 else 0
+    P = min(w.lengths()) - window if window > 0 else 0
+    if window > 0 and P < 1:
+        raise SystemExit(f"--window {window} leaves no prefix in the shortest sequence")
+    ws = torch.empty(model.workspace_size(rows, G, rk.RK_WS_CLEAN_STATE | flags), dtype=torch.uint8, device="cuda")
     s_out = torch.empty(len(alphas), len(layers), dtype=torch.float32, device="cuda")
     d_out = torch.empty(len(alphas), batch.n_seqs, len(layers), dtype=torch.float32, device="cuda")
     T_ref = max(w.lengths())
     budgets = [int(round(rho * T_ref * len(layers))) for rho in (0.1, 0.2, 0.3)]
 
     def step():
-        model.sensitivity_profile(batch, layers, alphas, s_out, ws, rows, G, d_out=d_out)
+        model.sensitivity_profile(batch, layers, alphas, s_out, ws, rows, G, d_out=d_out, window_start=P, flags=flags)
         s_host = s_out.cpu().numpy().astype(np.float64)     # synchronises
         out = []
         for a in range(len(alphas)):
@@ -207,12 +242,13 @@ def main():
     t1 = time.perf_counter()
     launches, fam_ms = rk.timing_end()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
-    tokens_layers = sum(w.lengths()) * len(layers) * len(alphas)
+    eval_rows = sum(T - P for T in w.lengths())     # rows each pass recomputes (all rows unless cached window)
+    tokens_layers = eval_rows * len(layers) * len(alphas)
     value = tokens_layers / (ms_per_step / 1e3)
 
     fam_avg_ms = fam_ms / max(launches, 1)
     n_pass_lm = G  # perturbed passes scored per LM-head launch (algorithmic: pert logits only)
-    flops = family_flops(args.family, cfg, rows, n_pass_lm)
+    flops = family_flops(args.family, cfg, eval_rows, n_pass_lm)
     achieved = flops / (fam_avg_ms / 1e3) / 1e12
     traffic = None
     rec = TRAFFIC.get((args.family, w.name))
@@ -224,8 +260,10 @@ def main():
             "flop_per_launch": flops}
     log(f"{args.family}: {launches} launches, avg {fam_avg_ms:.4f} ms, {achieved:.1f} TFLOP/s")
 
+    mode = "" if window == 0 else f"; cached window: prefix {P}, window {window} per sequence"
     res = {
-        "metric": "perturbed token-layers/s (sensitivity-profile throughput)",
+        "metric": ("perturbed token-layers/s (sensitivity-profile throughput)" if window == 0 else
+                   "perturbed window token-layers/s (cached-window sensitivity-profile throughput)"),
         "value": round(value, 1),
         "unit": "token-layers/s",
         "n_gpus": 1,
@@ -239,12 +277,12 @@ def main():
         "data": "synthetic (random-init N(0,0.02) weights, Zipf(1.1) tokens)",
         "config": {"workload": f"{w.name}: {cfg.n_layers}L d{cfg.d_model} {cfg.n_heads}x{cfg.head_dim} "
                                f"FFN{cfg.d_ff} V{cfg.vocab}; {batch.n_seqs}x{T_ref} tokens; "
-                               f"alpha {alphas}; all layers; ratios {list(w.ratios)}; budgets {budgets}",
+                               f"alpha {alphas}; all layers; ratios {list(w.ratios)}; budgets {budgets}{mode}",
                    "perturbed_token_layers_per_step": tokens_layers, "profile_wall_ms": round(ms_per_step, 3)},
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(w, W, toks)
+        res["cpu_baseline"] = cpu_baseline(w, W, toks) if window == 0 else cpu_baseline_window(w, W, toks, window)
     print(json.dumps(res), flush=True)
 
 

@@ -10,7 +10,8 @@
 //     the exponent of 2;
 //   * one workgroup = 4 waves x 32 queries of one head; it runs a pair of
 //     128-query blocks (nqb - 1 - x, then x) so all pairs of a sequence cost the
-//     same, longest sequences first;
+//     same, longest sequences first (one block per workgroup when the rows sit
+//     behind a cached prefix, which every block reads in full);
 //   * 64-key tiles of K and V go global -> LDS by buffer_load ... lds (no
 //     staging registers; rows past the sequence read as zero) through a
 //     ring of 2-3 stages;
@@ -200,9 +201,11 @@ __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_ker
   }
 
   const bf16x2_t ones = {(__bf16)1.0f, (__bf16)1.0f};
-  const int n_blocks = (x == nqb - 1 - x) ? 1 : 2;
+  // causal rows: the pair (nqb - 1 - x, x); behind a cached prefix every q-block
+  // costs about the same, so one q-block per item
+  const int n_blocks = PREFIX ? 1 : ((x == nqb - 1 - x) ? 1 : 2);
   for (int bi = 0; bi < n_blocks; ++bi) {
-    const int qb = bi == 0 ? nqb - 1 - x : x;
+    const int qb = (PREFIX || bi == 0) ? nqb - 1 - x : x;
     const int q0 = qb * BQ;
     const int my_q = min(q0 + w * 32 + l32, T - 1);   // rows past T duplicate row T - 1
     bf16x8_t qf[NKS];
@@ -383,10 +386,11 @@ hipError_t launch_attention(const void* qkv, int64_t ldq, void* out, int64_t ldo
       }
       wk.order[b] = v;
     }
+    const bool pre = prefix && prefix->P > 0;
     wk.cum[0] = 0;
     for (int j = 0; j < st.n; ++j) {
       const int k = wk.order[j], nqb = (st.off[k + 1] - st.off[k] + 127) / 128;
-      wk.cum[j + 1] = wk.cum[j] + (nqb + 1) / 2;
+      wk.cum[j + 1] = wk.cum[j] + (pre ? nqb : (nqb + 1) / 2);
     }
     wk.total = wk.cum[st.n];
     if (wk.total == 0) return hipSuccess;
@@ -396,7 +400,6 @@ hipError_t launch_attention(const void* qkv, int64_t ldq, void* out, int64_t ldo
     const int n_items = wk.total * n_heads;
     const int grid = (n_items + 8 * grp - 1) / (8 * grp) * (8 * grp);
     KvPrefix pk{};
-    const bool pre = prefix && prefix->P > 0;
     if (pre) {
       pk = *prefix;
       if ((int64_t)st.n * pk.P * std::max(pk.ldk, pk.ldv) * 2 >= ((int64_t)1 << 31)) return hipErrorInvalidValue;

@@ -328,11 +328,16 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 
 // --------------------------------------------------------------------------- dispatch
 // Tile choice (measured on MI355X over the decoder's projection shapes): a
-// 256x256 tile on 8 waves (2x4, 128x64 per wave) wherever it divides N;
-// otherwise 128x128 on 4 waves.
+// 256x256 tile on 8 waves (2x4, 128x64 per wave) wherever it divides N and
+// yields at least half a wave of tiles; otherwise 128x128 on 4 waves.
 static void pick_tile(const GemmArgs& a, bool swiglu, int* bm, int* bn_, int* bk, int* waves, int* stages) {
   const bool fits256 = swiglu ? (a.d_ff % 128 == 0) : (a.N % 256 == 0);
-  if (fits256 && a.K % 64 == 0) { *bm = 256; *bn_ = 256; *bk = 64; *waves = 8; *stages = 2; return; }
+  // fewer than half a wave of 256x256 tiles on 256 CUs (small M, e.g. window rows): smaller tiles
+  const int64_t tiles256 = (int64_t)((a.M + 255) / 256) * (a.N / 256);
+  if (fits256 && a.K % 64 == 0 && tiles256 >= 128) {
+    *bm = 256; *bn_ = 256; *bk = 64; *waves = 8; *stages = 2;
+    return;
+  }
   *bm = 128; *bn_ = 128; *bk = 64; *waves = 4; *stages = 2;
 }
 

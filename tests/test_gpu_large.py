@@ -110,3 +110,47 @@ def test_large_workload(name, llama_weights):
             assert err.max() <= LOGIT_MAX_32L and np.median(err) <= LOGIT_MEDIAN_32L
     del m, st
     gc.collect()
+
+
+def test_cached_window_llama3_8b_shape(llama_weights):
+    """The cached-window mode at the Llama-3-8B shape (GQA 32q/8kv x 128, 32
+    layers): a sequence of 4096 tokens of the workload runs with a 3840-token
+    cached prefix and a 256-token window through rk_sensitivity_profile; the
+    oracle (float32) checks the per-layer d on a 320-token sequence (prefix 192,
+    window 128) run through rk_profile_layer, for the first and the last layer."""
+    import torch
+    import paper_2608_08684_amd as rk
+    from gpu_helpers import empty_bytes
+    w = F.get_workload("llama3-8b-bf16")
+    cfg = w.model
+    W = llama_weights
+    L = cfg.n_layers
+    run = Runner(cfg, W)
+    toks = F.make_tokens(w)
+    # full-size window profile: sequence 0 at 4096 tokens, window 256
+    big = make_batch([toks[0][:4096]])
+    s, d = run.profile(big, [0, L - 1], [0.05, 0.1], max_group=4, window_start=3840,
+                       flags=rk.RK_FLAG_CACHED_WINDOW)
+    log(f"cached window 8B shape, 3840 + 256 tokens: s = {s.tolist()}")
+    assert np.all(np.isfinite(s)) and np.all(s > 0) and np.all(s[1] > s[0])
+    del big
+    _free()
+    # oracle check on a short sequence
+    Pw, T = 192, 320
+    t = toks[1][:T]
+    b = make_batch([t])
+    st = empty_bytes(run.model.window_state_size(b.rows))
+    ws = empty_bytes(run.model.workspace_size(b.rows, 1, rk.RK_FLAG_CACHED_WINDOW))
+    run.model.window_reference(b, Pw, st, ws)
+    m = OM.Model(cfg, f32_weights(cfg, W), np.float32)
+    wref = OPR.window_clean_state(m, t, Pw)
+    for l in (0, L - 1):
+        dg = torch.empty(1, dtype=torch.float32, device="cuda")
+        run.model.profile_layer(b, l, 0.1, st, dg, ws, window_start=Pw, flags=rk.RK_FLAG_CACHED_WINDOW)
+        torch.cuda.synchronize()
+        g = float(dg.cpu()[0])
+        r, _ = OPR.window_profile_layer(m, wref, 0, l, OPR.PerturbParams(0.1, window_start=Pw))
+        log(f"cached window 8B shape layer {l}: d gpu {g:.6e} oracle {r:.6e} rel {abs(g - r) / r:.2e}")
+        assert abs(g - r) <= KL_REL * r or abs(g - r) <= KL_ABS
+    del m, wref, run
+    _free()
