@@ -164,6 +164,7 @@ def main():
     ap.add_argument("--max-group", type=int, default=12)
     ap.add_argument("--family", default="gemm_gate_up", help="kernel family for the roofline figure")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying a HIP graph")
     ap.add_argument("--window", type=int, default=0,
                     help="cached-window mode: evaluate the last WINDOW tokens of every sequence against the cached "
                          "prefix (0: the resumed full-sequence profile)")
@@ -211,11 +212,12 @@ def main():
     rows = batch.rows
     G = min(args.max_group, rk.RK_MAX_GROUP)
     window = int(args.window)
-    flags = rk.RK_FLAG_CACHED_WINDOW if window > 0 else 0
+    flags = (rk.RK_FLAG_CACHED_WINDOW if window > 0 else 0) | (0 if args.no_graph else rk.RK_FLAG_GRAPH)
     P = min(w.lengths()) - window if window > 0 else 0
     if window > 0 and P < 1:
         raise SystemExit(f"--window {window} leaves no prefix in the shortest sequence")
-    ws = torch.empty(model.workspace_size(rows, G, rk.RK_WS_CLEAN_STATE | flags), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(model.workspace_size(rows, G, rk.RK_WS_CLEAN_STATE | (flags & rk.RK_FLAG_CACHED_WINDOW)),
+                     dtype=torch.uint8, device="cuda")
     s_out = torch.empty(len(alphas), len(layers), dtype=torch.float32, device="cuda")
     d_out = torch.empty(len(alphas), batch.n_seqs, len(layers), dtype=torch.float32, device="cuda")
     T_ref = max(w.lengths())
@@ -231,16 +233,25 @@ def main():
                     out.append(rk.layer_budgets(s_host[a], B, r)[1])
         return out
 
+    # Each step runs in its own kernel-timing session (the timed family's launches
+    # carry HIP events on the launch stream; with a replayed graph the events are
+    # nodes of the graph), so warm-up also captures the graph that the timed steps
+    # replay.
     for _ in range(args.warmup):
+        rk.timing_begin(args.family)
         step()
+        rk.timing_end()
     torch.cuda.synchronize()
-    rk.timing_begin(args.family)
+    launches, fam_ms = 0, 0.0
     t0 = time.perf_counter()
     for _ in range(args.steps):
+        rk.timing_begin(args.family)
         step()
+        n, ms = rk.timing_end()
+        launches += n
+        fam_ms += ms
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    launches, fam_ms = rk.timing_end()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     eval_rows = sum(T - P for T in w.lengths())     # rows each pass recomputes (all rows unless cached window)
     tokens_layers = eval_rows * len(layers) * len(alphas)
@@ -275,6 +286,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (random-init N(0,0.02) weights, Zipf(1.1) tokens)",
+        "launch": "eager" if args.no_graph else "HIP graph replay",
         "config": {"workload": f"{w.name}: {cfg.n_layers}L d{cfg.d_model} {cfg.n_heads}x{cfg.head_dim} "
                                f"FFN{cfg.d_ff} V{cfg.vocab}; {batch.n_seqs}x{T_ref} tokens; "
                                f"alpha {alphas}; all layers; ratios {list(w.ratios)}; budgets {budgets}{mode}",

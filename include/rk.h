@@ -71,6 +71,16 @@ typedef enum {
 #define RK_FLAG_UNFUSED_KL     0x2u  /* materialise fp32 logits and run the separate
                                         log-softmax + KL kernel instead of the fused
                                         LM-head + KL kernel                          */
+#define RK_FLAG_GRAPH          0x8u  /* rk_sensitivity_profile only: the first call
+                                        runs eagerly and records its launch sequence
+                                        in a HIP graph; later calls replay the graph
+                                        while every argument (device pointers, sizes,
+                                        host arrays) stays the same;
+                                        one graph per process, replaced when the
+                                        arguments change.  Saves the per-launch
+                                        overhead of the ~10^3-10^4 kernels of a
+                                        profile.  With kernel timing on, each graphed
+                                        call needs its own rk_timing_begin.         */
 #define RK_FLAG_CACHED_WINDOW  0x4u  /* the literal reading of Section 4.3: each
                                         sequence is a cached prefix [0, P) and an
                                         evaluation window [P, T_i), P = window_start;

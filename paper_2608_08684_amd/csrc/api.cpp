@@ -20,6 +20,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <functional>
 #include <string>
 #include <vector>
 
@@ -502,7 +503,7 @@ static rk_status check_params(const rk_perturb_params* p) {
     set_error("window_start / protect_head / protect_tail must be >= 0");
     return RK_ERR_ARG;
   }
-  if (p->flags & ~(RK_FLAG_FULL_RECOMPUTE | RK_FLAG_UNFUSED_KL | RK_FLAG_CACHED_WINDOW)) {
+  if (p->flags & ~(RK_FLAG_FULL_RECOMPUTE | RK_FLAG_UNFUSED_KL | RK_FLAG_CACHED_WINDOW | RK_FLAG_GRAPH)) {
     set_error("unknown flags");
     return RK_ERR_ARG;
   }
@@ -515,6 +516,78 @@ static rk_status check_params(const rk_perturb_params* p) {
 
 static rk_status check_window_model(const rk_model* m) {
   if (!m->bf16) { set_error("the cached-window mode needs a bf16 model"); return RK_ERR_UNSUPPORTED; }
+  return RK_OK;
+}
+
+// One recorded launch sequence per process: the sensitivity profile's kernels
+// captured on a private stream into a HIP graph (after an eager run of the same
+// call), replayed on the caller's stream while the arguments stay the same.
+// With kernel timing on, the graph also holds the timing events (recorded as event
+// nodes during capture); a replay re-records the same events, so the timing
+// session sees the same event pairs as the captured call (timing_begin must
+// precede each graphed call).
+struct GraphCache {
+  std::vector<uint64_t> key;
+  hipGraphExec_t exec = nullptr;
+  hipStream_t cap = nullptr;
+  size_t timed = 0;   // timing event pairs inside the graph
+};
+static GraphCache g_graph;
+
+template <class F>
+static rk_status run_graphed(std::vector<uint64_t> key, F&& run, hipStream_t s) {
+  key.push_back(g_timing.on ? std::hash<std::string>()(g_timing.family) : 0);
+  if (g_timing.on && g_timing.used != 0) {
+    set_error("a graphed call needs a fresh timing session (rk_timing_begin) when timing is on");
+    return RK_ERR_ARG;
+  }
+  if (g_graph.exec && g_graph.key == key) {
+    RK_TRY(hipGraphLaunch(g_graph.exec, s));
+    if (g_timing.on) g_timing.used = g_graph.timed;
+    return RK_OK;
+  }
+  // first use: run eagerly (this call's results and timing events), then record
+  // the same sequence for the replays; the recording reuses the timing events the
+  // eager run created (no event is created while a stream is capturing)
+  rk_status e = run(s);
+  if (e != RK_OK) return e;
+  if (!g_graph.cap) RK_TRY(hipStreamCreateWithFlags(&g_graph.cap, hipStreamNonBlocking));
+  if (g_graph.exec) {
+    RK_TRY(hipGraphExecDestroy(g_graph.exec));
+    g_graph.exec = nullptr;
+    g_graph.key.clear();
+  }
+  const size_t used = g_timing.used;
+  g_timing.used = 0;
+  RK_TRY(hipStreamBeginCapture(g_graph.cap, hipStreamCaptureModeThreadLocal));
+  e = run(g_graph.cap);
+  hipGraph_t graph = nullptr;
+  const hipError_t ec = hipStreamEndCapture(g_graph.cap, &graph);
+  const size_t timed = g_timing.used;
+  g_timing.used = used;
+  if (e != RK_OK) {
+    if (graph) (void)hipGraphDestroy(graph);
+    return e;
+  }
+  if (ec != hipSuccess) {
+    set_error("HIP graph capture failed: %s", hipGetErrorString(ec));
+    return RK_ERR_HIP;
+  }
+  if (g_timing.on && timed != used) {
+    (void)hipGraphDestroy(graph);
+    set_error("recorded launch sequence differs from the eager one");
+    return RK_ERR_HIP;
+  }
+  hipGraphExec_t exec = nullptr;
+  const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(graph);
+  if (ei != hipSuccess) {
+    set_error("HIP graph instantiation failed: %s", hipGetErrorString(ei));
+    return RK_ERR_HIP;
+  }
+  g_graph.exec = exec;
+  g_graph.key = key;
+  g_graph.timed = g_timing.on ? used : 0;
   return RK_OK;
 }
 
@@ -737,9 +810,9 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
   const WsPlan wp = ws_plan(m, max_rows, max_group, wflags);
   if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
 
-  hipStream_t s = (hipStream_t)stream;
   // Buffers are carved for max_rows; each batch uses the leading rows of each.
   const Bufs b = carve(wp, workspace);
+  auto run = [&](hipStream_t s) -> rk_status {
   RK_TRY(launch_zero_f64(b.sacc, n_A * n_alpha, s));
   const int n_pass = n_A * n_alpha;
   int first = 0;
@@ -808,6 +881,29 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
   }
   RK_TRY(launch_finalize(b.sacc, n_pass, 1.0 / (double)N, s_out, s));
   return RK_OK;
+  };
+  if (!(p->flags & RK_FLAG_GRAPH)) return run((hipStream_t)stream);
+  // the key: everything the launch sequence bakes in
+  std::vector<uint64_t> key;
+  auto put = [&](uint64_t v) { key.push_back(v); };
+  put((uint64_t)(uintptr_t)m);
+  put((uint64_t)(uintptr_t)m->tok_emb); put((uint64_t)(uintptr_t)m->lm_head); put((uint64_t)(uintptr_t)m->final_norm);
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    put((uint64_t)(uintptr_t)m->w_qkv[l]); put((uint64_t)(uintptr_t)m->w_o[l]);
+    put((uint64_t)(uintptr_t)m->w_gate_up[l]); put((uint64_t)(uintptr_t)m->w_down[l]);
+    put((uint64_t)(uintptr_t)m->attn_norm[l]); put((uint64_t)(uintptr_t)m->mlp_norm[l]);
+  }
+  put((uint64_t)(uintptr_t)calib->tokens); put((uint64_t)N); put((uint64_t)calib->seq_index0);
+  for (int i = 0; i <= N; ++i) put((uint64_t)calib->offsets[i]);
+  put((uint64_t)n_A);
+  for (int j = 0; j < n_A; ++j) put((uint64_t)layers[j]);
+  put((uint64_t)n_alpha);
+  for (int a = 0; a < n_alpha; ++a) { uint32_t u; memcpy(&u, &alphas[a], 4); put(u); }
+  put(p->seed); put((uint64_t)p->window_start); put((uint64_t)p->protect_head); put((uint64_t)p->protect_tail);
+  put(p->flags); put((uint64_t)max_rows); put((uint64_t)max_group);
+  put((uint64_t)(uintptr_t)s_out); put((uint64_t)(uintptr_t)d_out); put((uint64_t)(uintptr_t)workspace);
+  put((uint64_t)ws_bytes);
+  return run_graphed(key, run, (hipStream_t)stream);
 }
 
 rk_status rk_perturb_values(const rk_model* m, const rk_batch* batch, int32_t layer, float alpha,
