@@ -31,12 +31,31 @@ __device__ __forceinline__ void store8(bf16_t* p, const float* v) {
   *reinterpret_cast<v4u*>(p) = u;
 }
 
+// 4 values to 4 consecutive elements (16 bytes fp32, 8 bytes bf16)
+__device__ __forceinline__ void store4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+__device__ __forceinline__ void store4(bf16_t* p, float4 v) {
+  uint2 u;
+  u.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
+  u.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+  *reinterpret_cast<uint2*>(p) = u;
+}
+// 16 bytes between LDS and global memory (the LDS side 8-byte aligned for bf16 rows)
+__device__ __forceinline__ void copy16(float* dst, const float* src) {
+  *reinterpret_cast<float4*>(dst) = *reinterpret_cast<const float4*>(src);
+}
+__device__ __forceinline__ void copy16(bf16_t* dst, const bf16_t* src) {
+  const uint2 a = reinterpret_cast<const uint2*>(src)[0], b = reinterpret_cast<const uint2*>(src)[1];
+  *reinterpret_cast<uint4*>(dst) = make_uint4(a.x, a.y, b.x, b.y);
+}
+
 // --------------------------------------------------------------------------- epilogues
 // Called per (row, 8 consecutive output columns starting at c0) with cs = the
 // staged fp32 row of a BN-wide tile.  out_cols(BN) = output columns per tile.
 template <typename O>
 struct EpiRope {
   static constexpr int out_cols(int BN) { return BN; }
+  static constexpr bool kPaired = true;
+  static constexpr int pair_dist(int, int head_dim) { return head_dim / 2; }
   // tab[pos * head_dim/2 + j] = (cos, sin) of position pos, pair j; pos[row] = position of the row
   O* out; int64_t ldo; int rope_cols; int head_dim; const float2* tab; const int32_t* pos; int q_cols; float q_scale;
   template <int BN>
@@ -66,11 +85,33 @@ struct EpiRope {
     }
     store8(dst, v);
   }
+  // register form: x = tile columns tc..tc+3 (first half of a head), y = their
+  // partners head_dim/2 further on; o0, o1 = the outputs at the same columns
+  using stage_t = O;
+  static constexpr int kOut = 2;
+  template <int BN>
+  __device__ __forceinline__ void pair(int row, int bn, int tc, float4 x, float4 y, float4& o0, float4& o1) const {
+    const int gc = bn * BN + tc, half = head_dim >> 1;
+    if (gc >= rope_cols) {  // value columns: no rotation
+      o0 = x;
+      o1 = y;
+      return;
+    }
+    const float4* t4 = reinterpret_cast<const float4*>(tab + (int64_t)pos[row] * half + (gc & (head_dim - 1)));
+    const float4 t01 = t4[0], t23 = t4[1];   // (cos, sin) of pairs j .. j+3
+    const float sc = gc < q_cols ? q_scale : 1.0f;
+    o0 = make_float4(fmaf(-y.x, t01.y, x.x * t01.x) * sc, fmaf(-y.y, t01.w, x.y * t01.z) * sc,
+                     fmaf(-y.z, t23.y, x.z * t23.x) * sc, fmaf(-y.w, t23.w, x.w * t23.z) * sc);
+    o1 = make_float4(fmaf(x.x, t01.y, y.x * t01.x) * sc, fmaf(x.y, t01.w, y.y * t01.z) * sc,
+                     fmaf(x.z, t23.y, y.z * t23.x) * sc, fmaf(x.w, t23.w, y.w * t23.z) * sc);
+  }
 };
 
 struct EpiResidual {
   static constexpr int out_cols(int BN) { return BN; }
+  static constexpr bool kPaired = false;
   float* out; int64_t ldo; const float* res; int64_t ldr;
+  using stage_t = float;
   template <int BN>
   __device__ void apply(int row, int bn, int c0, const float* cs) const {
     const int64_t n = (int64_t)bn * BN + c0;
@@ -85,7 +126,20 @@ struct EpiResidual {
 template <typename O>
 struct EpiSwiGLU {
   static constexpr int out_cols(int BN) { return BN / 2; }  // tile columns [0, BN/2) gate, [BN/2, BN) up
+  static constexpr bool kPaired = true;
+  static constexpr int pair_dist(int BN, int) { return BN / 2; }
   O* out; int64_t ldo;
+  static __device__ __forceinline__ float silu_mul(float g, float u) {
+    return g * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-g * 1.4426950408889634f)) * u;
+  }
+  // register form: gate = tile columns tc..tc+3 (< BN/2), up = the same columns + BN/2;
+  // o0 = output columns tc..tc+3 of this tile
+  using stage_t = O;
+  static constexpr int kOut = 1;
+  template <int BN>
+  __device__ __forceinline__ void pair(int, int, int, float4 g, float4 u, float4& o0, float4&) const {
+    o0 = make_float4(silu_mul(g.x, u.x), silu_mul(g.y, u.y), silu_mul(g.z, u.z), silu_mul(g.w, u.w));
+  }
   template <int BN>
   __device__ void apply(int row, int bn, int c0, const float* cs) const {
     // silu(g) = g / (1 + e^-g) with the hardware exp2 and reciprocal (about 1 ulp
@@ -103,7 +157,9 @@ struct EpiSwiGLU {
 
 struct EpiStoreF32 {
   static constexpr int out_cols(int BN) { return BN; }
+  static constexpr bool kPaired = false;
   float* out; int64_t ldo;
+  using stage_t = float;
   template <int BN>
   __device__ void apply(int row, int bn, int c0, const float* cs) const {
     store8(out + (int64_t)row * ldo + (int64_t)bn * BN + c0, cs + c0);
@@ -131,7 +187,11 @@ __device__ __forceinline__ int b_row(int bn, int n, int d_ff) {
 }
 
 // --------------------------------------------------------------------------- bf16 MFMA kernel
-template <int BM, int BN, int BK, int NWM, int NWN, int STAGES, class E, bool SWIGLU>
+// PD: distance in tile columns between the two values an epilogue combines (a
+// rotary pair, gate/up); wave wn's two 32-column blocks are c and c + PD with
+// c = (wn / (PD/32)) * 2 PD + (wn % (PD/32)) * 32, so each lane holds both
+// values in registers.  PD = 32 is the plain layout (wave wn: columns 64 wn ..).
+template <int BM, int BN, int BK, int NWM, int NWN, int STAGES, int PD, class E, bool SWIGLU>
 __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t* __restrict__ A, int64_t lda,
                                                                   const bf16_t* __restrict__ B, int64_t ldb, int M,
                                                                   int K, int d_ff, int n_bn, int group_m, E e) {
@@ -140,16 +200,26 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t*
   constexpr int MI = WTM / 32, NI = WTN / 32;     // 32x32 blocks per wave
   constexpr int CH = BK / 8;                      // 16-byte chunks per tile row
   constexpr int AS = BM * CH, BS = BN * CH;       // 16-byte slots per stage
-  constexpr int PIPE = STAGES * (AS + BS), STAGE_OUT = 64 * (BN + 4) / 4;
+  constexpr int PIPE = STAGES * (AS + BS);
+  static_assert(NI == 2 && BN % (2 * PD) == 0 && PD % 32 == 0, "two 32-column blocks per wave, pairs inside the tile");
+  // Epilogue staging: paired epilogues stage their outputs (type O), the others the
+  // fp32 accumulators; rows padded by 4 elements; in ROUNDS passes over the rows
+  // when the whole tile would not fit.
+  using SO = typename E::stage_t;
+  constexpr int OC = E::out_cols(BN), SP = OC + 4;
+  constexpr int ROUNDS = BM * SP * (int)sizeof(SO) <= 136 * 1024 ? 1 : (BM * SP * (int)sizeof(SO) <= 272 * 1024 ? 2 : 4);
+  static_assert(MI % ROUNDS == 0, "staging rounds split each wave's rows evenly");
+  constexpr int STG = (BM / ROUNDS) * SP * (int)sizeof(SO) / 16;
+  static_assert(PIPE * 16 <= 160 * 1024 && STG * 16 <= 160 * 1024, "LDS");
   // DMA instructions per thread and stage (A tile, then B tile or its gate and up halves)
   constexpr int NL = (BM * CH + BN * CH) / (64 * NW);
   static_assert(STAGES >= 2 && (STAGES - 2) * NL < 16, "ring depth");
-  static_assert(WTM >= 64 && WTM % 64 == 0, "a 64-row staging slice must lie inside one wave row");
-  __shared__ __attribute__((aligned(16))) v4u smem[PIPE > STAGE_OUT ? PIPE : STAGE_OUT];
+  __shared__ __attribute__((aligned(16))) v4u smem[PIPE > STG ? PIPE : STG];
   v4u* As = smem;
   v4u* Bs = smem + STAGES * AS;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31;
   const int wm = w / NWN, wn = w % NWN;
+  const int wcol = (wn / (PD / 32)) * (2 * PD) + (wn % (PD / 32)) * 32;   // tile column of block ni = 0
   int bm_, bn;
   xcd_tile((int)blockIdx.x, (M + BM - 1) / BM, n_bn, group_m, &bm_, &bn);
   const int m0 = bm_ * BM;
@@ -209,7 +279,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t*
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi) af[0][mi] = frag<CH>(At, wm * WTM + mi * 32 + l32, 0, lane);
 #pragma unroll
-    for (int ni = 0; ni < NI; ++ni) bfr[0][ni] = frag<CH>(Bt, wn * WTN + ni * 32 + l32, 0, lane);
+    for (int ni = 0; ni < NI; ++ni) bfr[0][ni] = frag<CH>(Bt, wcol + ni * PD + l32, 0, lane);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
@@ -218,7 +288,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t*
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) af[c ^ 1][mi] = frag<CH>(At, wm * WTM + mi * 32 + l32, ks + 1, lane);
 #pragma unroll
-        for (int ni = 0; ni < NI; ++ni) bfr[c ^ 1][ni] = frag<CH>(Bt, wn * WTN + ni * 32 + l32, ks + 1, lane);
+        for (int ni = 0; ni < NI; ++ni) bfr[c ^ 1][ni] = frag<CH>(Bt, wcol + ni * PD + l32, ks + 1, lane);
       }
       if (copy) {
 #pragma unroll
@@ -230,7 +300,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t*
       for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
         for (int ni = 0; ni < NI; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[c][mi], bfr[c][ni], acc[mi][ni], 0, 0, 0);
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[c][ni], af[c][mi], acc[mi][ni], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -244,30 +314,57 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t*
     kstep(kt, cur, nxt, false, true);
     cur = cur == STAGES - 1 ? 0 : cur + 1;
   }
-  __syncthreads();   // the staging area below overlaps the ring
-
-  // Stage 64 rows at a time and run the epilogue on whole rows.
-  float* Cs = reinterpret_cast<float*>(smem);
-  constexpr int CSS = BN + 4;
+  // Epilogue.  The MFMAs above take B as the first operand, so acc[mi][ni] is the
+  // transposed 32x32 block: lane l holds row l % 32 and, in elements 4g..4g+3,
+  // the four consecutive columns 8 g + 4 (l / 32) .. +3 of the block.  Paired
+  // epilogues combine blocks 0 and 1 (columns c and c + PD) in registers; the
+  // results go through LDS so the global accesses are whole rows.
+  __syncthreads();   // the staging area overlaps the ring
+  SO* Cs = reinterpret_cast<SO*>(smem);
+  constexpr int WR = WTM / ROUNDS, MIR = MI / ROUNDS;   // rows per wave and round, blocks per round
 #pragma unroll
-  for (int slice = 0; slice < BM / 64; ++slice) {
-    const int owner = (slice * 64) / WTM;
-    const int mi0 = (slice * 64 - owner * WTM) / 32;
-    if (wm == owner) {
+  for (int h = 0; h < ROUNDS; ++h) {
+    if (h) __syncthreads();   // the previous round has been written out
 #pragma unroll
-      for (int mm = 0; mm < 2; ++mm)
+    for (int q = 0; q < MIR; ++q) {
+      const int mi = h * MIR + q;
+      const int row = m0 + wm * WTM + mi * 32 + l32;
+      SO* cs = Cs + (wm * WR + q * 32 + l32) * SP;
 #pragma unroll
-        for (int ni = 0; ni < NI; ++ni)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int r = mm * 32 + (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
-            const int c = wn * WTN + ni * 32 + l32;
-            Cs[r * CSS + c] = acc[mi0 + mm][ni][i];
-          }
+      for (int g = 0; g < 4; ++g) {
+        const int tc = wcol + g * 8 + (lane >> 5) * 4;
+        const float4 x = make_float4(acc[mi][0][4 * g], acc[mi][0][4 * g + 1], acc[mi][0][4 * g + 2], acc[mi][0][4 * g + 3]);
+        const float4 y = make_float4(acc[mi][1][4 * g], acc[mi][1][4 * g + 1], acc[mi][1][4 * g + 2], acc[mi][1][4 * g + 3]);
+        if constexpr (E::kPaired) {
+          float4 o0 = make_float4(0.f, 0.f, 0.f, 0.f), o1 = o0;
+          if (row < M) e.template pair<BN>(row, bn, tc, x, y, o0, o1);
+          store4(cs + tc, o0);
+          if constexpr (E::kOut == 2) store4(cs + tc + PD, o1);
+        } else {
+          store4(cs + tc, x);
+          store4(cs + tc + PD, y);
+        }
+      }
     }
     __syncthreads();
-    run_epilogue<BN, E, NT>(e, Cs, m0 + slice * 64, M, bn);
-    __syncthreads();
+    // staged row r is tile row (r / WR) * WTM + h * WR + r % WR
+    if constexpr (E::kPaired) {
+      constexpr int CE = 16 / (int)sizeof(SO), CPR = OC / CE, RPP = NT / CPR;
+      static_assert(NT % CPR == 0, "whole rows per pass");
+      const int c = (tid % CPR) * CE;
+      for (int r = tid / CPR; r < BM / ROUNDS; r += RPP) {
+        const int row = m0 + (r / WR) * WTM + h * WR + r % WR;
+        if (row < M) copy16(e.out + (int64_t)row * e.ldo + (int64_t)bn * OC + c, Cs + r * SP + c);
+      }
+    } else {
+      constexpr int TPR = OC / 8, RPP = NT / TPR;
+      static_assert(NT % TPR == 0, "whole rows per pass");
+      const int c0 = (tid % TPR) * 8;
+      for (int r = tid / TPR; r < BM / ROUNDS; r += RPP) {
+        const int row = m0 + (r / WR) * WTM + h * WR + r % WR;
+        if (row < M) e.template apply<BN>(row, bn, c0, Cs + r * SP);
+      }
+    }
   }
 }
 
@@ -341,13 +438,28 @@ static void pick_tile(const GemmArgs& a, bool swiglu, int* bm, int* bn_, int* bk
   *bm = 128; *bn_ = 128; *bk = 64; *waves = 4; *stages = 2;
 }
 
-template <int BM, int BN, int BK, int ST, class E, bool SWIGLU, int NWM = 2, int NWN = 2>
-static void go_bf16(const GemmArgs& a, const E& e, hipStream_t s) {
+template <int BM, int BN, int BK, int ST, int PD, class E, bool SWIGLU, int NWM, int NWN>
+static void go_pd(const GemmArgs& a, const E& e, hipStream_t s) {
   const int nbn = SWIGLU ? a.d_ff / (BN / 2) : a.N / BN;
   const int nbm = (a.M + BM - 1) / BM;
   const int group_m = a.group_m > 0 ? a.group_m : 8;
-  gemm_bf16_kernel<BM, BN, BK, NWM, NWN, ST, E, SWIGLU><<<nbm * nbn, 64 * NWM * NWN, 0, s>>>(
+  gemm_bf16_kernel<BM, BN, BK, NWM, NWN, ST, PD, E, SWIGLU><<<nbm * nbn, 64 * NWM * NWN, 0, s>>>(
       (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.K, a.d_ff, nbn, group_m, e);
+}
+
+// the pair distance each epilogue needs (plain layout when it pairs nothing)
+template <int BM, int BN, int BK, int ST, class E, bool SWIGLU, int NWM = 2, int NWN = 2>
+static hipError_t go_bf16(const GemmArgs& a, const E& e, hipStream_t s) {
+  if constexpr (!E::kPaired) {
+    go_pd<BM, BN, BK, ST, 32, E, SWIGLU, NWM, NWN>(a, e, s);
+  } else if constexpr (SWIGLU) {
+    go_pd<BM, BN, BK, ST, BN / 2, E, SWIGLU, NWM, NWN>(a, e, s);
+  } else {
+    if (a.head_dim == 64) go_pd<BM, BN, BK, ST, 32, E, SWIGLU, NWM, NWN>(a, e, s);
+    else if (a.head_dim == 128) go_pd<BM, BN, BK, ST, 64, E, SWIGLU, NWM, NWN>(a, e, s);
+    else return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 template <class E, bool SWIGLU>
@@ -360,18 +472,14 @@ static hipError_t go(const GemmArgs& a, bool bf16, const E& e, hipStream_t s) {
       st = a.tile_stages ? a.tile_stages : 2;
     }
 #define RK_TILE(BM_, BN_, BK_, W_, ST_, NWM_, NWN_)                                     \
-  if (bm == BM_ && bn == BN_ && bk == BK_ && waves == W_ && st == ST_) {                \
-    go_bf16<BM_, BN_, BK_, ST_, E, SWIGLU, NWM_, NWN_>(a, e, s);                        \
-    return hipGetLastError();                                                          \
-  }
+  if (bm == BM_ && bn == BN_ && bk == BK_ && waves == W_ && st == ST_)                  \
+    return go_bf16<BM_, BN_, BK_, ST_, E, SWIGLU, NWM_, NWN_>(a, e, s);
+    // every variant gives each wave two 32-column blocks (BN = 64 NWN)
     RK_TILE(256, 256, 64, 8, 2, 2, 4)
     RK_TILE(256, 256, 32, 8, 3, 2, 4)
     RK_TILE(256, 256, 32, 8, 4, 2, 4)
-    RK_TILE(256, 128, 64, 8, 3, 2, 4)
-    RK_TILE(256, 256, 64, 4, 2, 2, 2)
     RK_TILE(128, 128, 64, 4, 2, 2, 2)
     RK_TILE(128, 128, 64, 4, 3, 2, 2)
-    RK_TILE(128, 256, 32, 4, 4, 2, 2)
 #undef RK_TILE
     return hipErrorInvalidValue;
   } else {
