@@ -118,9 +118,11 @@ static WsPlan ws_plan(const rk_model* m, int64_t R, int G, uint32_t flags) {
   p.xp = o;       o += align256((size_t)G * Rp * c.d_model * a);
   p.part = o;
   if (m->bf16) {
-    // chunks(rows) * rows <= min(n_vt * 128 * n_tt, (2048 + n_tt) * 128) for rows <= R
-    const size_t n_vt = c.vocab / 128, n_tt = (R + 127) / 128;
-    const size_t bound = std::min(n_vt * 128 * n_tt, (2048 + n_tt) * 128);
+    // lm_chunks(rows) * rows <= min(n_vt * 128 * n_tt, (2048 + n_tt) * 128) and
+    // lm_kl_chunks(rows) * rows <= min(n_vt * 256 * n_tb, (1024 + n_tb) * 256) for rows <= R
+    const size_t n_vt = c.vocab / 128, n_tt = (R + 127) / 128, n_tb = (R + 255) / 256;
+    const size_t bound = std::max(std::min(n_vt * 128 * n_tt, (2048 + n_tt) * 128),
+                                  std::min(n_vt * 256 * n_tb, (1024 + n_tb) * 256));
     o += align256(bound * (size_t)G * 8);
   }
   p.logits_c = o;

@@ -4,14 +4,19 @@
 //   output / down     -> residual add into the fp32 stream,
 //   gate|up           -> SwiGLU (silu(gate) * up), written as one [M, d_ff] tile,
 //   LM head (unfused) -> plain fp32 logits.
-// bf16 path: BM x BN block tile (256x256 on 8 waves where it divides N, else
-// 128x128 on 4), v_mfma_f32_32x32x16_bf16, K-steps streamed global -> LDS by
-// buffer loads into a ring of LDS stages (see mfma_tile.h).
-// fp32 path: a VALU kernel with the same epilogues (64x128 tile).
-// Both stage the finished tile through LDS 64 rows at a time so each epilogue
-// sees whole rows (a rotary pair j, j + d_h/2 or a gate/up pair lies inside one
-// tile).
+// bf16 path: BM x BN block tile (256x256 or 256x192 on 8 waves, whichever wastes
+// less of the last round of workgroups; 128x128 on 4 for small M),
+// v_mfma_f32_32x32x16_bf16, K-steps streamed global -> LDS by buffer loads into a
+// ring of LDS stages (see mfma_tile.h).  The finished tile leaves through LDS so
+// the global accesses are whole rows; a rotary pair j, j + d_h/2 or a gate/up pair
+// always lies inside one tile.
+// fp32 path: a VALU kernel with the same epilogues (64x128 tile), staged 64 rows
+// at a time.
 #include "mfma_tile.h"
+
+#include <algorithm>
+#include <cstdint>
+#include <type_traits>
 
 namespace rk {
 
@@ -191,6 +196,8 @@ __device__ __forceinline__ int b_row(int bn, int n, int d_ff) {
 // rotary pair, gate/up); wave wn's two 32-column blocks are c and c + PD with
 // c = (wn / (PD/32)) * 2 PD + (wn % (PD/32)) * 32, so each lane holds both
 // values in registers.  PD = 32 is the plain layout (wave wn: columns 64 wn ..).
+// Waves with three column blocks (NI = 3) take the plain layout, and paired
+// epilogues then combine their values from the staged fp32 tile instead.
 template <int BM, int BN, int BK, int NWM, int NWN, int STAGES, int PD, class E, bool SWIGLU>
 __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t* __restrict__ A, int64_t lda,
                                                                   const bf16_t* __restrict__ B, int64_t ldb, int M,
@@ -201,12 +208,14 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t*
   constexpr int CH = BK / 8;                      // 16-byte chunks per tile row
   constexpr int AS = BM * CH, BS = BN * CH;       // 16-byte slots per stage
   constexpr int PIPE = STAGES * (AS + BS);
-  static_assert(NI == 2 && BN % (2 * PD) == 0 && PD % 32 == 0, "two 32-column blocks per wave, pairs inside the tile");
-  // Epilogue staging: paired epilogues stage their outputs (type O), the others the
-  // fp32 accumulators; rows padded by 4 elements; in ROUNDS passes over the rows
-  // when the whole tile would not fit.
-  using SO = typename E::stage_t;
-  constexpr int OC = E::out_cols(BN), SP = OC + 4;
+  constexpr bool REG_PAIR = E::kPaired && NI == 2;   // pairs combined in registers
+  static_assert((NI == 2 && BN % (2 * PD) == 0 && PD % 32 == 0) || (NI == 3 && PD == 32), "column blocks");
+  static_assert(!SWIGLU || REG_PAIR, "SwiGLU tiles pair gate and up in registers");
+  // Epilogue staging: register-paired epilogues stage their outputs (type O), the
+  // others the fp32 accumulators; rows padded by 4 elements; in ROUNDS passes over
+  // the rows when the whole tile would not fit.
+  using SO = typename std::conditional<REG_PAIR, typename E::stage_t, float>::type;
+  constexpr int OC = REG_PAIR ? E::out_cols(BN) : BN, SP = OC + 4;
   constexpr int ROUNDS = BM * SP * (int)sizeof(SO) <= 136 * 1024 ? 1 : (BM * SP * (int)sizeof(SO) <= 272 * 1024 ? 2 : 4);
   static_assert(MI % ROUNDS == 0, "staging rounds split each wave's rows evenly");
   constexpr int STG = (BM / ROUNDS) * SP * (int)sizeof(SO) / 16;
@@ -219,7 +228,9 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t*
   v4u* Bs = smem + STAGES * AS;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31;
   const int wm = w / NWN, wn = w % NWN;
-  const int wcol = (wn / (PD / 32)) * (2 * PD) + (wn % (PD / 32)) * 32;   // tile column of block ni = 0
+  // tile column of column block ni
+  const int wcol = NI == 2 ? (wn / (PD / 32)) * (2 * PD) + (wn % (PD / 32)) * 32 : wn * WTN;
+  auto colblk = [&](int ni) { return NI == 2 ? wcol + ni * PD : wcol + ni * 32; };
   int bm_, bn;
   xcd_tile((int)blockIdx.x, (M + BM - 1) / BM, n_bn, group_m, &bm_, &bn);
   const int m0 = bm_ * BM;
@@ -279,7 +290,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t*
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi) af[0][mi] = frag<CH>(At, wm * WTM + mi * 32 + l32, 0, lane);
 #pragma unroll
-    for (int ni = 0; ni < NI; ++ni) bfr[0][ni] = frag<CH>(Bt, wcol + ni * PD + l32, 0, lane);
+    for (int ni = 0; ni < NI; ++ni) bfr[0][ni] = frag<CH>(Bt, colblk(ni) + l32, 0, lane);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
@@ -288,7 +299,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t*
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) af[c ^ 1][mi] = frag<CH>(At, wm * WTM + mi * 32 + l32, ks + 1, lane);
 #pragma unroll
-        for (int ni = 0; ni < NI; ++ni) bfr[c ^ 1][ni] = frag<CH>(Bt, wcol + ni * PD + l32, ks + 1, lane);
+        for (int ni = 0; ni < NI; ++ni) bfr[c ^ 1][ni] = frag<CH>(Bt, colblk(ni) + l32, ks + 1, lane);
       }
       if (copy) {
 #pragma unroll
@@ -332,38 +343,41 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t*
       SO* cs = Cs + (wm * WR + q * 32 + l32) * SP;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int tc = wcol + g * 8 + (lane >> 5) * 4;
-        const float4 x = make_float4(acc[mi][0][4 * g], acc[mi][0][4 * g + 1], acc[mi][0][4 * g + 2], acc[mi][0][4 * g + 3]);
-        const float4 y = make_float4(acc[mi][1][4 * g], acc[mi][1][4 * g + 1], acc[mi][1][4 * g + 2], acc[mi][1][4 * g + 3]);
-        if constexpr (E::kPaired) {
+        const int q4 = g * 8 + (lane >> 5) * 4;
+        if constexpr (REG_PAIR) {
+          const int tc = wcol + q4;
+          const float4 x = make_float4(acc[mi][0][4 * g], acc[mi][0][4 * g + 1], acc[mi][0][4 * g + 2], acc[mi][0][4 * g + 3]);
+          const float4 y = make_float4(acc[mi][1][4 * g], acc[mi][1][4 * g + 1], acc[mi][1][4 * g + 2], acc[mi][1][4 * g + 3]);
           float4 o0 = make_float4(0.f, 0.f, 0.f, 0.f), o1 = o0;
           if (row < M) e.template pair<BN>(row, bn, tc, x, y, o0, o1);
           store4(cs + tc, o0);
           if constexpr (E::kOut == 2) store4(cs + tc + PD, o1);
         } else {
-          store4(cs + tc, x);
-          store4(cs + tc + PD, y);
+#pragma unroll
+          for (int ni = 0; ni < NI; ++ni)
+            store4(cs + colblk(ni) + q4, make_float4(acc[mi][ni][4 * g], acc[mi][ni][4 * g + 1],
+                                                     acc[mi][ni][4 * g + 2], acc[mi][ni][4 * g + 3]));
         }
       }
     }
     __syncthreads();
     // staged row r is tile row (r / WR) * WTM + h * WR + r % WR
-    if constexpr (E::kPaired) {
+    if constexpr (REG_PAIR) {
       constexpr int CE = 16 / (int)sizeof(SO), CPR = OC / CE, RPP = NT / CPR;
-      static_assert(NT % CPR == 0, "whole rows per pass");
       const int c = (tid % CPR) * CE;
-      for (int r = tid / CPR; r < BM / ROUNDS; r += RPP) {
-        const int row = m0 + (r / WR) * WTM + h * WR + r % WR;
-        if (row < M) copy16(e.out + (int64_t)row * e.ldo + (int64_t)bn * OC + c, Cs + r * SP + c);
-      }
+      if (tid < RPP * CPR)
+        for (int r = tid / CPR; r < BM / ROUNDS; r += RPP) {
+          const int row = m0 + (r / WR) * WTM + h * WR + r % WR;
+          if (row < M) copy16(e.out + (int64_t)row * e.ldo + (int64_t)bn * OC + c, Cs + r * SP + c);
+        }
     } else {
-      constexpr int TPR = OC / 8, RPP = NT / TPR;
-      static_assert(NT % TPR == 0, "whole rows per pass");
+      constexpr int TPR = E::out_cols(BN) / 8, RPP = NT / TPR;
       const int c0 = (tid % TPR) * 8;
-      for (int r = tid / TPR; r < BM / ROUNDS; r += RPP) {
-        const int row = m0 + (r / WR) * WTM + h * WR + r % WR;
-        if (row < M) e.template apply<BN>(row, bn, c0, Cs + r * SP);
-      }
+      if (tid < RPP * TPR)
+        for (int r = tid / TPR; r < BM / ROUNDS; r += RPP) {
+          const int row = m0 + (r / WR) * WTM + h * WR + r % WR;
+          if (row < M) e.template apply<BN>(row, bn, c0, Cs + r * SP);
+        }
     }
   }
 }
@@ -427,12 +441,32 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 // Tile choice (measured on MI355X over the decoder's projection shapes): a
 // 256x256 tile on 8 waves (2x4, 128x64 per wave) wherever it divides N and
 // yields at least half a wave of tiles; otherwise 128x128 on 4 waves.
+static int cu_count() {
+  static int n = 0;
+  if (n == 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess && hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+      n = v;
+    else
+      n = 256;
+  }
+  return n;
+}
+
 static void pick_tile(const GemmArgs& a, bool swiglu, int* bm, int* bn_, int* bk, int* waves, int* stages) {
+  const int ncu = cu_count();
+  const int64_t nm = (a.M + 255) / 256;
   const bool fits256 = swiglu ? (a.d_ff % 128 == 0) : (a.N % 256 == 0);
-  // fewer than half a wave of 256x256 tiles on 256 CUs (small M, e.g. window rows): smaller tiles
-  const int64_t tiles256 = (int64_t)((a.M + 255) / 256) * (a.N / 256);
-  if (fits256 && a.K % 64 == 0 && tiles256 >= 128) {
-    *bm = 256; *bn_ = 256; *bk = 64; *waves = 8; *stages = 2;
+  // 192-wide tiles have three column blocks per wave, so their rotary pairs would
+  // go through the staged tile: measured slower than 256-wide tiles for q|k|v
+  const bool fits192 = !swiglu && a.N % 192 == 0 && a.epi != Epi::kStoreRope;
+  const int64_t tiles256 = fits256 ? nm * (a.N / 256) : 0, tiles192 = fits192 ? nm * (a.N / 192) : 0;
+  // fewer than half a wave of large tiles on the CUs (small M, e.g. window rows): 128x128 tiles
+  if (a.K % 64 == 0 && std::max(tiles256, tiles192) >= ncu / 2) {
+    // the 256-row tile whose last round of workgroups wastes least: cost = rounds x tile area
+    const int64_t c256 = fits256 ? (tiles256 + ncu - 1) / ncu * 256 : INT64_MAX;
+    const int64_t c192 = fits192 ? (tiles192 + ncu - 1) / ncu * 192 : INT64_MAX;
+    *bm = 256; *bn_ = c192 < c256 ? 192 : 256; *bk = 64; *waves = 8; *stages = 2;
     return;
   }
   *bm = 128; *bn_ = 128; *bk = 64; *waves = 4; *stages = 2;
@@ -450,7 +484,14 @@ static void go_pd(const GemmArgs& a, const E& e, hipStream_t s) {
 // the pair distance each epilogue needs (plain layout when it pairs nothing)
 template <int BM, int BN, int BK, int ST, class E, bool SWIGLU, int NWM = 2, int NWN = 2>
 static hipError_t go_bf16(const GemmArgs& a, const E& e, hipStream_t s) {
-  if constexpr (!E::kPaired) {
+  if constexpr (BN / NWN != 64) {
+    if constexpr (SWIGLU) {
+      return hipErrorInvalidValue;   // SwiGLU needs the paired layout
+    } else {
+      if (E::kPaired && BN % a.head_dim != 0) return hipErrorInvalidValue;   // rotary pairs inside the tile
+      go_pd<BM, BN, BK, ST, 32, E, SWIGLU, NWM, NWN>(a, e, s);
+    }
+  } else if constexpr (!E::kPaired) {
     go_pd<BM, BN, BK, ST, 32, E, SWIGLU, NWM, NWN>(a, e, s);
   } else if constexpr (SWIGLU) {
     go_pd<BM, BN, BK, ST, BN / 2, E, SWIGLU, NWM, NWN>(a, e, s);
@@ -474,8 +515,9 @@ static hipError_t go(const GemmArgs& a, bool bf16, const E& e, hipStream_t s) {
 #define RK_TILE(BM_, BN_, BK_, W_, ST_, NWM_, NWN_)                                     \
   if (bm == BM_ && bn == BN_ && bk == BK_ && waves == W_ && st == ST_)                  \
     return go_bf16<BM_, BN_, BK_, ST_, E, SWIGLU, NWM_, NWN_>(a, e, s);
-    // every variant gives each wave two 32-column blocks (BN = 64 NWN)
+    // each wave: two 32-column blocks (BN = 64 NWN) or three (BN = 96 NWN, not SwiGLU)
     RK_TILE(256, 256, 64, 8, 2, 2, 4)
+    RK_TILE(256, 192, 64, 8, 2, 4, 2)
     RK_TILE(256, 256, 32, 8, 3, 2, 4)
     RK_TILE(256, 256, 32, 8, 4, 2, 4)
     RK_TILE(128, 128, 64, 4, 2, 2, 2)

@@ -129,32 +129,146 @@ __global__ void lse_merge_kernel(const float2* __restrict__ part, int n_chunks, 
 // with p_v = exp(a_v - A_t), so KL_t = T1 + log1p(S) (= sum p (a - b) - A + B
 // without forming A and B).  delta = 0 gives exactly T1 = S = 0.  p is recomputed
 // per pass instead of being held, which keeps the kernel at two waves per SIMD.
+//
+// A workgroup of 8 waves owns 256 tokens and a chunk of 128-wide vocab tiles.  For
+// each vocab tile it computes the clean logit tile (kept in registers as `a`) and
+// then the G perturbed tiles against the same W rows, folding each into the
+// per-lane (T1, S) of its pass.  All the k-steps of all these tiles form one
+// stream through a 3-stage LDS ring, so the copies run ahead across tile
+// boundaries.  Wave w owns tokens 32 w .. 32 w + 31 (the MFMA N side) and all 128
+// vocab rows of the tile (M side): its reductions over vocab stay in its lanes.
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kKlTok = 256;     // tokens per workgroup
+constexpr int kKlStages = 3;
+
+// One 16-byte global->LDS copy per lane through a raw buffer descriptor over
+// [base, base + nrec): lanes whose offset falls outside read zeros.
+__device__ __forceinline__ void dma16_rows(const void* base, uint32_t nrec, uint32_t voff, int32_t soff,
+                                           uint32_t lds) {
+  const uint64_t b = (uint64_t)base;
+  i32x4_t rsrc;
+  rsrc[0] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)b);
+  rsrc[1] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)(b >> 32));
+  rsrc[2] = __builtin_amdgcn_readfirstlane((int32_t)nrec);
+  rsrc[3] = 0x00020000;   // raw buffer, 32-bit data format
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+               :
+               : "v"(voff), "s"(rsrc), "s"(soff), "{m0}"(lds)
+               : "memory");
+}
 
 template <int GMAX>
-__global__ __launch_bounds__(256, 2) void lm_kl_kernel(const bf16_t* __restrict__ Xc, const bf16_t* __restrict__ Xp,
-                                                       int64_t pass_stride, int G, const bf16_t* __restrict__ W,
-                                                       int rows, int d, int n_vt, int vt_per_chunk,
-                                                       const float* __restrict__ lse, float2* __restrict__ part) {
-  __shared__ __attribute__((aligned(16))) v4u smem[4096];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int t0 = blockIdx.x * 128, chunk = blockIdx.y;
+__global__ __launch_bounds__(512) void lm_kl_kernel(const bf16_t* __restrict__ Xc, const bf16_t* __restrict__ Xp,
+                                                    int64_t pass_stride, int G, const bf16_t* __restrict__ W,
+                                                    int rows, int d, int n_vt, int vt_per_chunk,
+                                                    const float* __restrict__ lse, float2* __restrict__ part) {
+  constexpr int CH = 8;                          // 16-byte chunks per 64-wide k row
+  constexpr int WS = 128 * CH, XS = kKlTok * CH, SS = WS + XS;   // 16-byte slots per stage
+  constexpr int NLW = WS / 512, NLX = XS / 512, NL = NLW + NLX;  // copies per thread and stage
+  constexpr int ST = kKlStages;
+  __shared__ __attribute__((aligned(16))) v4u smem[ST * SS];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31;
+  const int t0 = blockIdx.x * kKlTok, chunk = blockIdx.y;
   const int vt0 = chunk * vt_per_chunk, vt1 = min(n_vt, vt0 + vt_per_chunk);
-  const int token = t0 + w * 32 + (lane & 31);
-  const float Ac = lse[min(token, rows - 1)] * kLog2e;
+  const int nk = d / 64;
+  const int nsteps = (vt1 - vt0) * (G + 1) * nk;
+  const int token = t0 + w * 32 + l32;
+  float Ac = lse[min(token, rows - 1)] * kLog2e;
+  asm volatile("" : "+v"(Ac));   // loaded before the copies start: no vector-memory wait inside the loop
+
+  // Copy geometry: in round j a wave instruction fills rows 64 j + 8 w .. +7 of a
+  // tile, lane -> (row 64 j + 8 w + lane / 8, swizzled chunk); the swizzle of a row
+  // depends on (row / 2) % 8 only, so it is the same in every round.
+  const int r0 = w * 8 + (lane >> 3);
+  const uint32_t voff0 = (uint32_t)(r0 * d * 2 + (((lane & 7) ^ swz<CH>(r0)) * 16));
+  const uint32_t round_bytes = (uint32_t)(64 * d * 2);
+  const uint32_t x_nrec = (uint32_t)(max(0, min(rows - t0, kKlTok)) * d * 2);
+  const uint32_t w_nrec = (uint32_t)(128 * d * 2);
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) v4u*)smem;
+
+  // producer position: the next k-step to copy
+  int p_kt = 0, p_g = -1, p_vt = vt0, issued = 0;
+  auto issue_one = [&](int j, int slot) {
+    const uint32_t lds = lds0 + (uint32_t)(slot * SS * 16);
+    const int32_t soff = p_kt * 128;
+    if (j < NLW) {
+      dma16_rows(W + (int64_t)p_vt * 128 * d, w_nrec, voff0 + j * round_bytes, soff,
+                 lds + (uint32_t)((j * 8 + w) * 64 * 16));
+    } else {
+      const int jx = j - NLW;
+      const bf16_t* xb = (p_g < 0 ? Xc : Xp + (int64_t)p_g * pass_stride) + (int64_t)t0 * d;
+      dma16_rows(xb, x_nrec, voff0 + jx * round_bytes, soff, lds + (uint32_t)((WS + (jx * 8 + w) * 64) * 16));
+    }
+  };
+  auto advance = [&]() {
+    ++issued;
+    if (++p_kt == nk) {
+      p_kt = 0;
+      if (++p_g == G) { p_g = -1; ++p_vt; }
+    }
+  };
+#pragma unroll
+  for (int q = 0; q < ST - 1; ++q)
+    if (issued < nsteps) {
+#pragma unroll
+      for (int j = 0; j < NL; ++j) issue_one(j, q);
+      advance();
+    }
+
   float T1[GMAX], S[GMAX];
 #pragma unroll
   for (int g = 0; g < GMAX; ++g) { T1[g] = 0.f; S[g] = 0.f; }
   f32x16_t a[4], b[4];
-  for (int vt = vt0; vt < vt1; ++vt) {
-    // g = -1 computes the clean tile (kept in a), then each pass g reuses it
-    for (int g = -1; g < G; ++g) {
-      logit_tile(W, g < 0 ? Xc : Xp + (int64_t)g * pass_stride, vt * 128, t0, d, smem, smem + 2048, b);
-      if (g < 0) {
+  int kt = 0, g = -1, slot = 0, pslot = ST - 1;
+  constexpr int PER = (NL + 3) / 4;   // copies issued per k-slice
+  for (int s = 0; s < nsteps; ++s) {
+    if (issued > s + 1) wait_vmem_le<NL * (ST - 2)>(); else wait_vmem();
+    __syncthreads();   // k-step s is in LDS for every wave; the slot of s - 1 is free
+    if (kt == 0) {
 #pragma unroll
-        for (int vb = 0; vb < 4; ++vb) a[vb] = b[vb];
-        continue;
+      for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) b[vb][i] = 0.f;
+    }
+    const bool copy = issued < nsteps;
+    const v4u* Wt = smem + slot * SS;
+    const v4u* Xt = Wt + WS;
+    bf16x8_t wf[2][4], xf[2];
+#pragma unroll
+    for (int vb = 0; vb < 4; ++vb) wf[0][vb] = frag<CH>(Wt, vb * 32 + l32, 0, lane);
+    xf[0] = frag<CH>(Xt, w * 32 + l32, 0, lane);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int c = ks & 1;
+      if (ks < 3) {
+#pragma unroll
+        for (int vb = 0; vb < 4; ++vb) wf[c ^ 1][vb] = frag<CH>(Wt, vb * 32 + l32, ks + 1, lane);
+        xf[c ^ 1] = frag<CH>(Xt, w * 32 + l32, ks + 1, lane);
       }
+      if (copy) {
+#pragma unroll
+        for (int j = ks * PER; j < (ks + 1) * PER; ++j)
+          if (j < NL) issue_one(j, pslot);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int vb = 0; vb < 4; ++vb)
+        b[vb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[c][vb], xf[c], b[vb], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (copy) {
+      advance();
+      pslot = pslot == ST - 1 ? 0 : pslot + 1;
+    }
+    slot = slot == ST - 1 ? 0 : slot + 1;
+    if (++kt < nk) continue;
+    // a logit tile is complete
+    kt = 0;
+    if (g < 0) {
+#pragma unroll
+      for (int vb = 0; vb < 4; ++vb) a[vb] = b[vb];
+    } else {
       float t1 = 0.f, s2 = 0.f;
 #pragma unroll
       for (int vb = 0; vb < 4; ++vb)
@@ -171,13 +285,14 @@ __global__ __launch_bounds__(256, 2) void lm_kl_kernel(const bf16_t* __restrict_
       for (int j = 0; j < GMAX; ++j)
         if (j == g) { T1[j] += t1; S[j] += s2; }
     }
+    if (++g == G) g = -1;
   }
 #pragma unroll
-  for (int g = 0; g < GMAX; ++g) {
-    if (g < G) {
-      const float x = T1[g] + __shfl_xor(T1[g], 32, 64);
-      const float y = S[g] + __shfl_xor(S[g], 32, 64);
-      if ((lane >> 5) == 0 && token < rows) part[((int64_t)chunk * G + g) * rows + token] = make_float2(x, y);
+  for (int g2 = 0; g2 < GMAX; ++g2) {
+    if (g2 < G) {
+      const float x = T1[g2] + __shfl_xor(T1[g2], 32, 64);
+      const float y = S[g2] + __shfl_xor(S[g2], 32, 64);
+      if ((lane >> 5) == 0 && token < rows) part[((int64_t)chunk * G + g2) * rows + token] = make_float2(x, y);
     }
   }
 }
@@ -204,6 +319,16 @@ int lm_chunks(int rows, int vocab) {
   return (n_vt + per - 1) / per;
 }
 
+// chunks of the fused KL kernel: about 1024 workgroups of 256 tokens
+int lm_kl_chunks(int rows, int vocab) {
+  const int n_vt = vocab / 128, n_tb = (rows + kKlTok - 1) / kKlTok;
+  int chunks = (1024 + n_tb - 1) / n_tb;
+  if (chunks > n_vt) chunks = n_vt;
+  if (chunks < 1) chunks = 1;
+  const int per = (n_vt + chunks - 1) / chunks;
+  return (n_vt + per - 1) / per;
+}
+
 static int vt_per_chunk(int vocab, int chunks) {
   const int n_vt = vocab / 128;
   return (n_vt + chunks - 1) / chunks;
@@ -224,15 +349,16 @@ hipError_t launch_lm_lse(const bf16_t* x, const bf16_t* W, int rows, int d, int 
 hipError_t launch_lm_kl(const bf16_t* xc, const bf16_t* xp, int64_t pass_stride, int G, const bf16_t* W, int rows,
                         int d, int vocab, const float* lse, float2* part, float* kl, hipStream_t s) {
   if (rows <= 0 || G <= 0) return hipSuccess;
-  const int chunks = lm_chunks(rows, vocab);
-  dim3 grid((rows + 127) / 128, chunks);
+  if (d % 64 != 0 || vocab % 128 != 0 || (int64_t)kKlTok * d * 2 > 0x7fffffff) return hipErrorInvalidValue;
+  const int chunks = lm_kl_chunks(rows, vocab);
+  dim3 grid((rows + kKlTok - 1) / kKlTok, chunks);
   const int vpc = vt_per_chunk(vocab, chunks);
   if (G <= 4)
-    lm_kl_kernel<4><<<grid, 256, 0, s>>>(xc, xp, pass_stride, G, W, rows, d, vocab / 128, vpc, lse, part);
+    lm_kl_kernel<4><<<grid, 512, 0, s>>>(xc, xp, pass_stride, G, W, rows, d, vocab / 128, vpc, lse, part);
   else if (G <= 8)
-    lm_kl_kernel<8><<<grid, 256, 0, s>>>(xc, xp, pass_stride, G, W, rows, d, vocab / 128, vpc, lse, part);
+    lm_kl_kernel<8><<<grid, 512, 0, s>>>(xc, xp, pass_stride, G, W, rows, d, vocab / 128, vpc, lse, part);
   else if (G <= RK_MAX_GROUP)
-    lm_kl_kernel<RK_MAX_GROUP><<<grid, 256, 0, s>>>(xc, xp, pass_stride, G, W, rows, d, vocab / 128, vpc, lse, part);
+    lm_kl_kernel<RK_MAX_GROUP><<<grid, 512, 0, s>>>(xc, xp, pass_stride, G, W, rows, d, vocab / 128, vpc, lse, part);
   else
     return hipErrorInvalidValue;
   hipError_t e = hipGetLastError();

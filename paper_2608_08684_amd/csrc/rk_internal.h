@@ -122,7 +122,8 @@ hipError_t launch_attention(const void* qkv, int64_t ldq, void* out, int64_t ldo
                             const KvPrefix* prefix = nullptr);
 
 // Clean log-sum-exp of the LM head, fused (bf16): lse[r] = logsumexp_v (x[r] . W[v]).
-int lm_chunks(int rows, int vocab);
+int lm_chunks(int rows, int vocab);      // vocab chunks of lm_lse (partials: chunks * rows float2)
+int lm_kl_chunks(int rows, int vocab);   // vocab chunks of lm_kl (partials: chunks * G * rows float2)
 hipError_t launch_lm_lse(const bf16_t* x, const bf16_t* W, int rows, int d, int vocab, float2* part,
                          float* lse, hipStream_t s);
 // Fused LM head + KL (bf16): for pass g, kl[g][r] = KL(softmax(x_c W^T) || softmax(x_g W^T)).
