@@ -139,7 +139,6 @@ __global__ void lse_merge_kernel(const float2* __restrict__ part, int n_chunks, 
 // vocab rows of the tile (M side): its reductions over vocab stay in its lanes.
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kKlTok = 256;     // tokens per workgroup
-constexpr int kKlStages = 3;
 
 // One 16-byte global->LDS copy per lane through a raw buffer descriptor over
 // [base, base + nrec): lanes whose offset falls outside read zeros.
@@ -157,31 +156,50 @@ __device__ __forceinline__ void dma16_rows(const void* base, uint32_t nrec, uint
                : "memory");
 }
 
-template <int GMAX>
+// Wait until at most `ahead` k-steps of NL copies each (those issued after the
+// one about to be consumed) are still in flight; ahead <= K.
+template <int NL, int K>
+__device__ __forceinline__ void wait_steps_ahead(int ahead) {
+  if constexpr (K <= 0) {
+    wait_vmem();
+  } else {
+    if (ahead >= K) wait_vmem_le<NL * K>();
+    else wait_steps_ahead<NL, K - 1>(ahead);
+  }
+}
+
+template <int GMAX, int BK, int ST>
 __global__ __launch_bounds__(512) void lm_kl_kernel(const bf16_t* __restrict__ Xc, const bf16_t* __restrict__ Xp,
                                                     int64_t pass_stride, int G, const bf16_t* __restrict__ W,
-                                                    int rows, int d, int n_vt, int vt_per_chunk,
+                                                    int rows, int d, int n_vt, int n_chunks,
                                                     const float* __restrict__ lse, float2* __restrict__ part) {
-  constexpr int CH = 8;                          // 16-byte chunks per 64-wide k row
+  constexpr int CH = BK / 8;                     // 16-byte chunks per k row of a stage
+  constexpr int RPI = 64 / CH;                   // rows per wave copy instruction
   constexpr int WS = 128 * CH, XS = kKlTok * CH, SS = WS + XS;   // 16-byte slots per stage
   constexpr int NLW = WS / 512, NLX = XS / 512, NL = NLW + NLX;  // copies per thread and stage
-  constexpr int ST = kKlStages;
+  constexpr int NKS = BK / 16;                   // k-slices per k-step
+  static_assert(WS % 512 == 0 && (ST - 2) * NL < 16 && ST * SS * 16 <= 160 * 1024, "stage geometry");
   __shared__ __attribute__((aligned(16))) v4u smem[ST * SS];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31;
-  const int t0 = blockIdx.x * kKlTok, chunk = blockIdx.y;
-  const int vt0 = chunk * vt_per_chunk, vt1 = min(n_vt, vt0 + vt_per_chunk);
-  const int nk = d / 64;
+  // Workgroup -> (token block, vocab chunk): the 32 workgroups an XCD runs at once
+  // cover 4 token blocks x 8 chunks, so one pass's X rows (4 x 384 KB at d = 768)
+  // and the W tiles in use (8 x 192 KB) stay in that XCD's L2 through the passes.
+  int tb, chunk;
+  xcd_tile((int)blockIdx.x, (rows + kKlTok - 1) / kKlTok, n_chunks, 4, &tb, &chunk);
+  const int t0 = tb * kKlTok;
+  const int vt0 = (int)((int64_t)chunk * n_vt / n_chunks), vt1 = (int)((int64_t)(chunk + 1) * n_vt / n_chunks);
+  const int nk = d / BK;
   const int nsteps = (vt1 - vt0) * (G + 1) * nk;
   const int token = t0 + w * 32 + l32;
   float Ac = lse[min(token, rows - 1)] * kLog2e;
   asm volatile("" : "+v"(Ac));   // loaded before the copies start: no vector-memory wait inside the loop
 
-  // Copy geometry: in round j a wave instruction fills rows 64 j + 8 w .. +7 of a
-  // tile, lane -> (row 64 j + 8 w + lane / 8, swizzled chunk); the swizzle of a row
-  // depends on (row / 2) % 8 only, so it is the same in every round.
-  const int r0 = w * 8 + (lane >> 3);
-  const uint32_t voff0 = (uint32_t)(r0 * d * 2 + (((lane & 7) ^ swz<CH>(r0)) * 16));
-  const uint32_t round_bytes = (uint32_t)(64 * d * 2);
+  // Copy geometry: in round j a wave instruction fills rows 8 RPI j + RPI w ..
+  // + RPI - 1 of a tile, lane -> (row 8 RPI j + RPI w + lane / CH, swizzled chunk);
+  // rounds advance by a multiple of 16 rows, which leaves the row swizzle unchanged.
+  const int r0 = w * RPI + lane / CH;
+  const uint32_t voff0 = (uint32_t)(r0 * d * 2 + (((lane % CH) ^ swz<CH>(r0)) * 16));
+  const uint32_t round_bytes = (uint32_t)(8 * RPI * d * 2);
   const uint32_t x_nrec = (uint32_t)(max(0, min(rows - t0, kKlTok)) * d * 2);
   const uint32_t w_nrec = (uint32_t)(128 * d * 2);
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) v4u*)smem;
@@ -190,7 +208,7 @@ __global__ __launch_bounds__(512) void lm_kl_kernel(const bf16_t* __restrict__ X
   int p_kt = 0, p_g = -1, p_vt = vt0, issued = 0;
   auto issue_one = [&](int j, int slot) {
     const uint32_t lds = lds0 + (uint32_t)(slot * SS * 16);
-    const int32_t soff = p_kt * 128;
+    const int32_t soff = p_kt * BK * 2;
     if (j < NLW) {
       dma16_rows(W + (int64_t)p_vt * 128 * d, w_nrec, voff0 + j * round_bytes, soff,
                  lds + (uint32_t)((j * 8 + w) * 64 * 16));
@@ -220,9 +238,9 @@ __global__ __launch_bounds__(512) void lm_kl_kernel(const bf16_t* __restrict__ X
   for (int g = 0; g < GMAX; ++g) { T1[g] = 0.f; S[g] = 0.f; }
   f32x16_t a[4], b[4];
   int kt = 0, g = -1, slot = 0, pslot = ST - 1;
-  constexpr int PER = (NL + 3) / 4;   // copies issued per k-slice
+  constexpr int PER = (NL + NKS - 1) / NKS;   // copies issued per k-slice
   for (int s = 0; s < nsteps; ++s) {
-    if (issued > s + 1) wait_vmem_le<NL * (ST - 2)>(); else wait_vmem();
+    wait_steps_ahead<NL, ST - 2>(issued - 1 - s);
     __syncthreads();   // k-step s is in LDS for every wave; the slot of s - 1 is free
     if (kt == 0) {
 #pragma unroll
@@ -239,9 +257,9 @@ __global__ __launch_bounds__(512) void lm_kl_kernel(const bf16_t* __restrict__ X
     xf[0] = frag<CH>(Xt, w * 32 + l32, 0, lane);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int ks = 0; ks < NKS; ++ks) {
       const int c = ks & 1;
-      if (ks < 3) {
+      if (ks + 1 < NKS) {
 #pragma unroll
         for (int vb = 0; vb < 4; ++vb) wf[c ^ 1][vb] = frag<CH>(Wt, vb * 32 + l32, ks + 1, lane);
         xf[c ^ 1] = frag<CH>(Xt, w * 32 + l32, ks + 1, lane);
@@ -319,14 +337,12 @@ int lm_chunks(int rows, int vocab) {
   return (n_vt + per - 1) / per;
 }
 
-// chunks of the fused KL kernel: about 1024 workgroups of 256 tokens
+// chunks of the fused KL kernel: about 1024 workgroups of 256 tokens; chunk c
+// takes vocab tiles [c n_vt / chunks, (c + 1) n_vt / chunks)
 int lm_kl_chunks(int rows, int vocab) {
   const int n_vt = vocab / 128, n_tb = (rows + kKlTok - 1) / kKlTok;
-  int chunks = (1024 + n_tb - 1) / n_tb;
-  if (chunks > n_vt) chunks = n_vt;
-  if (chunks < 1) chunks = 1;
-  const int per = (n_vt + chunks - 1) / chunks;
-  return (n_vt + per - 1) / per;
+  const int chunks = (1024 + n_tb - 1) / n_tb;
+  return chunks > n_vt ? n_vt : (chunks < 1 ? 1 : chunks);
 }
 
 static int vt_per_chunk(int vocab, int chunks) {
@@ -351,14 +367,20 @@ hipError_t launch_lm_kl(const bf16_t* xc, const bf16_t* xp, int64_t pass_stride,
   if (rows <= 0 || G <= 0) return hipSuccess;
   if (d % 64 != 0 || vocab % 128 != 0 || (int64_t)kKlTok * d * 2 > 0x7fffffff) return hipErrorInvalidValue;
   const int chunks = lm_kl_chunks(rows, vocab);
-  dim3 grid((rows + kKlTok - 1) / kKlTok, chunks);
-  const int vpc = vt_per_chunk(vocab, chunks);
+  const int grid = (rows + kKlTok - 1) / kKlTok * chunks;
+#ifndef RK_KL_BK
+#define RK_KL_BK 64
+#define RK_KL_ST 3
+#endif
+  constexpr int BK = RK_KL_BK, ST = RK_KL_ST;
+  if (d % BK != 0) return hipErrorInvalidValue;
   if (G <= 4)
-    lm_kl_kernel<4><<<grid, 512, 0, s>>>(xc, xp, pass_stride, G, W, rows, d, vocab / 128, vpc, lse, part);
+    lm_kl_kernel<4, BK, ST><<<grid, 512, 0, s>>>(xc, xp, pass_stride, G, W, rows, d, vocab / 128, chunks, lse, part);
   else if (G <= 8)
-    lm_kl_kernel<8><<<grid, 512, 0, s>>>(xc, xp, pass_stride, G, W, rows, d, vocab / 128, vpc, lse, part);
+    lm_kl_kernel<8, BK, ST><<<grid, 512, 0, s>>>(xc, xp, pass_stride, G, W, rows, d, vocab / 128, chunks, lse, part);
   else if (G <= RK_MAX_GROUP)
-    lm_kl_kernel<RK_MAX_GROUP><<<grid, 512, 0, s>>>(xc, xp, pass_stride, G, W, rows, d, vocab / 128, vpc, lse, part);
+    lm_kl_kernel<RK_MAX_GROUP, BK, ST><<<grid, 512, 0, s>>>(xc, xp, pass_stride, G, W, rows, d, vocab / 128, chunks, lse,
+                                                             part);
   else
     return hipErrorInvalidValue;
   hipError_t e = hipGetLastError();
