@@ -119,12 +119,13 @@ def cached_attention(q: np.ndarray, k_prefix: np.ndarray, v_prefix: np.ndarray, 
 
 def block(m: Model, l: int, h: np.ndarray, positions: np.ndarray,
           v_hook: Optional[Callable[[np.ndarray], np.ndarray]] = None, kv_out: Optional[list] = None,
-          prefix_kv: Optional[tuple] = None) -> np.ndarray:
+          prefix_kv: Optional[tuple] = None, q_out: Optional[list] = None) -> np.ndarray:
     """One decoder block.  ``v_hook`` (if given) replaces the layer's Value states
     [T, H_kv, d_h] before attention; Q and K are untouched.  ``kv_out`` (a list)
-    receives the block's rotated Keys and its Values.  ``prefix_kv`` = (K, V) of
-    cached earlier positions makes the rows of h new positions attending to that
-    cache as well (``cached_attention``); the hook does not touch the cache."""
+    receives the block's rotated Keys and its Values, ``q_out`` its rotated
+    Queries [T, H, d_h].  ``prefix_kv`` = (K, V) of cached earlier positions makes
+    the rows of h new positions attending to that cache as well
+    (``cached_attention``); the hook does not touch the cache."""
     c = m.cfg
     H, Hkv, dh = c.n_heads, c.n_kv_heads, c.head_dim
     T = h.shape[0]
@@ -139,6 +140,8 @@ def block(m: Model, l: int, h: np.ndarray, positions: np.ndarray,
         v = v_hook(v)
     if kv_out is not None:
         kv_out.append((k, v))
+    if q_out is not None:
+        q_out.append(q)
     if prefix_kv is None:
         o = causal_attention(q, k, v)
     else:
