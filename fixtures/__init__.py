@@ -260,3 +260,43 @@ def make_workload(name: str, model: ModelConfig, lengths: Sequence[int], alphas=
     lengths = tuple(int(x) for x in lengths)
     return Workload(name, seed_id, model, CalibConfig(len(lengths), 0, None, 1.1, lengths),
                     tuple(alphas), tuple(ratios))
+
+
+# ----------------------------------------------------------------------------- cache states
+
+def make_kv_state(n_layers: int, lengths: Sequence[int], n_heads: int, n_kv_heads: int, head_dim: int,
+                  obs_window: int, seed_id: int = 0, score_std: float = 2.5):
+    """Synthetic prompt caches for the SnapKV selection, as bf16 bit patterns.
+
+    kv [L, R, 2 * H_kv * d_h]: per row the Keys of every KV head then its Values,
+    N(0, 1) each; a few positions per sequence and head get Keys aligned with the
+    head's mean query direction ("heavy hitters"), so the votes have structure.
+    q [L, n * w, H * d_h]: the observation queries of each sequence (its last w
+    rows), drawn so that query . key has standard deviation ``score_std`` in log2
+    units.  Rows are sequences concatenated (R = sum of lengths).  Drawn from
+    ``default_rng([3, seed_id, l])`` per layer."""
+    R, n = int(sum(lengths)), len(lengths)
+    kvc = 2 * n_kv_heads * head_dim
+    kv = np.empty((n_layers, R, kvc), dtype=np.uint16)
+    q = np.empty((n_layers, n * obs_window, n_heads * head_dim), dtype=np.uint16)
+    offs = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
+    group = n_heads // n_kv_heads
+    for l in range(n_layers):
+        rng = np.random.default_rng([3, seed_id, l])
+        k = rng.standard_normal((R, n_kv_heads, head_dim)).astype(np.float32)
+        v = rng.standard_normal((R, n_kv_heads, head_dim)).astype(np.float32)
+        dirs = rng.standard_normal((n_kv_heads, head_dim)).astype(np.float32)
+        dirs /= np.linalg.norm(dirs, axis=-1, keepdims=True)
+        qq = np.empty((n * obs_window, n_heads, head_dim), dtype=np.float32)
+        for i in range(n):
+            T = int(lengths[i])
+            for g in range(n_kv_heads):
+                hot = rng.choice(max(1, T - obs_window), size=min(8, max(1, T - obs_window)), replace=False)
+                k[offs[i] + hot, g, :] += 3.0 * dirs[g]
+            noise = rng.standard_normal((obs_window, n_heads, head_dim)).astype(np.float32)
+            for h in range(n_heads):
+                noise[:, h, :] += 1.5 * dirs[h // group]
+            qq[i * obs_window:(i + 1) * obs_window] = noise * (score_std / np.sqrt(head_dim))
+        kv[l] = bf16_bits(np.concatenate([k.reshape(R, -1), v.reshape(R, -1)], axis=1))
+        q[l] = bf16_bits(qq.reshape(n * obs_window, -1))
+    return kv, q

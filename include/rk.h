@@ -264,12 +264,79 @@ rk_status rk_perturb_values(const rk_model *m, const rk_batch *batch, int32_t la
 rk_status rk_layer_budgets(const double *s, int32_t n, int64_t B, double r, double gamma, double eps,
                            rk_rounding mode, double *w_out, int64_t *b_out);
 
+/* ---------------------------------------------------------------- budgets' consumer: SnapKV */
+
+/* Section 4.4: the budgets b_l replace the uniform per-layer budget of the base
+ * compressor, whose own token scoring and selection are kept; layer l then keeps
+ * b_l positions (the compressed cache of Section 3).  The base method is SnapKV;
+ * the paper gives none of its constants, so they are parameters:
+ *   obs_window w (1..64): the last w positions of each prompt; their queries vote
+ *     and they are always kept;
+ *   vote of KV head g for a prefix position u < T - w: the causal softmax weight
+ *     the w observation queries put on key u, summed over the queries and over
+ *     the query heads sharing g;
+ *   pooling along positions, odd kernel (1..31): RK_POOL_MAX = maximum within
+ *     kernel/2 positions, RK_POOL_AVG = their sum / kernel (zeros outside);
+ *   retained: the window and the b - w prefix positions of highest pooled vote
+ *     (ties to the lower position); b >= T keeps all, b <= w the last b.
+ * bf16 models only; (n_heads / n_kv_heads) * ceil(w / 32) <= 8.                  */
+typedef enum { RK_POOL_MAX = 0, RK_POOL_AVG = 1 } rk_pooling;
+typedef struct {
+  int32_t obs_window;
+  int32_t pool_kernel;
+  rk_pooling pooling;
+} rk_snapkv_params;
+
+/* Longest prefix (T - w) a sequence may have for rk_snapkv_compress. */
+#define RK_SNAPKV_MAX_PREFIX 36864
+
+/* Bytes of the prefill state of a batch of n_rows rows and n_seqs sequences:
+ *   kv: [L, n_rows, 2 * n_kv_heads * head_dim] bf16, per row the rotated Keys of
+ *       every KV head, then its Values (the prompt's KV cache, Section 3);
+ *   q:  [L, n_seqs * w, n_heads * head_dim] bf16, the rotated queries of each
+ *       sequence's last w positions multiplied by log2(e) / sqrt(head_dim),
+ *   kv first, q at the next multiple of 256 bytes.                               */
+size_t rk_snapkv_state_size(const rk_model *m, int64_t n_rows, int32_t n_seqs, int32_t obs_window);
+
+/* Workspace bytes of rk_snapkv_prefill and rk_snapkv_compress for such a batch. */
+size_t rk_snapkv_workspace_size(const rk_model *m, int64_t n_rows, int32_t n_seqs, int32_t obs_window);
+
+/* The prompts' forward pass through every layer, keeping the KV cache and the
+ * observation queries in `state` (layout above).  Every sequence must be longer
+ * than obs_window.                                                               */
+rk_status rk_snapkv_prefill(const rk_model *m, const rk_batch *batch, int32_t obs_window, void *state,
+                            size_t state_bytes, void *workspace, size_t ws_bytes, void *stream);
+
+/* Compressed-cache layout (host, synchronous).  budgets: HOST int64
+ * [n_seqs * n_layers], b_{i,l} at i * n_layers + l.  n_keep(i, l) = min(max(b, 0),
+ * T_i); offsets_out (HOST int64 [n_seqs * n_layers + 1], may be NULL) receives the
+ * exclusive prefix sums of n_keep in that order.  Returns the total, or -1 on a
+ * bad argument.  Block (i, l, g) of the outputs of rk_snapkv_compress holds
+ * n_keep(i, l) entries starting at entry offsets[i * L + l] * n_kv_heads +
+ * g * n_keep(i, l).                                                              */
+int64_t rk_snapkv_layout(const rk_batch *batch, int32_t n_layers, const int64_t *budgets, int64_t *offsets_out);
+
+/* SnapKV selection with the per-layer budgets, every (sequence, layer, KV head),
+ * from a prefill state of the same batch.
+ *   positions: DEVICE int32 [n_kv_heads * total]: retained positions (within
+ *     the sequence), increasing, per block;
+ *   k_out, v_out: DEVICE bf16 [n_kv_heads * total, head_dim]: their rotated Keys
+ *     and Values;
+ *   scores: DEVICE fp32 [n_layers, n_kv_heads, sum_i (T_i - w)] pooled votes,
+ *     sequence by sequence, or NULL.
+ * Requires obs_window < T_i and T_i - obs_window <= RK_SNAPKV_MAX_PREFIX.        */
+rk_status rk_snapkv_compress(const rk_model *m, const rk_batch *batch, const rk_snapkv_params *p,
+                             const int64_t *budgets, const void *state, size_t state_bytes, int32_t *positions,
+                             void *k_out, void *v_out, float *scores, void *workspace, size_t ws_bytes,
+                             void *stream);
+
 /* ---------------------------------------------------------------- diagnostics */
 
 /* Per-kernel timing for measurement: after rk_timing_begin(family) every launch
  * of that kernel family is bracketed by HIP events recorded on its launch stream
  * (families: "rmsnorm", "gemm_qkv", "noise", "attention", "gemm_o",
- * "gemm_gate_up", "gemm_down", "lm_lse", "lm_kl", "kl_logits", "lm_logits").
+ * "gemm_gate_up", "gemm_down", "lm_lse", "lm_kl", "kl_logits", "lm_logits",
+ * "snap_scores", "snap_select").
  * rk_timing_end waits for the recorded events, returns the number of launches
  * and their summed duration in milliseconds, and stops recording.  Host-side
  * state is process-wide; not for concurrent use from several threads.          */

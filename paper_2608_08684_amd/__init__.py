@@ -26,7 +26,8 @@ from typing import Optional, Sequence
 import numpy as np
 
 __all__ = ["RKError", "load", "Model", "Batch", "layer_budgets", "timing_begin", "timing_end", "LIB_PATH", "RK_FLAG_FULL_RECOMPUTE",
-           "RK_FLAG_UNFUSED_KL", "RK_FLAG_CACHED_WINDOW", "RK_FLAG_GRAPH", "RK_WS_CLEAN_STATE", "RK_MAX_BATCH_SEQS", "RK_MAX_GROUP"]
+           "RK_FLAG_UNFUSED_KL", "RK_FLAG_CACHED_WINDOW", "RK_FLAG_GRAPH", "RK_WS_CLEAN_STATE", "RK_MAX_BATCH_SEQS", "RK_MAX_GROUP",
+           "RK_POOL_MAX", "RK_POOL_AVG", "RK_SNAPKV_MAX_PREFIX", "snapkv_layout"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librk.so")
 
@@ -40,6 +41,9 @@ RK_FLAG_GRAPH = 0x8
 RK_WS_CLEAN_STATE = 0x100
 RK_MAX_BATCH_SEQS = 64
 RK_MAX_GROUP = 16
+RK_POOL_MAX = 0
+RK_POOL_AVG = 1
+RK_SNAPKV_MAX_PREFIX = 36864
 
 _STATUS = {0: "RK_OK", -1: "RK_ERR_ARG", -2: "RK_ERR_SHAPE", -3: "RK_ERR_WORKSPACE", -4: "RK_ERR_HIP",
            -5: "RK_ERR_UNSUPPORTED"}
@@ -77,6 +81,10 @@ class _Params(ctypes.Structure):
                 ("protect_tail", ctypes.c_int32), ("flags", ctypes.c_uint32)]
 
 
+class _SnapParams(ctypes.Structure):
+    _fields_ = [("obs_window", ctypes.c_int32), ("pool_kernel", ctypes.c_int32), ("pooling", ctypes.c_int)]
+
+
 _lib = None
 
 
@@ -109,6 +117,12 @@ def load() -> ctypes.CDLL:
         "rk_last_error": (ctypes.c_char_p, []),
         "rk_timing_begin": (st, [ctypes.c_char_p]),
         "rk_timing_end": (st, [ctypes.POINTER(i64), ctypes.POINTER(f64)]),
+        "rk_snapkv_state_size": (sz, [vp, i64, i32, i32]),
+        "rk_snapkv_workspace_size": (sz, [vp, i64, i32, i32]),
+        "rk_snapkv_prefill": (st, [vp, ctypes.POINTER(_Batch), i32, vp, sz, vp, sz, vp]),
+        "rk_snapkv_layout": (i64, [ctypes.POINTER(_Batch), i32, ctypes.POINTER(i64), ctypes.POINTER(i64)]),
+        "rk_snapkv_compress": (st, [vp, ctypes.POINTER(_Batch), ctypes.POINTER(_SnapParams), ctypes.POINTER(i64), vp,
+                                    sz, vp, vp, vp, vp, vp, sz, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -238,11 +252,46 @@ class Model:
                                              _ptr(d_out), _ptr(workspace),
                                              workspace.numel() * workspace.element_size(), _stream(stream)))
 
+    # -- SnapKV consumer of the budgets
+    def snapkv_state_size(self, rows: int, n_seqs: int, obs_window: int) -> int:
+        return int(load().rk_snapkv_state_size(self._h, int(rows), int(n_seqs), int(obs_window)))
+
+    def snapkv_workspace_size(self, rows: int, n_seqs: int, obs_window: int) -> int:
+        return int(load().rk_snapkv_workspace_size(self._h, int(rows), int(n_seqs), int(obs_window)))
+
+    def snapkv_prefill(self, batch: Batch, obs_window: int, state, workspace, stream=None):
+        _check(load().rk_snapkv_prefill(self._h, ctypes.byref(batch._c), int(obs_window), _ptr(state),
+                                        state.numel() * state.element_size(), _ptr(workspace),
+                                        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+    def snapkv_compress(self, batch: Batch, budgets, state, positions, k_out, v_out, workspace, obs_window: int = 32,
+                        pool_kernel: int = 7, pooling: int = RK_POOL_MAX, scores=None, stream=None):
+        p = _SnapParams(int(obs_window), int(pool_kernel), int(pooling))
+        b = np.ascontiguousarray(np.asarray(budgets, dtype=np.int64).reshape(-1))
+        _check(load().rk_snapkv_compress(self._h, ctypes.byref(batch._c), ctypes.byref(p),
+                                         b.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), _ptr(state),
+                                         state.numel() * state.element_size(), _ptr(positions), _ptr(k_out),
+                                         _ptr(v_out), _ptr(scores), _ptr(workspace),
+                                         workspace.numel() * workspace.element_size(), _stream(stream)))
+
     def perturb_values(self, batch: Batch, layer: int, alpha: float, v, row_stride: int, seed: int = 2,
                        protect_head: int = 0, protect_tail: int = 0, stream=None):
         p = _params(seed, 0, protect_head, protect_tail, 0)
         _check(load().rk_perturb_values(self._h, ctypes.byref(batch._c), int(layer), float(alpha), ctypes.byref(p),
                                         _ptr(v), int(row_stride), _stream(stream)))
+
+
+def snapkv_layout(batch: Batch, n_layers: int, budgets):
+    """rk_snapkv_layout: (total kept entries per KV head, offsets int64 [n_seqs * n_layers + 1]).
+    budgets: int [n_seqs, n_layers] (b_{i,l})."""
+    b = np.ascontiguousarray(np.asarray(budgets, dtype=np.int64).reshape(-1))
+    offs = np.zeros(batch.n_seqs * int(n_layers) + 1, dtype=np.int64)
+    total = load().rk_snapkv_layout(ctypes.byref(batch._c), int(n_layers),
+                                    b.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                    offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)))
+    if total < 0:
+        raise RKError(-1, "rk_snapkv_layout: bad arguments")
+    return int(total), offs
 
 
 def timing_begin(family: str):

@@ -234,14 +234,21 @@ struct Noise {
   const rk_perturb_params* p;
 };
 
+// Observation queries to keep from a block (SnapKV prefill): the q columns of
+// each sequence's last w rows.
+struct ObsCapture {
+  void* q;
+  int w;
+};
+
 // One decoder block from h_in to h_out (h_out may equal h_in); `noise` perturbs
 // the block's Values between the q|k|v projection and attention.
 // With `pre`, the block's rows are the window rows of a cached-window batch and
 // attention also reads the cached prefix; `kv_out` (if given) receives the
-// block's K and V columns, row by row.
+// block's K and V columns, row by row, and `obs` the observation queries.
 static rk_status run_block(const rk_model* m, int l, const float* h_in, float* h_out, const Bufs& b,
                            const SeqTable& st, const Noise* noise, hipStream_t s, const KvPrefix* pre = nullptr,
-                           void* kv_out = nullptr) {
+                           void* kv_out = nullptr, const ObsCapture* obs = nullptr) {
   const rk_model_config& c = m->cfg;
   const int R = st.rows, d = c.d_model;
   { Timed t("rmsnorm", s); RK_TRY(launch_rmsnorm(h_in, m->attn_norm[l], b.x, m->bf16, R, d, c.rms_eps, s)); }
@@ -260,6 +267,7 @@ static rk_status run_block(const rk_model* m, int l, const float* h_in, float* h
     RK_TRY(launch_copy_cols(b.qkv, m->qkv_cols * a, (int64_t)c.n_heads * c.head_dim * a, kv_out, kv_cols(m) * a,
                             kv_cols(m) * a, R, s));
   }
+  if (obs) RK_TRY(launch_snap_qobs(b.qkv, m->qkv_cols, st, obs->w, c.n_heads * c.head_dim, obs->q, s));
   if (noise) {
     char* v = (char*)b.qkv + (size_t)(c.n_heads + c.n_kv_heads) * c.head_dim * act_bytes(m);
     Timed t("noise", s);
@@ -521,6 +529,62 @@ static rk_status check_window_model(const rk_model* m) {
   return RK_OK;
 }
 
+// ----------------------------------------------------------------------------- SnapKV consumer
+// Prefill state: the KV cache of every layer for all rows, then the observation
+// queries of every layer.
+struct SnapPlan {
+  size_t kv, q, total;
+};
+
+static SnapPlan snap_plan(const rk_model* m, int64_t R, int n, int w) {
+  const rk_model_config& c = m->cfg;
+  SnapPlan p;
+  size_t o = 0;
+  p.kv = o; o += align256((size_t)c.n_layers * R * kv_cols(m) * 2);
+  p.q = o;  o += align256((size_t)c.n_layers * n * w * c.n_heads * c.head_dim * 2);
+  p.total = o;
+  return p;
+}
+
+// Scratch of the selection: chunk partials, normalizers and one layer's votes.
+struct SnapScratch {
+  size_t part, cnorm, votes, total;
+};
+
+static SnapScratch snap_scratch(const rk_model* m, int64_t R, int n, int w) {
+  const rk_model_config& c = m->cfg;
+  SnapScratch p;
+  size_t o = 0;
+  p.part = o;  o += align256((size_t)n * c.n_heads * w * snap_chunks((int)std::min<int64_t>(R, 0x7fffffff)) * 8);
+  p.cnorm = o; o += align256((size_t)n * c.n_heads * w * 4);
+  p.votes = o; o += align256((size_t)c.n_kv_heads * R * 4);
+  p.total = o;
+  return p;
+}
+
+static rk_status check_snap(const rk_model* m, int w) {
+  if (!m->bf16) { set_error("SnapKV selection needs a bf16 model"); return RK_ERR_UNSUPPORTED; }
+  if (w < 1 || w > 64) { set_error("obs_window must be in [1, 64]"); return RK_ERR_ARG; }
+  const int combos = (m->cfg.n_heads / m->cfg.n_kv_heads) * ((w + 31) / 32);
+  if (combos > kSnapMaxCombos) {
+    set_error("(n_heads / n_kv_heads) * ceil(obs_window / 32) = %d exceeds %d", combos, kSnapMaxCombos);
+    return RK_ERR_UNSUPPORTED;
+  }
+  return RK_OK;
+}
+
+static rk_status check_snap_lengths(const SeqTable& st, int w) {
+  for (int i = 0; i < st.n; ++i) {
+    const int T = st.off[i + 1] - st.off[i];
+    if (T <= w) { set_error("sequence %d (%d tokens) is not longer than obs_window %d", i, T, w); return RK_ERR_SHAPE; }
+    if (T - w > kSnapMaxPrefix) {
+      set_error("sequence %d: prefix of %d positions exceeds %d", i, T - w, kSnapMaxPrefix);
+      return RK_ERR_UNSUPPORTED;
+    }
+  }
+  return RK_OK;
+}
+
 // One recorded launch sequence per process: the sensitivity profile's kernels
 // captured on a private stream into a HIP graph (after an eager run of the same
 // call), replayed on the caller's stream while the arguments stay the same.
@@ -705,6 +769,123 @@ rk_status rk_window_reference(const rk_model* m, const rk_batch* batch, int32_t 
   if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
   const Bufs b = carve(wp, workspace);
   return window_reference(m, batch->tokens, st, pst, wst, win_view(m, st.rows, state), b, (hipStream_t)stream);
+}
+
+size_t rk_snapkv_state_size(const rk_model* m, int64_t n_rows, int32_t n_seqs, int32_t obs_window) {
+  if (!m || !m->bf16 || n_rows < 1 || n_seqs < 1 || obs_window < 1) return 0;
+  return snap_plan(m, n_rows, n_seqs, obs_window).total;
+}
+
+size_t rk_snapkv_workspace_size(const rk_model* m, int64_t n_rows, int32_t n_seqs, int32_t obs_window) {
+  if (!m || !m->bf16 || n_rows < 1 || n_seqs < 1 || obs_window < 1) return 0;
+  return std::max(ws_plan(m, n_rows, 1, 0).total, snap_scratch(m, n_rows, n_seqs, obs_window).total);
+}
+
+rk_status rk_snapkv_prefill(const rk_model* m, const rk_batch* batch, int32_t obs_window, void* state,
+                            size_t state_bytes, void* workspace, size_t ws_bytes, void* stream) {
+  rk_status e = check_batch(m, batch);
+  if (e != RK_OK) return e;
+  if ((e = check_snap(m, obs_window)) != RK_OK) return e;
+  if (!state || !workspace) { set_error("null state or workspace"); return RK_ERR_ARG; }
+  SeqTable st;
+  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  for (int i = 0; i < st.n; ++i)
+    if (st.off[i + 1] - st.off[i] <= obs_window) {
+      set_error("sequence %d is not longer than obs_window %d", i, obs_window);
+      return RK_ERR_SHAPE;
+    }
+  const SnapPlan sp = snap_plan(m, st.rows, st.n, obs_window);
+  if (state_bytes < sp.total) { set_error("SnapKV state too small (%zu < %zu)", state_bytes, sp.total); return RK_ERR_WORKSPACE; }
+  const WsPlan wp = ws_plan(m, st.rows, 1, 0);
+  if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
+  const Bufs b = carve(wp, workspace);
+  const rk_model_config& c = m->cfg;
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t R = st.rows, d = c.d_model;
+  char* kv = (char*)state + sp.kv;
+  char* q = (char*)state + sp.q;
+  const size_t kv_layer = (size_t)R * kv_cols(m) * 2, q_layer = (size_t)st.n * obs_window * c.n_heads * c.head_dim * 2;
+  RK_TRY(launch_rope_table(b.rope, b.rope_pos, st, c.head_dim, c.rope_theta, s));
+  RK_TRY(launch_embed(m->tok_emb, m->bf16, batch->tokens, b.h, (int)R, (int)d, s));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const ObsCapture obs{q + l * q_layer, obs_window};
+    if ((e = run_block(m, l, b.h, b.h, b, st, nullptr, s, nullptr, kv + l * kv_layer, &obs)) != RK_OK) return e;
+  }
+  return RK_OK;
+}
+
+int64_t rk_snapkv_layout(const rk_batch* batch, int32_t n_layers, const int64_t* budgets, int64_t* offsets_out) {
+  if (!batch || !batch->offsets || !budgets || n_layers < 1 || batch->n_seqs < 1) return -1;
+  int64_t total = 0;
+  for (int i = 0; i < batch->n_seqs; ++i) {
+    const int64_t T = batch->offsets[i + 1] - batch->offsets[i];
+    if (T < 0) return -1;
+    for (int l = 0; l < n_layers; ++l) {
+      if (offsets_out) offsets_out[(int64_t)i * n_layers + l] = total;
+      total += std::min(std::max(budgets[(int64_t)i * n_layers + l], (int64_t)0), T);
+    }
+  }
+  if (offsets_out) offsets_out[(int64_t)batch->n_seqs * n_layers] = total;
+  return total;
+}
+
+rk_status rk_snapkv_compress(const rk_model* m, const rk_batch* batch, const rk_snapkv_params* p,
+                             const int64_t* budgets, const void* state, size_t state_bytes, int32_t* positions,
+                             void* k_out, void* v_out, float* scores, void* workspace, size_t ws_bytes,
+                             void* stream) {
+  rk_status e = check_batch(m, batch);
+  if (e != RK_OK) return e;
+  if (!p || !budgets || !state || !positions || !k_out || !v_out || !workspace) {
+    set_error("null params, budgets, state, outputs or workspace");
+    return RK_ERR_ARG;
+  }
+  const int w = p->obs_window;
+  if ((e = check_snap(m, w)) != RK_OK) return e;
+  if (p->pool_kernel < 1 || p->pool_kernel > 31 || p->pool_kernel % 2 == 0) {
+    set_error("pool_kernel must be odd and in [1, 31]");
+    return RK_ERR_ARG;
+  }
+  if (p->pooling != RK_POOL_MAX && p->pooling != RK_POOL_AVG) { set_error("unknown pooling"); return RK_ERR_ARG; }
+  SeqTable st;
+  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  if ((e = check_snap_lengths(st, w)) != RK_OK) return e;
+  const SnapPlan sp = snap_plan(m, st.rows, st.n, w);
+  if (state_bytes < sp.total) { set_error("SnapKV state too small (%zu < %zu)", state_bytes, sp.total); return RK_ERR_WORKSPACE; }
+  const SnapScratch sc = snap_scratch(m, st.rows, st.n, w);
+  if (ws_bytes < sc.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, sc.total); return RK_ERR_WORKSPACE; }
+  const rk_model_config& c = m->cfg;
+  const int L = c.n_layers;
+  std::vector<int64_t> offs((size_t)st.n * L + 1);
+  if (rk_snapkv_layout(batch, L, budgets, offs.data()) < 0) { set_error("bad budgets or offsets"); return RK_ERR_ARG; }
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  float2* part = (float2*)(ws + sc.part);
+  float* cnorm = (float*)(ws + sc.cnorm);
+  float* votes = (float*)(ws + sc.votes);
+  const int64_t prefix_rows = (int64_t)st.rows - (int64_t)st.n * w;
+  const int64_t ldkv = kv_cols(m);
+  const size_t kv_layer = (size_t)st.rows * ldkv * 2, q_layer = (size_t)st.n * w * c.n_heads * c.head_dim * 2;
+  std::vector<int32_t> keep(st.n);
+  std::vector<int64_t> entry0(st.n);
+  for (int l = 0; l < L; ++l) {
+    const char* kv = (const char*)state + sp.kv + l * kv_layer;
+    const char* q = (const char*)state + sp.q + l * q_layer;
+    {
+      Timed t("snap_scores", s);
+      RK_TRY(launch_snap_scores(kv, ldkv, q, st, w, c.n_heads, c.n_kv_heads, c.head_dim, part, cnorm, votes,
+                                prefix_rows, s));
+    }
+    for (int i = 0; i < st.n; ++i) {
+      const int64_t o = offs[(size_t)i * L + l];
+      keep[i] = (int32_t)(offs[(size_t)i * L + l + 1] - o);
+      entry0[i] = o * c.n_kv_heads;
+    }
+    Timed t("snap_select", s);
+    RK_TRY(launch_snap_select(votes, prefix_rows, kv, ldkv, st, w, c.n_kv_heads, c.head_dim, p->pool_kernel,
+                              p->pooling == RK_POOL_AVG, keep.data(), entry0.data(), positions, k_out, v_out,
+                              scores ? scores + (size_t)l * c.n_kv_heads * prefix_rows : nullptr, s));
+  }
+  return RK_OK;
 }
 
 size_t rk_workspace_size(const rk_model* m, int64_t max_rows, int32_t max_group, uint32_t flags) {

@@ -242,3 +242,70 @@ def test_cached_window_entry_points_validate_before_launching():
     assert lib.rk_sensitivity_profile(h, ctypes.byref(batch), lay, 1, alp, 1, ctypes.byref(p_long), 1000, 1, fake,
                                       None, fake, big, None) == rk.RK_ERR_SHAPE
     lib.rk_model_destroy(h)
+
+
+def test_snapkv_entry_points_validate_before_launching():
+    """Argument checks and the host layout helper of the SnapKV consumer (no kernel runs here)."""
+    lib = rk.load()
+    fake = ctypes.c_void_p(0x1000)
+    offs = np.array([0, 100, 250], dtype=np.int64)
+    batch = rk._Batch(fake, offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 2, 0)
+    big = 1 << 40
+    L = 2
+    budgets = np.array([[30, 200], [0, 90]], dtype=np.int64)
+    bptr = budgets.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))
+    # layout: n_keep = min(max(b, 0), T) in (sequence, layer) order
+    o = np.zeros(5, dtype=np.int64)
+    assert lib.rk_snapkv_layout(ctypes.byref(batch), L, bptr, o.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))) == 220
+    assert list(o) == [0, 30, 130, 130, 220]
+    total, o2 = rk.snapkv_layout(_BatchView(batch), L, budgets)
+    assert total == 220 and list(o2) == list(o)
+    assert lib.rk_snapkv_layout(ctypes.byref(batch), 0, bptr, None) == -1
+    # fp32 models are not supported
+    st, h32 = _create(_FakeCfg(dtype="f32"))
+    assert lib.rk_snapkv_state_size(h32, 250, 2, 32) == 0
+    assert lib.rk_snapkv_prefill(h32, ctypes.byref(batch), 32, fake, big, fake, big, None) == rk.RK_ERR_UNSUPPORTED
+    lib.rk_model_destroy(h32)
+    st, h = _create(_FakeCfg())
+    assert st == rk.RK_OK
+    assert 0 < lib.rk_snapkv_state_size(h, 250, 2, 32) < lib.rk_snapkv_state_size(h, 250, 2, 64)
+    assert lib.rk_snapkv_workspace_size(h, 250, 2, 32) > 0
+    sp = lambda w, k, pool: rk._SnapParams(w, k, pool)
+    call = lambda p, sb=big, wb=big, bud=bptr: lib.rk_snapkv_compress(h, ctypes.byref(batch), ctypes.byref(p), bud,
+                                                                       fake, sb, fake, fake, fake, None, fake, wb,
+                                                                       None)
+    assert call(sp(0, 7, 0)) == rk.RK_ERR_ARG            # empty observation window
+    assert call(sp(65, 7, 0)) == rk.RK_ERR_ARG           # window above 64
+    assert call(sp(32, 6, 0)) == rk.RK_ERR_ARG           # even pooling kernel
+    assert call(sp(32, 33, 0)) == rk.RK_ERR_ARG          # kernel above 31
+    assert call(sp(32, 7, 5)) == rk.RK_ERR_ARG           # unknown pooling
+    assert call(sp(32, 7, 0), sb=16) == rk.RK_ERR_WORKSPACE
+    assert call(sp(32, 7, 0), wb=16) == rk.RK_ERR_WORKSPACE
+    assert call(sp(32, 7, 0), bud=None) == rk.RK_ERR_ARG
+    short = np.array([0, 30, 250], dtype=np.int64)       # a sequence not longer than the window
+    bs = rk._Batch(fake, short.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 2, 0)
+    assert lib.rk_snapkv_compress(h, ctypes.byref(bs), ctypes.byref(sp(32, 7, 0)), bptr, fake, big, fake, fake, fake,
+                                  None, fake, big, None) == rk.RK_ERR_SHAPE
+    assert lib.rk_snapkv_prefill(h, ctypes.byref(bs), 32, fake, big, fake, big, None) == rk.RK_ERR_SHAPE
+    longp = np.array([0, 40000], dtype=np.int64)           # prefix beyond what the selection holds
+    bl = rk._Batch(fake, longp.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 1, 0)
+    assert lib.rk_snapkv_compress(h, ctypes.byref(bl), ctypes.byref(sp(32, 7, 0)), bptr, fake, big, fake, fake, fake,
+                                  None, fake, big, None) == rk.RK_ERR_UNSUPPORTED
+    assert lib.rk_snapkv_prefill(h, ctypes.byref(batch), 32, fake, 16, fake, big, None) == rk.RK_ERR_WORKSPACE
+    lib.rk_model_destroy(h)
+    # grouped queries x query blocks beyond 8
+    st, hg = _create(_FakeCfg(n_heads=32, n_kv_heads=2))
+    assert st == rk.RK_OK
+    assert lib.rk_snapkv_prefill(hg, ctypes.byref(batch), 32, fake, big, fake, big, None) == rk.RK_ERR_UNSUPPORTED
+    lib.rk_model_destroy(hg)
+
+
+class _BatchView:
+    """A binding Batch over an existing ctypes batch (host-only tests)."""
+
+    def __init__(self, c):
+        self._c = c
+
+    @property
+    def n_seqs(self):
+        return self._c.n_seqs
