@@ -155,6 +155,151 @@ def cpu_baseline(w, W, toks, prefix: int = 2048):
                       f"{dt:.1f} s for {n} token-layers (clean pass included)"}
 
 
+SNAP_WINDOW, SNAP_KERNEL, SNAP_RHO, SNAP_RATIO = 32, 7, 0.2, 2.0
+
+
+def snapkv_budgets(w, L: int):
+    """Per-sequence, per-layer budgets: B_i = rho T_i L (Eq. global-budget with a
+    retention ratio rho) split by the allocation half of Algorithm 1 over a fixed
+    decreasing profile s_l = 1 / (1 + l)."""
+    import paper_2608_08684_amd as rk
+    s = [1.0 / (1.0 + l) for l in range(L)]
+    return np.array([rk.layer_budgets(s, int(round(SNAP_RHO * T * L)), SNAP_RATIO)[1] for T in w.lengths()],
+                    dtype=np.int64)
+
+
+def snapkv_bytes(cfg, lens, budgets, obs: int):
+    """Algorithmic HBM bytes per layer of the two kernel families (averaged over
+    layers): scores read every Key twice (statistics, then votes), the observation
+    queries once and write the votes; select reads the votes, reads and writes the
+    retained Keys and Values and writes their positions."""
+    R, n = int(sum(lens)), len(lens)
+    L, Hkv, H, dh = cfg.n_layers, cfg.n_kv_heads, cfg.n_heads, cfg.head_dim
+    pre = R - n * obs
+    scores = 2 * R * Hkv * dh * 2 + n * obs * H * dh * 2 + Hkv * pre * 4
+    kept = sum(min(max(int(b), 0), T) for T, row in zip(lens, budgets) for b in row) / L
+    select = Hkv * pre * 4 + kept * Hkv * (4 * dh * 2 + 4)
+    return scores, select
+
+
+def cpu_baseline_snapkv(cfg, layers: int = 6):
+    """Oracle SnapKV selection of one 8192-token sequence of the same shape, the
+    first `layers` layers of a fixtures cache state."""
+    import fixtures as F
+    from oracle import snapkv as OS
+    T, obs = 8192, SNAP_WINDOW
+    H, Hkv, dh = cfg.n_heads, cfg.n_kv_heads, cfg.head_dim
+    kv, q = F.make_kv_state(layers, [T], H, Hkv, dh, obs, seed_id=99)
+    p = OS.SnapParams(obs_window=obs, pool_kernel=SNAP_KERNEL)
+    b = int(round(SNAP_RHO * T))
+    t0 = time.perf_counter()
+    for l in range(layers):
+        k = F.bf16_to_f32(kv[l, :, : Hkv * dh]).astype(np.float64).reshape(T, Hkv, dh)
+        v = F.bf16_to_f32(kv[l, :, Hkv * dh:]).astype(np.float64).reshape(T, Hkv, dh)
+        qq = np.zeros((T, H, dh))
+        qq[T - obs:] = F.bf16_to_f32(q[l]).astype(np.float64).reshape(obs, H, dh) * (np.sqrt(dh) / 1.4426950408889634)
+        OS.compress_layer(qq, k, v, b, p)
+    dt = time.perf_counter() - t0
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max(int(x.get("num_threads", 1)) for x in threadpool_info()) if threadpool_info() else os.cpu_count()
+    except Exception:
+        cores = os.cpu_count()
+    return {"value": T * layers / dt, "unit": "prompt token-layers/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"one {T}-token sequence of the same shape, {layers} layers, b = {b}, float64 oracle: "
+                      f"{dt:.1f} s"}
+
+
+def snapkv_main(args):
+    """SnapKV selection with the per-layer budgets (the budgets' consumer) on the
+    Llama-3-8B shape: 4 x 8192-token prompts, 32 layers, 32 query / 8 KV heads of
+    128, observation window 32, max pooling 7, budgets from a 20% retention."""
+    import torch
+    import fixtures as F
+    import paper_2608_08684_amd as rk
+    from tests.gpu_helpers import make_batch
+    w = F.get_workload("llama3-8b-bf16")
+    cfg = w.model
+    L, H, Hkv, dh = cfg.n_layers, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim
+    lens = w.lengths()
+    obs = SNAP_WINDOW
+    t0 = time.perf_counter()
+    # the selection reads only the model's shape; one placeholder buffer stands in for the weights
+    ph = torch.zeros(256, dtype=torch.uint8, device="cuda")
+    model = rk.Model(cfg, {"tok_emb": ph, "lm_head": ph, "final_norm": ph,
+                           **{k: [ph] * L for k in ("w_qkv", "w_o", "w_gate_up", "w_down", "attn_norm", "mlp_norm")}})
+    batch = make_batch([np.zeros(T, dtype=np.int32) for T in lens])
+    R = batch.rows
+    # prompt caches: two fixtures layers, repeated over the 32 layers
+    kv2, q2 = F.make_kv_state(2, lens, H, Hkv, dh, obs, seed_id=7)
+    state = torch.empty(model.snapkv_state_size(R, len(lens), obs), dtype=torch.uint8, device="cuda")
+    kvl = R * 2 * Hkv * dh * 2
+    ql = len(lens) * obs * H * dh * 2
+    q_off = (L * kvl + 255) // 256 * 256
+    for l in range(L):
+        state[l * kvl:(l + 1) * kvl] = torch.from_numpy(kv2[l % 2].reshape(-1).view(np.uint8)).cuda()
+        state[q_off + l * ql:q_off + (l + 1) * ql] = torch.from_numpy(q2[l % 2].reshape(-1).view(np.uint8)).cuda()
+    del kv2, q2
+    budgets = snapkv_budgets(w, L)
+    total, _ = rk.snapkv_layout(batch, L, budgets)
+    pos = torch.empty(Hkv * total, dtype=torch.int32, device="cuda")
+    ko = torch.empty(Hkv * total, dh, dtype=torch.int16, device="cuda")
+    vo = torch.empty_like(ko)
+    ws = torch.empty(model.snapkv_workspace_size(R, len(lens), obs), dtype=torch.uint8, device="cuda")
+    log(f"SnapKV inputs ready in {time.perf_counter() - t0:.1f} s")
+
+    def step():
+        model.snapkv_compress(batch, budgets, state, pos, ko, vo, ws, obs_window=obs, pool_kernel=SNAP_KERNEL,
+                              pooling=rk.RK_POOL_MAX)
+
+    fams = ("snap_scores", "snap_select")
+    for k in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    fam_ms = {f: 0.0 for f in fams}
+    fam_n = {f: 0 for f in fams}
+    fam_steps = {f: 0 for f in fams}
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        f = fams[k % 2]                 # alternate the timed family step by step
+        rk.timing_begin(f)
+        step()
+        n, ms = rk.timing_end()
+        fam_n[f] += n
+        fam_ms[f] += ms
+        fam_steps[f] += 1
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    value = R * L / (ms_per_step / 1e3)
+    # algorithmic bytes per launch = bytes of every layer / launches per call
+    per_layer = dict(zip(fams, snapkv_bytes(cfg, lens, budgets, obs)))
+    per_launch = {f: per_layer[f] * L / (fam_n[f] / max(fam_steps[f], 1)) if fam_n[f] else 0.0 for f in fams}
+    avg = {f: fam_ms[f] / max(fam_n[f], 1) for f in fams}
+    step_ms = {f: fam_ms[f] / max(fam_steps[f], 1) for f in fams}
+    dom = max(fams, key=lambda f: step_ms[f])
+    achieved = per_launch[dom] / (avg[dom] / 1e3) / 1e9
+    roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": dom, "launches": fam_n[dom],
+            "avg_ms": round(avg[dom], 4), "bytes_per_launch": int(per_launch[dom]),
+            "other": {f: {"avg_ms": round(avg[f], 4), "bytes_per_launch": int(per_launch[f]),
+                          "GB/s": round(per_launch[f] / (avg[f] / 1e3) / 1e9, 1)} for f in fams if f != dom}}
+    log(f"{dom}: {fam_n[dom]} launches, avg {avg[dom]:.4f} ms, {achieved:.0f} GB/s")
+    res = {
+        "metric": "prompt token-layers/s (SnapKV selection with per-layer budgets)",
+        "value": round(value, 1), "unit": "token-layers/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (fixtures cache state: N(0,1) keys and values "
+                                                       "with heavy hitters, observation queries)",
+        "config": {"workload": f"llama3-8b-bf16 SnapKV: {L}L {H}q/{Hkv}kv x {dh}; {len(lens)}x{max(lens)} tokens; "
+                               f"window {obs}, max pooling {SNAP_KERNEL}; budgets rho {SNAP_RHO}, r {SNAP_RATIO} "
+                               f"over s_l = 1/(1+l); {total} kept positions per KV head"},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline_snapkv(cfg)
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -168,6 +313,8 @@ def main():
     ap.add_argument("--window", type=int, default=0,
                     help="cached-window mode: evaluate the last WINDOW tokens of every sequence against the cached "
                          "prefix (0: the resumed full-sequence profile)")
+    ap.add_argument("--snapkv", action="store_true",
+                    help="time the SnapKV selection with per-layer budgets (the budgets' consumer) instead")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (calibrates HBM byte counters)")
     ap.add_argument("--derive-traffic", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
@@ -192,6 +339,9 @@ def main():
             y.copy_(x)
         torch.cuda.synchronize()
         log(f"copied {n} bytes 3 times")
+        return
+    if args.snapkv:
+        snapkv_main(args)
         return
     import fixtures as F
     import paper_2608_08684_amd as rk

@@ -546,7 +546,7 @@ static SnapPlan snap_plan(const rk_model* m, int64_t R, int n, int w) {
   return p;
 }
 
-// Scratch of the selection: chunk partials, normalizers and one layer's votes.
+// Scratch of the selection: chunk partials, normalizers and every layer's votes.
 struct SnapScratch {
   size_t part, cnorm, votes, total;
 };
@@ -555,9 +555,10 @@ static SnapScratch snap_scratch(const rk_model* m, int64_t R, int n, int w) {
   const rk_model_config& c = m->cfg;
   SnapScratch p;
   size_t o = 0;
-  p.part = o;  o += align256((size_t)n * c.n_heads * w * snap_chunks((int)std::min<int64_t>(R, 0x7fffffff)) * 8);
-  p.cnorm = o; o += align256((size_t)n * c.n_heads * w * 4);
-  p.votes = o; o += align256((size_t)c.n_kv_heads * R * 4);
+  p.part = o;  o += align256((size_t)c.n_layers * n * c.n_heads * w *
+                             snap_chunks((int)std::min<int64_t>(R, 0x7fffffff)) * 8);
+  p.cnorm = o; o += align256((size_t)c.n_layers * n * c.n_heads * w * 4);
+  p.votes = o; o += align256((size_t)c.n_layers * c.n_kv_heads * R * 4);
   p.total = o;
   return p;
 }
@@ -865,26 +866,29 @@ rk_status rk_snapkv_compress(const rk_model* m, const rk_batch* batch, const rk_
   const int64_t prefix_rows = (int64_t)st.rows - (int64_t)st.n * w;
   const int64_t ldkv = kv_cols(m);
   const size_t kv_layer = (size_t)st.rows * ldkv * 2, q_layer = (size_t)st.n * w * c.n_heads * c.head_dim * 2;
-  std::vector<int32_t> keep(st.n);
-  std::vector<int64_t> entry0(st.n);
-  for (int l = 0; l < L; ++l) {
-    const char* kv = (const char*)state + sp.kv + l * kv_layer;
-    const char* q = (const char*)state + sp.q + l * q_layer;
-    {
-      Timed t("snap_scores", s);
-      RK_TRY(launch_snap_scores(kv, ldkv, q, st, w, c.n_heads, c.n_kv_heads, c.head_dim, part, cnorm, votes,
-                                prefix_rows, s));
-    }
-    for (int i = 0; i < st.n; ++i) {
-      const int64_t o = offs[(size_t)i * L + l];
-      keep[i] = (int32_t)(offs[(size_t)i * L + l + 1] - o);
-      entry0[i] = o * c.n_kv_heads;
-    }
-    Timed t("snap_select", s);
-    RK_TRY(launch_snap_select(votes, prefix_rows, kv, ldkv, st, w, c.n_kv_heads, c.head_dim, p->pool_kernel,
-                              p->pooling == RK_POOL_AVG, keep.data(), entry0.data(), positions, k_out, v_out,
-                              scores ? scores + (size_t)l * c.n_kv_heads * prefix_rows : nullptr, s));
+  // votes of every layer, then one selection pass over all (sequence, layer) items
+  {
+    Timed t("snap_scores", s);
+    RK_TRY(launch_snap_scores((const char*)state + sp.kv, ldkv, (int64_t)(kv_layer / 2), (const char*)state + sp.q,
+                              (int64_t)(q_layer / 2), L, st, w, c.n_heads, c.n_kv_heads, c.head_dim, part, cnorm,
+                              votes, prefix_rows, s));
   }
+  const int n_items = st.n * L;
+  std::vector<int16_t> seq(n_items), lay(n_items);
+  std::vector<int32_t> keep(n_items);
+  std::vector<int64_t> entry0(n_items);
+  for (int i = 0; i < st.n; ++i)
+    for (int l = 0; l < L; ++l) {
+      const size_t j = (size_t)i * L + l;
+      seq[j] = (int16_t)i;
+      lay[j] = (int16_t)l;
+      keep[j] = (int32_t)(offs[j + 1] - offs[j]);
+      entry0[j] = offs[j] * c.n_kv_heads;
+    }
+  Timed t("snap_select", s);
+  RK_TRY(launch_snap_select(votes, prefix_rows, (const char*)state + sp.kv, ldkv, (int64_t)(kv_layer / 2), st, w,
+                            c.n_kv_heads, c.head_dim, p->pool_kernel, p->pooling == RK_POOL_AVG, n_items, seq.data(),
+                            lay.data(), keep.data(), entry0.data(), positions, k_out, v_out, scores, s));
   return RK_OK;
 }
 

@@ -158,16 +158,20 @@ hipError_t launch_snap_qobs(const void* qkv, int64_t ldq, const SeqTable& st, in
 constexpr int kSnapMaxPrefix = RK_SNAPKV_MAX_PREFIX;   // prefix positions held in LDS by the selection
 constexpr int kSnapMaxCombos = 8;                      // (query heads per KV head) x ceil(w / 32)
 int snap_chunks(int max_len);                          // key chunks of the scoring kernels
-// votes[g * prefix_rows + (off[i] - i w) + u] for prefix keys u < T_i - w; part: n * H * w * chunks
-// float2, cnorm: n * H * w floats.
-hipError_t launch_snap_scores(const void* kv, int64_t ldkv, const void* qobs, const SeqTable& st, int w, int n_heads,
-                              int n_kv, int head_dim, float2* part, float* cnorm, float* votes, int64_t prefix_rows,
+// Votes of every layer: votes[(l * n_kv + g) * prefix_rows + (off[i] - i w) + u] for prefix keys
+// u < T_i - w; layer l's cache at kv + l * kv_layer_stride and queries at qobs + l * q_layer_stride
+// (elements); part: L * n * H * w * chunks float2, cnorm: L * n * H * w floats.
+hipError_t launch_snap_scores(const void* kv, int64_t ldkv, int64_t kv_layer_stride, const void* qobs,
+                              int64_t q_layer_stride, int n_layers, const SeqTable& st, int w, int n_heads, int n_kv,
+                              int head_dim, float2* part, float* cnorm, float* votes, int64_t prefix_rows,
                               hipStream_t s);
-// Pooling, selection and gather; keep[i], entry0[i] per sequence (host arrays of st.n).
+// Pooling, selection and gather for n_items (sequence, layer) items (host arrays);
+// votes and scores [layer][n_kv][prefix_rows], kv of layer l at kv + l * kv_layer_stride.
 hipError_t launch_snap_select(const float* votes, int64_t prefix_rows, const void* kv, int64_t ldkv,
-                              const SeqTable& st, int w, int n_kv, int head_dim, int pool_kernel, bool pool_avg,
-                              const int32_t* keep, const int64_t* entry0, int32_t* positions, void* k_out,
-                              void* v_out, float* scores, hipStream_t s);
+                              int64_t kv_layer_stride, const SeqTable& st, int w, int n_kv, int head_dim,
+                              int pool_kernel, bool pool_avg, int n_items, const int16_t* seq, const int16_t* layer,
+                              const int32_t* keep, const int64_t* entry0, int32_t* positions, void* k_out, void* v_out,
+                              float* scores, hipStream_t s);
 hipError_t launch_finalize(const double* s_acc, int n, double inv_n, float* s_out, hipStream_t s);
 hipError_t launch_zero_f64(double* p, int n, hipStream_t s);
 
