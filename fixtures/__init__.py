@@ -300,3 +300,15 @@ def make_kv_state(n_layers: int, lengths: Sequence[int], n_heads: int, n_kv_head
         kv[l] = bf16_bits(np.concatenate([k.reshape(R, -1), v.reshape(R, -1)], axis=1))
         q[l] = bf16_bits(qq.reshape(n * obs_window, -1))
     return kv, q
+
+
+def random_keep(n_seqs: int, n_kv_heads: int, P: int, b: int, seed_id: int = 0) -> np.ndarray:
+    """Retained prompt positions for compression tests: for every sequence and KV
+    head, b distinct positions in [0, P), increasing; int32 [n, H_kv, b].  Drawn
+    from ``default_rng([4, seed_id])``."""
+    rng = np.random.default_rng([4, seed_id])
+    out = np.empty((n_seqs, n_kv_heads, b), dtype=np.int32)
+    for i in range(n_seqs):
+        for g in range(n_kv_heads):
+            out[i, g] = np.sort(rng.choice(P, size=b, replace=False))
+    return out

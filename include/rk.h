@@ -330,6 +330,33 @@ rk_status rk_snapkv_compress(const rk_model *m, const rk_batch *batch, const rk_
                              void *k_out, void *v_out, float *scores, void *workspace, size_t ws_bytes,
                              void *stream);
 
+/* ---------------------------------------------------------------- compression damage */
+
+/* Isolated single-layer compression damage (Section 2, Eq.
+ * layer-compression-damage) in the cached-window split: the window [P, T) of
+ * every sequence is evaluated against the prompt caches of rk_window_reference
+ * (same batch, window_start = P) with only layer `layer`'s prompt cache
+ * restricted to n_keep retained positions per KV head (1 <= n_keep <= P); the
+ * other layers keep their full caches.  d_out[i] = mean over the window of
+ * KL(P_full || P_compressed), kl_pos (may be NULL) the per-position values
+ * (window rows only).
+ *   positions: DEVICE int32, position j (< P, within the sequence) retained by
+ *     KV head g of sequence i at positions[i * seq_stride + g * n_keep + j]
+ *     (seq_stride >= n_kv_heads * n_keep).  With the outputs of
+ *     rk_snapkv_compress for prompts of P tokens and the same budget b at every
+ *     layer, layer l's positions start at entry l * n_kv_heads * b with
+ *     seq_stride = n_layers * n_kv_heads * b.
+ * Workspace: rk_workspace_size(m, rows, 1, RK_FLAG_CACHED_WINDOW).  bf16 only.  */
+rk_status rk_compression_damage(const rk_model *m, const rk_batch *batch, int32_t window_start, int32_t layer,
+                                const int32_t *positions, int64_t seq_stride, int32_t n_keep, const void *state,
+                                size_t state_bytes, float *d_out, float *kl_pos, void *workspace, size_t ws_bytes,
+                                void *stream);
+
+/* Spearman's rho of two profiles x, y [n] (Section 2, Table
+ * sensitivity-correlation): the Pearson correlation of their ranks, ties sharing
+ * the mean rank; NaN when a profile is constant.  Host only, float64.          */
+rk_status rk_spearman(const double *x, const double *y, int32_t n, double *rho);
+
 /* ---------------------------------------------------------------- diagnostics */
 
 /* Per-kernel timing for measurement: after rk_timing_begin(family) every launch

@@ -27,7 +27,7 @@ import numpy as np
 
 __all__ = ["RKError", "load", "Model", "Batch", "layer_budgets", "timing_begin", "timing_end", "LIB_PATH", "RK_FLAG_FULL_RECOMPUTE",
            "RK_FLAG_UNFUSED_KL", "RK_FLAG_CACHED_WINDOW", "RK_FLAG_GRAPH", "RK_WS_CLEAN_STATE", "RK_MAX_BATCH_SEQS", "RK_MAX_GROUP",
-           "RK_POOL_MAX", "RK_POOL_AVG", "RK_SNAPKV_MAX_PREFIX", "snapkv_layout"]
+           "RK_POOL_MAX", "RK_POOL_AVG", "RK_SNAPKV_MAX_PREFIX", "snapkv_layout", "spearman"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librk.so")
 
@@ -117,6 +117,9 @@ def load() -> ctypes.CDLL:
         "rk_last_error": (ctypes.c_char_p, []),
         "rk_timing_begin": (st, [ctypes.c_char_p]),
         "rk_timing_end": (st, [ctypes.POINTER(i64), ctypes.POINTER(f64)]),
+        "rk_compression_damage": (st, [vp, ctypes.POINTER(_Batch), i32, i32, vp, i64, i32, vp, sz, vp, vp, vp, sz,
+                                       vp]),
+        "rk_spearman": (st, [ctypes.POINTER(f64), ctypes.POINTER(f64), i32, ctypes.POINTER(f64)]),
         "rk_snapkv_state_size": (sz, [vp, i64, i32, i32]),
         "rk_snapkv_workspace_size": (sz, [vp, i64, i32, i32]),
         "rk_snapkv_prefill": (st, [vp, ctypes.POINTER(_Batch), i32, vp, sz, vp, sz, vp]),
@@ -252,6 +255,15 @@ class Model:
                                              _ptr(d_out), _ptr(workspace),
                                              workspace.numel() * workspace.element_size(), _stream(stream)))
 
+    def compression_damage(self, batch: Batch, window_start: int, layer: int, positions, n_keep: int, state, d_out,
+                           workspace, seq_stride=None, kl_pos=None, stream=None):
+        stride = int(self.cfg.n_kv_heads * n_keep if seq_stride is None else seq_stride)
+        _check(load().rk_compression_damage(self._h, ctypes.byref(batch._c), int(window_start), int(layer),
+                                            _ptr(positions), stride, int(n_keep), _ptr(state),
+                                            state.numel() * state.element_size(), _ptr(d_out), _ptr(kl_pos),
+                                            _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                            _stream(stream)))
+
     # -- SnapKV consumer of the budgets
     def snapkv_state_size(self, rows: int, n_seqs: int, obs_window: int) -> int:
         return int(load().rk_snapkv_state_size(self._h, int(rows), int(n_seqs), int(obs_window)))
@@ -279,6 +291,18 @@ class Model:
         p = _params(seed, 0, protect_head, protect_tail, 0)
         _check(load().rk_perturb_values(self._h, ctypes.byref(batch._c), int(layer), float(alpha), ctypes.byref(p),
                                         _ptr(v), int(row_stride), _stream(stream)))
+
+
+def spearman(x: Sequence[float], y: Sequence[float]) -> float:
+    """rk_spearman: Spearman's rho (average ranks for ties; nan for a constant profile)."""
+    xv = np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+    yv = np.ascontiguousarray(np.asarray(y, dtype=np.float64))
+    if xv.shape != yv.shape:
+        raise ValueError("profiles of different lengths")
+    rho = ctypes.c_double()
+    _check(load().rk_spearman(xv.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                              yv.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), len(xv), ctypes.byref(rho)))
+    return float(rho.value)
 
 
 def snapkv_layout(batch: Batch, n_layers: int, budgets):

@@ -97,7 +97,7 @@ static WinPlan win_plan(const rk_model* m, int64_t R) {
 }
 
 struct WsPlan {
-  size_t h, x, qkv, att, ff, xp, part, logits_c, logits_p, kl, rope, rope_pos, dbatch, sacc, vpert, clean, total;
+  size_t h, x, qkv, att, ff, xp, part, logits_c, logits_p, kl, rope, rope_pos, dbatch, sacc, vpert, cpre, clean, total;
   bool unfused;
 };
 
@@ -136,6 +136,8 @@ static WsPlan ws_plan(const rk_model* m, int64_t R, int G, uint32_t flags) {
   p.sacc = o;     o += align256((size_t)kMaxSAcc * 8);
   p.vpert = o;
   if (flags & RK_FLAG_CACHED_WINDOW) o += align256((size_t)R * (kv_cols(m) / 2) * a);
+  p.cpre = o;   // a compressed prompt cache (K and V columns)
+  if (flags & RK_FLAG_CACHED_WINDOW) o += align256((size_t)R * kv_cols(m) * a);
   p.clean = o;
   if (flags & RK_WS_CLEAN_STATE)
     o += (flags & RK_FLAG_CACHED_WINDOW) ? win_plan(m, R).total : clean_plan(m, R).total;
@@ -149,6 +151,7 @@ struct Bufs {
   float2* part; float* logits_c; float* logits_p; float* kl; float2* rope; int32_t* rope_pos; float* dbatch;
   double* sacc;
   void* vpert;
+  void* cpre;
   char* clean;
 };
 
@@ -159,7 +162,7 @@ static Bufs carve(const WsPlan& p, void* ws) {
   u.xp = b + p.xp; u.part = (float2*)(b + p.part); u.logits_c = (float*)(b + p.logits_c);
   u.logits_p = (float*)(b + p.logits_p); u.kl = (float*)(b + p.kl); u.rope = (float2*)(b + p.rope);
   u.rope_pos = (int32_t*)(b + p.rope_pos);
-  u.dbatch = (float*)(b + p.dbatch); u.sacc = (double*)(b + p.sacc); u.vpert = b + p.vpert; u.clean = b + p.clean;
+  u.dbatch = (float*)(b + p.dbatch); u.sacc = (double*)(b + p.sacc); u.vpert = b + p.vpert; u.cpre = b + p.cpre; u.clean = b + p.clean;
   return u;
 }
 
@@ -471,6 +474,34 @@ static rk_status window_perturbed_final(const rk_model* m, const SeqTable& pst, 
     if ((e = run_block(m, l, b.h, b.h, b, wst, nullptr, s, &pk)) != RK_OK) return e;
   }
   RK_TRY(launch_rmsnorm(b.h, m->final_norm, xf_out, m->bf16, (int)Rw, (int)d, c.rms_eps, s));
+  return RK_OK;
+}
+
+// Compression damage of layer `layer` (Section 2, Eq. layer-compression-damage):
+// the window rows resume from their input to that block with its prompt cache
+// replaced by the b retained positions of every KV head (gathered into a b-row
+// cache per sequence); the caches of the other layers stay full.  The rotary
+// table must hold the window positions.
+static rk_status window_compressed_final(const rk_model* m, const SeqTable& pst, const SeqTable& wst, const Win& wn,
+                                         int layer, const int32_t* pos, int64_t seq_stride, int b, void* xf_out,
+                                         const Bufs& bf, hipStream_t s) {
+  const rk_model_config& c = m->cfg;
+  const int64_t d = c.d_model, Rp = pst.rows, Rw = wst.rows, a = act_bytes(m), kc = kv_cols(m);
+  const char* kv_l = (const char*)wn.kv + (size_t)layer * Rp * kc * a;
+  RK_TRY(launch_prefix_gather(kv_l, kc, pst.n, pst.max_len, c.n_kv_heads, c.head_dim, pos, seq_stride, b, bf.cpre,
+                              s));
+  KvPrefix pk;
+  pk.k = (const bf16_t*)bf.cpre;
+  pk.v = (const bf16_t*)bf.cpre + kc / 2;
+  pk.ldk = pk.ldv = kc;
+  pk.P = b;
+  rk_status e = run_block(m, layer, wn.w.h + (size_t)layer * Rw * d, bf.h, bf, wst, nullptr, s, &pk);
+  if (e != RK_OK) return e;
+  for (int l = layer + 1; l < c.n_layers; ++l) {
+    pk = cache_prefix(m, wn, pst, l, nullptr);
+    if ((e = run_block(m, l, bf.h, bf.h, bf, wst, nullptr, s, &pk)) != RK_OK) return e;
+  }
+  RK_TRY(launch_rmsnorm(bf.h, m->final_norm, xf_out, m->bf16, (int)Rw, (int)d, c.rms_eps, s));
   return RK_OK;
 }
 
@@ -889,6 +920,35 @@ rk_status rk_snapkv_compress(const rk_model* m, const rk_batch* batch, const rk_
   RK_TRY(launch_snap_select(votes, prefix_rows, (const char*)state + sp.kv, ldkv, (int64_t)(kv_layer / 2), st, w,
                             c.n_kv_heads, c.head_dim, p->pool_kernel, p->pooling == RK_POOL_AVG, n_items, seq.data(),
                             lay.data(), keep.data(), entry0.data(), positions, k_out, v_out, scores, s));
+  return RK_OK;
+}
+
+rk_status rk_compression_damage(const rk_model* m, const rk_batch* batch, int32_t window_start, int32_t layer,
+                                const int32_t* positions, int64_t seq_stride, int32_t n_keep, const void* state,
+                                size_t state_bytes, float* d_out, float* kl_pos, void* workspace, size_t ws_bytes,
+                                void* stream) {
+  rk_status e = check_batch(m, batch);
+  if (e != RK_OK) return e;
+  if ((e = check_window_model(m)) != RK_OK) return e;
+  if (!positions || !state || !d_out || !workspace) { set_error("null positions, state, d_out or workspace"); return RK_ERR_ARG; }
+  if (layer < 0 || layer >= m->cfg.n_layers) { set_error("layer %d out of range", layer); return RK_ERR_ARG; }
+  if (n_keep < 1 || n_keep > window_start) { set_error("n_keep must be in [1, window_start]"); return RK_ERR_ARG; }
+  if (seq_stride < (int64_t)m->cfg.n_kv_heads * n_keep) { set_error("seq_stride below n_kv_heads * n_keep"); return RK_ERR_ARG; }
+  SeqTable st, pst, wst;
+  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  if ((e = window_tables(st, window_start, &pst, &wst)) != RK_OK) return e;
+  if (state_bytes < win_plan(m, st.rows).total) { set_error("window state too small"); return RK_ERR_WORKSPACE; }
+  const WsPlan wp = ws_plan(m, st.rows, 1, RK_FLAG_CACHED_WINDOW);
+  if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
+  const Bufs b = carve(wp, workspace);
+  const Win wn = win_view(m, st.rows, state);
+  hipStream_t s = (hipStream_t)stream;
+  RK_TRY(launch_rope_table(b.rope, b.rope_pos, wst, m->cfg.head_dim, m->cfg.rope_theta, s, window_start));
+  if ((e = window_compressed_final(m, pst, wst, wn, layer, positions, seq_stride, n_keep, b.xp, b, s)) != RK_OK)
+    return e;
+  float* kl = kl_pos ? kl_pos : b.kl;
+  if ((e = score_group(m, wst, wn.w, b.xp, 1, false, b.logits_p, kl, b, s)) != RK_OK) return e;
+  RK_TRY(launch_window_mean(kl, wst.rows, 1, wst, 0, d_out, s));
   return RK_OK;
 }
 

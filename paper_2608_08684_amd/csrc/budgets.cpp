@@ -82,3 +82,41 @@ extern "C" rk_status rk_layer_budgets(const double* s, int32_t n, int64_t B, dou
   }
   return RK_OK;
 }
+
+// Spearman's rho of two profiles (Section 2, Table sensitivity-correlation): the
+// Pearson correlation of their ranks, tied values sharing the mean of their
+// ranks; NaN when either side is constant.  Host only, float64.
+extern "C" rk_status rk_spearman(const double* x, const double* y, int32_t n, double* rho) {
+  using rk::set_error;
+  if (!x || !y || !rho) { set_error("rk_spearman: null pointer"); return RK_ERR_ARG; }
+  if (n < 2) { set_error("rk_spearman: n must be >= 2"); return RK_ERR_ARG; }
+  for (int32_t i = 0; i < n; ++i)
+    if (!isfinite(x[i]) || !isfinite(y[i])) { set_error("rk_spearman: values must be finite"); return RK_ERR_ARG; }
+  auto ranks = [n](const double* v) {
+    std::vector<int32_t> idx(n);
+    for (int32_t i = 0; i < n; ++i) idx[i] = i;
+    std::stable_sort(idx.begin(), idx.end(), [v](int32_t a, int32_t b) { return v[a] < v[b]; });
+    std::vector<double> r(n);
+    for (int32_t i = 0; i < n;) {
+      int32_t j = i;
+      while (j + 1 < n && v[idx[j + 1]] == v[idx[i]]) ++j;
+      for (int32_t k = i; k <= j; ++k) r[idx[k]] = 0.5 * (i + j) + 1.0;
+      i = j + 1;
+    }
+    return r;
+  };
+  const std::vector<double> rx = ranks(x), ry = ranks(y);
+  double mx = 0.0, my = 0.0;
+  for (int32_t i = 0; i < n; ++i) { mx += rx[i]; my += ry[i]; }
+  mx /= n;
+  my /= n;
+  double sxy = 0.0, sxx = 0.0, syy = 0.0;
+  for (int32_t i = 0; i < n; ++i) {
+    const double a = rx[i] - mx, b = ry[i] - my;
+    sxy += a * b;
+    sxx += a * a;
+    syy += b * b;
+  }
+  *rho = (sxx > 0.0 && syy > 0.0) ? sxy / sqrt(sxx * syy) : NAN;
+  return RK_OK;
+}

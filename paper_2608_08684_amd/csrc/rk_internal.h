@@ -165,6 +165,11 @@ hipError_t launch_snap_scores(const void* kv, int64_t ldkv, int64_t kv_layer_str
                               int64_t q_layer_stride, int n_layers, const SeqTable& st, int w, int n_heads, int n_kv,
                               int head_dim, float2* part, float* cnorm, float* votes, int64_t prefix_rows,
                               hipStream_t s);
+// A prompt cache of b rows per sequence from the retained positions (per KV head) of a
+// full prompt cache of P rows per sequence: row i * b + j, head g <- position
+// pos[i * seq_stride + g * b + j].
+hipError_t launch_prefix_gather(const void* kv, int64_t ldkv, int n_seqs, int P, int n_kv, int head_dim,
+                                const int32_t* pos, int64_t seq_stride, int b, void* out, hipStream_t s);
 // Pooling, selection and gather for n_items (sequence, layer) items (host arrays);
 // votes and scores [layer][n_kv][prefix_rows], kv of layer l at kv + l * kv_layer_stride.
 hipError_t launch_snap_select(const float* votes, int64_t prefix_rows, const void* kv, int64_t ldkv,

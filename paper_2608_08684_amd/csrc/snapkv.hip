@@ -377,7 +377,33 @@ __global__ void snap_qobs_kernel(const bf16_t* __restrict__ qkv, int64_t ldq, Se
     *reinterpret_cast<v4u*>(dst + (int64_t)row * qcols + c) = *reinterpret_cast<const v4u*>(qkv + src_row * ldq + c);
 }
 
+// Layer l's prompt cache restricted to retained positions, laid out as a prompt
+// cache of b rows per sequence: row i * b + j holds, for KV head g, the Key and
+// Value of position pos[i * seq_stride + g * b + j] of sequence i (prompt rows
+// i * P ..).  Used to evaluate the window with only that layer compressed.
+__global__ void prefix_gather_kernel(const bf16_t* __restrict__ kv, int64_t ldkv, int P, int n_kv, int head_dim,
+                                     const int32_t* __restrict__ pos, int64_t seq_stride, int b,
+                                     bf16_t* __restrict__ out) {
+  const int row = blockIdx.x, i = row / b, j = row % b;
+  const int cpr = head_dim / 8;                       // 16-byte chunks per head
+  for (int c = threadIdx.x; c < 2 * n_kv * cpr; c += blockDim.x) {
+    const int kvh = c / cpr, g = kvh % n_kv, ch = c % cpr;   // kvh < n_kv: Keys, else Values
+    const int u = min(max(pos[(int64_t)i * seq_stride + (int64_t)g * b + j], 0), P - 1);
+    const int64_t col = (int64_t)kvh * head_dim + ch * 8;
+    *reinterpret_cast<v4u*>(out + (int64_t)row * ldkv + col) =
+        *reinterpret_cast<const v4u*>(kv + ((int64_t)i * P + u) * ldkv + col);
+  }
+}
+
 // --------------------------------------------------------------------------- launchers
+hipError_t launch_prefix_gather(const void* kv, int64_t ldkv, int n_seqs, int P, int n_kv, int head_dim,
+                                const int32_t* pos, int64_t seq_stride, int b, void* out, hipStream_t s) {
+  if (n_seqs * b == 0) return hipSuccess;
+  prefix_gather_kernel<<<n_seqs * b, 128, 0, s>>>((const bf16_t*)kv, ldkv, P, n_kv, head_dim, pos, seq_stride, b,
+                                                  (bf16_t*)out);
+  return hipGetLastError();
+}
+
 hipError_t launch_snap_qobs(const void* qkv, int64_t ldq, const SeqTable& st, int w, int qcols, void* dst,
                             hipStream_t s) {
   snap_qobs_kernel<<<st.n * w, 128, 0, s>>>((const bf16_t*)qkv, ldq, st, w, qcols, (bf16_t*)dst);

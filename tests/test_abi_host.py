@@ -309,3 +309,43 @@ class _BatchView:
     @property
     def n_seqs(self):
         return self._c.n_seqs
+
+
+def test_spearman_matches_oracle_and_validates():
+    from oracle import damage as OD
+    rng = np.random.default_rng(11)
+    for n in (2, 5, 12, 32):
+        for _ in range(50):
+            x = rng.integers(0, 4, size=n).astype(float)
+            y = rng.standard_normal(n)
+            a, b = rk.spearman(x, y), OD.spearman(x, y)
+            assert (np.isnan(a) and np.isnan(b)) or a == pytest.approx(b, abs=1e-14)
+    with pytest.raises(rk.RKError):
+        rk.spearman([1.0], [2.0])
+    with pytest.raises(rk.RKError):
+        rk.spearman([1.0, np.nan], [2.0, 3.0])
+
+
+def test_compression_damage_validates_before_launching():
+    lib = rk.load()
+    fake = ctypes.c_void_p(0x1000)
+    offs = np.array([0, 100, 250], dtype=np.int64)
+    batch = rk._Batch(fake, offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 2, 0)
+    big = 1 << 40
+    st, h = _create(_FakeCfg())
+    assert st == rk.RK_OK
+    call = lambda P=50, layer=0, keep=10, stride=20, sb=big, wb=big, pos=fake: lib.rk_compression_damage(
+        h, ctypes.byref(batch), P, layer, pos, stride, keep, fake, sb, fake, None, fake, wb, None)
+    assert call(layer=2) == rk.RK_ERR_ARG                 # layer out of range
+    assert call(keep=0) == rk.RK_ERR_ARG                  # nothing kept
+    assert call(keep=51) == rk.RK_ERR_ARG                 # more than the prompt
+    assert call(stride=19) == rk.RK_ERR_ARG               # stride below n_kv_heads * n_keep
+    assert call(pos=None) == rk.RK_ERR_ARG
+    assert call(P=100) == rk.RK_ERR_SHAPE                 # no window left in the first sequence
+    assert call(sb=16) == rk.RK_ERR_WORKSPACE
+    assert call(wb=16) == rk.RK_ERR_WORKSPACE
+    lib.rk_model_destroy(h)
+    st, h32 = _create(_FakeCfg(dtype="f32"))
+    assert lib.rk_compression_damage(h32, ctypes.byref(batch), 50, 0, fake, 20, 10, fake, big, fake, None, fake, big,
+                                     None) == rk.RK_ERR_UNSUPPORTED
+    lib.rk_model_destroy(h32)
