@@ -15,6 +15,7 @@ roofline of the dominant kernel measured live with HIP events over the timed
 steps, and the CPU oracle's rate on a bounded sample of the same workload.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+                    [--window N | --snapkv | --damage]
 """
 from __future__ import annotations
 
@@ -300,6 +301,136 @@ def snapkv_main(args):
     print(json.dumps(res), flush=True)
 
 
+DMG_RHO, DMG_OBS = 0.2, 32
+
+
+def cpu_baseline_damage(w, W, toks, P: int, b: int):
+    """Oracle isolated compression damage of sequence 0 (window reference
+    included), every layer, b retained prompt positions per KV head drawn by
+    fixtures (the oracle's cost does not depend on which positions are kept)."""
+    import fixtures as F
+    from oracle import damage as OD
+    from oracle import model as OM
+    from oracle import profile as OPR
+    from tests.gpu_helpers import f32_weights  # noqa: E402
+    cfg = w.model
+    m = OM.Model(cfg, f32_weights(cfg, W), np.float32)
+    t = toks[0]
+    pos = F.random_keep(1, cfg.n_kv_heads, P, b, seed_id=5)[0]
+    t0 = time.perf_counter()
+    ws = OPR.window_clean_state(m, t, P)
+    for l in range(cfg.n_layers):
+        OD.damage_layer(m, ws, l, list(pos))
+    dt = time.perf_counter() - t0
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max(int(x.get("num_threads", 1)) for x in threadpool_info()) if threadpool_info() else os.cpu_count()
+    except Exception:
+        cores = os.cpu_count()
+    n = (len(t) - P) * cfg.n_layers
+    return {"value": n / dt, "unit": "window token-layers/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"sequence 0 (prompt {P}, window {len(t) - P}), all {cfg.n_layers} layers, {b} kept positions "
+                      f"per KV head, float32 oracle: {dt:.1f} s (window reference included)"}
+
+
+def damage_main(args):
+    """Isolated single-layer compression damage (Section 2) of every layer on the
+    GPT-2-small-shaped workload: the prompt [0, P) of each sequence compressed by
+    SnapKV with the same budget b at every layer, one layer at a time, the window
+    [P, T) evaluated against the caches; then Spearman's rho of the damage profile
+    against the cached-window sensitivity profile.  One step = the damage of every
+    layer for all sequences plus the rank correlation."""
+    import torch
+    import fixtures as F
+    import paper_2608_08684_amd as rk
+    from tests.gpu_helpers import make_batch, upload_weights
+    w = F.get_workload(args.workload)
+    cfg = w.model
+    L, Hkv, dh = cfg.n_layers, cfg.n_kv_heads, cfg.head_dim
+    window = args.window if args.window > 0 else 256
+    lens = w.lengths()
+    P = min(lens) - window
+    b = int(round(DMG_RHO * P))
+    t0 = time.perf_counter()
+    W = F.make_weights(cfg)
+    model = rk.Model(cfg, upload_weights(cfg, W))
+    toks = F.make_tokens(w)
+    batch = make_batch(toks)
+    rows = batch.rows
+    # the prompts' caches and the window reference
+    state = torch.empty(model.window_state_size(rows), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(model.workspace_size(rows, 1, rk.RK_FLAG_CACHED_WINDOW), dtype=torch.uint8, device="cuda")
+    model.window_reference(batch, P, state, ws)
+    # SnapKV on the prompts with the same budget at every layer (the base compressor)
+    pb = make_batch([t[:P] for t in toks])
+    sst = torch.empty(model.snapkv_state_size(pb.rows, pb.n_seqs, DMG_OBS), dtype=torch.uint8, device="cuda")
+    sws = torch.empty(model.snapkv_workspace_size(pb.rows, pb.n_seqs, DMG_OBS), dtype=torch.uint8, device="cuda")
+    model.snapkv_prefill(pb, DMG_OBS, sst, sws)
+    budgets = np.full((pb.n_seqs, L), b, dtype=np.int64)
+    total, _ = rk.snapkv_layout(pb, L, budgets)
+    pos = torch.empty(Hkv * total, dtype=torch.int32, device="cuda")
+    ko = torch.empty(Hkv * total, dh, dtype=torch.int16, device="cuda")
+    vo = torch.empty_like(ko)
+    model.snapkv_compress(pb, budgets, sst, pos, ko, vo, sws, obs_window=DMG_OBS)
+    del sst, sws, ko, vo
+    # the cached-window sensitivity profile the damage is ranked against
+    s_out = torch.empty(1, L, dtype=torch.float32, device="cuda")
+    pws = torch.empty(model.workspace_size(rows, L, rk.RK_WS_CLEAN_STATE | rk.RK_FLAG_CACHED_WINDOW),
+                      dtype=torch.uint8, device="cuda")
+    model.sensitivity_profile(batch, list(range(L)), [max(w.alphas)], s_out, pws, rows, L, window_start=P,
+                              flags=rk.RK_FLAG_CACHED_WINDOW)
+    s_prof = s_out.cpu().numpy()[0].astype(np.float64)
+    del pws
+    d_all = torch.empty(L, batch.n_seqs, dtype=torch.float32, device="cuda")
+    log(f"damage inputs ready in {time.perf_counter() - t0:.1f} s (prompt {P}, window {window}, b = {b})")
+
+    def step():
+        for l in range(L):
+            model.compression_damage(batch, P, l, pos[l * Hkv * b:], b, state, d_all[l], ws,
+                                     seq_stride=L * Hkv * b)
+        D = d_all.mean(dim=1).cpu().numpy().astype(np.float64)     # synchronises
+        return D, rk.spearman(s_prof, D)
+
+    for _ in range(args.warmup):
+        rk.timing_begin(args.family)
+        step()
+        rk.timing_end()
+    torch.cuda.synchronize()
+    launches, fam_ms = 0, 0.0
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        rk.timing_begin(args.family)
+        D, rho = step()
+        n, ms = rk.timing_end()
+        launches += n
+        fam_ms += ms
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    eval_rows = sum(T - P for T in lens)
+    value = eval_rows * L / (ms_per_step / 1e3)
+    avg = fam_ms / max(launches, 1)
+    flops = family_flops(args.family, cfg, eval_rows, 1)
+    achieved = flops / (avg / 1e3) / 1e12
+    roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": args.family,
+            "launches": launches, "avg_ms": round(avg, 4), "flop_per_launch": flops}
+    log(f"{args.family}: {launches} launches, avg {avg:.4f} ms, {achieved:.1f} TFLOP/s; D = {D}; rho = {rho:.3f}")
+    res = {
+        "metric": "window token-layers/s (isolated single-layer compression damage)",
+        "value": round(value, 1), "unit": "token-layers/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (random-init N(0,0.02) weights, Zipf(1.1) tokens)",
+        "config": {"workload": f"{w.name} compression damage: {L}L d{cfg.d_model} {cfg.n_heads}x{dh}; "
+                               f"{batch.n_seqs}x{max(lens)} tokens, prompt {P} + window {window}; SnapKV b = {b} "
+                               f"(window {DMG_OBS}, max pooling 7) at one layer at a time",
+                   "spearman_rho": None if np.isnan(rho) else round(float(rho), 4)},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline_damage(w, W, toks, P, b)
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -315,6 +446,9 @@ def main():
                          "prefix (0: the resumed full-sequence profile)")
     ap.add_argument("--snapkv", action="store_true",
                     help="time the SnapKV selection with per-layer budgets (the budgets' consumer) instead")
+    ap.add_argument("--damage", action="store_true",
+                    help="time the isolated single-layer compression damage of every layer instead (prompt = all "
+                         "but the last WINDOW tokens, default 256)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (calibrates HBM byte counters)")
     ap.add_argument("--derive-traffic", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
@@ -342,6 +476,9 @@ def main():
         return
     if args.snapkv:
         snapkv_main(args)
+        return
+    if args.damage:
+        damage_main(args)
         return
     import fixtures as F
     import paper_2608_08684_amd as rk
