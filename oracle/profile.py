@@ -16,6 +16,15 @@ Readings where the paper is silent: W_i is [window_start, T_i) (all positions by
 default); positions [protect_head, T_i - protect_tail) are eligible for noise (all
 by default); the same epsilon serves every alpha; epsilon is independent per
 (sequence, layer) and shared by the query heads of a KV head.
+
+The layer-local signal of the "w/o DS" ablation (Section 5, Table ablation) keeps
+the perturbation, the averaging and the allocation, and replaces the downstream
+response (the shift of the final predictive distribution) by a layer-local
+response score, which the paper does not define.  Reading taken here: the
+response of layer l itself, measured at its output before any later layer sees
+it, r_t = ||h~_{l+1,t} - h_{l+1,t}||^2 / ||h_{l+1,t}||^2 with h_{l+1} the clean
+output of block l and h~_{l+1} its output with the perturbed Values (a relative
+squared change: dimensionless, like the KL); 0 where h_{l+1,t} = 0.
 """
 from __future__ import annotations
 
@@ -101,24 +110,55 @@ def profile_layer(m: M.Model, st: M.CleanState, tokens: np.ndarray, seq: int, la
     return d, kl
 
 
+def local_response_rows(h_ref: np.ndarray, h_pert: np.ndarray) -> np.ndarray:
+    """Layer-local response per row: ||h_pert - h_ref||^2 / ||h_ref||^2 in float64
+    (0 for a zero reference row)."""
+    a = np.asarray(h_ref, dtype=np.float64)
+    b = np.asarray(h_pert, dtype=np.float64)
+    num = np.sum((b - a) ** 2, axis=-1)
+    den = np.sum(a * a, axis=-1)
+    return np.where(den > 0, num / np.where(den > 0, den, 1.0), 0.0)
+
+
+def window_mean(x: np.ndarray, window_start: int) -> float:
+    w0 = min(max(window_start, 0), len(x))
+    return float(np.mean(x[w0:])) if w0 < len(x) else 0.0
+
+
+def local_profile_layer(m: M.Model, st: M.CleanState, tokens: np.ndarray, seq: int, layer: int,
+                        p: PerturbParams):
+    """Layer-local signal (the "w/o DS" ablation): (d^loc_{i,l}, r_t for every
+    position) from block l alone, run on the cached h_l with and without the
+    Value perturbation; nothing after block l is evaluated."""
+    pos = np.arange(len(tokens))
+    h_ref = M.block(m, layer, st.hs[layer], pos)
+    h_pert = M.block(m, layer, st.hs[layer], pos, _hook(m, seq, layer, len(tokens), p))
+    r = local_response_rows(h_ref, h_pert)
+    return window_mean(r, p.window_start), r
+
+
 def sensitivity_profile(m: M.Model, token_seqs: Sequence[np.ndarray], layers: Sequence[int],
                         alphas: Sequence[float], seed: int = 2, window_start: int = 0,
                         protect_head: int = 0, protect_tail: int = 0,
-                        seq_indices: Optional[Sequence[int]] = None) -> Dict[str, np.ndarray]:
+                        seq_indices: Optional[Sequence[int]] = None, signal: str = "downstream") -> Dict[str, np.ndarray]:
     """Algorithm 1, profiling half.  Returns s [n_alpha, |A|] and d [n_alpha, N, |A|].
 
     ``seq_indices`` gives each sequence's index i in the calibration set (it keys
-    the noise); by default 0..N-1."""
+    the noise); by default 0..N-1.  ``signal="local"`` takes the layer-local
+    response in place of the window KL (the "w/o DS" ablation)."""
+    if signal not in ("downstream", "local"):
+        raise ValueError(signal)
     N = len(token_seqs)
     if seq_indices is None:
         seq_indices = list(range(N))
     d = np.zeros((len(alphas), N, len(layers)), dtype=np.float64)
+    one = profile_layer if signal == "downstream" else local_profile_layer
     for n, toks in enumerate(token_seqs):
         st = M.clean_pass(m, toks)
         for a, alpha in enumerate(alphas):
             p = PerturbParams(alpha, seed, window_start, protect_head, protect_tail)
             for j, l in enumerate(layers):
-                d[a, n, j], _ = profile_layer(m, st, toks, seq_indices[n], l, p)
+                d[a, n, j], _ = one(m, st, toks, seq_indices[n], l, p)
     s = d.sum(axis=1) / N
     return {"s": s, "d": d}
 
@@ -180,19 +220,39 @@ def window_profile_layer(m: M.Model, ws: WindowState, seq: int, layer: int, p: P
     return float(np.mean(kl)), kl
 
 
+def window_local_profile_layer(m: M.Model, ws: WindowState, seq: int, layer: int, p: PerturbParams):
+    """Layer-local signal in the cached-window mode: (d^loc_{i,l}, r_t for t in
+    [P, T)) from block l alone on the window rows, against the intact cache and
+    against the cache with layer l's eligible prefix Values perturbed."""
+    c = m.cfg
+    P = ws.P
+    pos = np.arange(P, P + ws.hs[0].shape[0])
+    k_l, v_l = ws.kv[layer]
+    eps = value_noise(p.seed, seq, layer, c.n_kv_heads, np.arange(P), c.head_dim)
+    v_pert = perturb_values(v_l, p.alpha, eps, p.protect_head, P - p.protect_tail)
+    h_ref = M.block(m, layer, ws.hs[layer], pos, prefix_kv=(k_l, v_l))
+    h_pert = M.block(m, layer, ws.hs[layer], pos, prefix_kv=(k_l, v_pert))
+    r = local_response_rows(h_ref, h_pert)
+    return float(np.mean(r)), r
+
+
 def window_sensitivity_profile(m: M.Model, token_seqs: Sequence[np.ndarray], layers: Sequence[int],
                                alphas: Sequence[float], p: PerturbParams,
-                               seq_indices: Optional[Sequence[int]] = None) -> Dict[str, np.ndarray]:
+                               seq_indices: Optional[Sequence[int]] = None,
+                               signal: str = "downstream") -> Dict[str, np.ndarray]:
     """s_l (Eq. layer-sensitivity) in the cached-window mode; the same shapes as
     ``sensitivity_profile``.  Every sequence needs T_i > window_start."""
+    if signal not in ("downstream", "local"):
+        raise ValueError(signal)
     N, nA = len(token_seqs), len(layers)
     if seq_indices is None:
         seq_indices = list(range(N))
+    one = window_profile_layer if signal == "downstream" else window_local_profile_layer
     d = np.zeros((len(alphas), N, nA), dtype=np.float64)
     for n, toks in enumerate(token_seqs):
         ws = window_clean_state(m, toks, p.window_start)
         for a, alpha in enumerate(alphas):
             q = dataclasses.replace(p, alpha=float(alpha))
             for j, l in enumerate(layers):
-                d[a, n, j] = window_profile_layer(m, ws, seq_indices[n], l, q)[0]
+                d[a, n, j] = one(m, ws, seq_indices[n], l, q)[0]
     return {"s": d.sum(axis=1) / N, "d": d}
