@@ -129,10 +129,11 @@ def cpu_baseline_window(w, W, toks, window: int):
                       f"oracle: {dt:.1f} s for {n} window token-layers (prefix prefill and reference included)"}
 
 
-def cpu_baseline(w, W, toks, prefix: int = 2048):
+def cpu_baseline(w, W, toks, prefix: int = 2048, local: bool = False):
     """Oracle (as it stands) on a bounded sample: the first `prefix` tokens of
     sequence 0 (a causal prefix computes exactly the same per-position values),
-    every layer, the largest alpha, clean pass included."""
+    every layer, the largest alpha, clean pass included (the layer-local signal
+    with `local`)."""
     from oracle import model as OM
     from oracle import profile as OPR
     from tests.gpu_helpers import f32_weights  # noqa: E402  (exact fp32 view of the bf16 weights)
@@ -142,8 +143,9 @@ def cpu_baseline(w, W, toks, prefix: int = 2048):
     alpha = max(w.alphas)
     t0 = time.perf_counter()
     st = OM.clean_pass(m, t)
+    one = OPR.local_profile_layer if local else OPR.profile_layer
     for l in range(cfg.n_layers):
-        OPR.profile_layer(m, st, t, 0, l, OPR.PerturbParams(alpha))
+        one(m, st, t, 0, l, OPR.PerturbParams(alpha))
     dt = time.perf_counter() - t0
     try:
         from threadpoolctl import threadpool_info
@@ -152,8 +154,9 @@ def cpu_baseline(w, W, toks, prefix: int = 2048):
         cores = os.cpu_count()
     n = len(t) * cfg.n_layers
     return {"value": n / dt, "unit": "perturbed token-layers/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"first {len(t)} tokens of sequence 0, all {cfg.n_layers} layers, alpha={alpha}, float32 oracle: "
-                      f"{dt:.1f} s for {n} token-layers (clean pass included)"}
+            "sample": f"first {len(t)} tokens of sequence 0, all {cfg.n_layers} layers, alpha={alpha}, float32 oracle"
+                      f"{' (layer-local signal)' if local else ''}: {dt:.1f} s for {n} token-layers (clean pass "
+                      f"included)"}
 
 
 SNAP_WINDOW, SNAP_KERNEL, SNAP_RHO, SNAP_RATIO = 32, 7, 0.2, 2.0
@@ -441,6 +444,9 @@ def main():
     ap.add_argument("--family", default="gemm_gate_up", help="kernel family for the roofline figure")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying a HIP graph")
+    ap.add_argument("--signal", choices=("downstream", "local"), default="downstream",
+                    help="profile signal: the KL of the final distributions (the method) or the layer-local "
+                         "response of the perturbed block (the w/o DS ablation)")
     ap.add_argument("--window", type=int, default=0,
                     help="cached-window mode: evaluate the last WINDOW tokens of every sequence against the cached "
                          "prefix (0: the resumed full-sequence profile)")
@@ -499,11 +505,14 @@ def main():
     rows = batch.rows
     G = min(args.max_group, rk.RK_MAX_GROUP)
     window = int(args.window)
-    flags = (rk.RK_FLAG_CACHED_WINDOW if window > 0 else 0) | (0 if args.no_graph else rk.RK_FLAG_GRAPH)
+    local = args.signal == "local"
+    flags = ((rk.RK_FLAG_CACHED_WINDOW if window > 0 else 0) | (0 if args.no_graph else rk.RK_FLAG_GRAPH) |
+             (rk.RK_FLAG_LOCAL_SIGNAL if local else 0))
     P = min(w.lengths()) - window if window > 0 else 0
     if window > 0 and P < 1:
         raise SystemExit(f"--window {window} leaves no prefix in the shortest sequence")
-    ws = torch.empty(model.workspace_size(rows, G, rk.RK_WS_CLEAN_STATE | (flags & rk.RK_FLAG_CACHED_WINDOW)),
+    ws = torch.empty(model.workspace_size(rows, G, rk.RK_WS_CLEAN_STATE |
+                                          (flags & (rk.RK_FLAG_CACHED_WINDOW | rk.RK_FLAG_LOCAL_SIGNAL))),
                      dtype=torch.uint8, device="cuda")
     s_out = torch.empty(len(alphas), len(layers), dtype=torch.float32, device="cuda")
     d_out = torch.empty(len(alphas), batch.n_seqs, len(layers), dtype=torch.float32, device="cuda")
@@ -559,9 +568,13 @@ def main():
     log(f"{args.family}: {launches} launches, avg {fam_avg_ms:.4f} ms, {achieved:.1f} TFLOP/s")
 
     mode = "" if window == 0 else f"; cached window: prefix {P}, window {window} per sequence"
+    mode += "; layer-local signal (w/o DS ablation)" if local else ""
+    metric = ("perturbed token-layers/s (sensitivity-profile throughput)" if window == 0 else
+              "perturbed window token-layers/s (cached-window sensitivity-profile throughput)")
+    if local:
+        metric = metric.replace("sensitivity-profile", "layer-local-signal profile")
     res = {
-        "metric": ("perturbed token-layers/s (sensitivity-profile throughput)" if window == 0 else
-                   "perturbed window token-layers/s (cached-window sensitivity-profile throughput)"),
+        "metric": metric,
         "value": round(value, 1),
         "unit": "token-layers/s",
         "n_gpus": 1,
@@ -581,7 +594,10 @@ def main():
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(w, W, toks) if window == 0 else cpu_baseline_window(w, W, toks, window)
+        if window == 0:
+            res["cpu_baseline"] = cpu_baseline(w, W, toks, local=local)
+        elif not local:
+            res["cpu_baseline"] = cpu_baseline_window(w, W, toks, window)
     print(json.dumps(res), flush=True)
 
 

@@ -88,6 +88,17 @@ typedef enum {
                                         perturbed, every other cache stays frozen,
                                         and only the window is recomputed (see
                                         rk_window_reference).  bf16 models only.     */
+#define RK_FLAG_LOCAL_SIGNAL   0x10u /* the layer-local signal of the "w/o DS"
+                                        ablation (Section 5, Table ablation): the
+                                        same perturbation and averaging, but d_{i,l}
+                                        is the window mean of the response of block
+                                        l itself, r_t = ||h~_{l+1,t} - h_{l+1,t}||^2
+                                        / ||h_{l+1,t}||^2 (its output with and
+                                        without the perturbed Values; 0 for a zero
+                                        clean row), in place of the KL of the final
+                                        distributions.  No layer after l and no LM
+                                        head is evaluated.  Not combinable with
+                                        RK_FLAG_UNFUSED_KL.                          */
 
 /* Most sequences one batch (one call's rows) may hold. */
 #define RK_MAX_BATCH_SEQS 64
@@ -183,7 +194,9 @@ size_t rk_window_state_size(const rk_model *m, int64_t n_rows);
  * RK_F32 models).  Returns 0 for invalid arguments.                            */
 size_t rk_workspace_size(const rk_model *m, int64_t max_rows, int32_t max_group, uint32_t flags);
 /* (flags may also hold RK_FLAG_CACHED_WINDOW: room for one layer's perturbed
- * prefix Values, and, with RK_WS_CLEAN_STATE, a cached-window state.)          */
+ * prefix Values, and, with RK_WS_CLEAN_STATE, a cached-window state; and
+ * RK_FLAG_LOCAL_SIGNAL: room for the clean output of the last block, and none
+ * for LM-head partials or logits.)                                             */
 
 /* ---------------------------------------------------------------- profiling */
 
@@ -215,7 +228,10 @@ rk_status rk_window_reference(const rk_model *m, const rk_batch *batch, int32_t 
  * With RK_FLAG_CACHED_WINDOW in p->flags, clean_state is a state from
  * rk_window_reference with the same window_start, and kl_pos / logits_out hold
  * the window rows only (sum_i (T_i - window_start) rows, sequence by sequence);
- * RK_FLAG_FULL_RECOMPUTE is not available in that mode.                         */
+ * RK_FLAG_FULL_RECOMPUTE is not available in that mode.
+ * With RK_FLAG_LOCAL_SIGNAL, d_out and kl_pos hold the layer-local response
+ * instead of the KL, logits_out must be NULL, and the workspace size takes
+ * RK_FLAG_LOCAL_SIGNAL in place of RK_FLAG_UNFUSED_KL.                         */
 rk_status rk_profile_layer(const rk_model *m, const rk_batch *batch, int32_t layer, float alpha,
                            const rk_perturb_params *p, const void *clean_state, size_t clean_bytes,
                            float *d_out, float *kl_pos, float *logits_out,
@@ -231,9 +247,11 @@ rk_status rk_profile_layer(const rk_model *m, const rk_batch *batch, int32_t lay
  *   finite and >= 0.  s_out: DEVICE fp32 [n_alpha, n_A].  d_out: DEVICE fp32
  *   [n_alpha, N, n_A] or NULL.  One clean pass per batch serves every alpha.
  * max_group: passes scored per LM-head launch (1..16).
- * With RK_FLAG_CACHED_WINDOW the profile is that of the cached-window mode.
+ * With RK_FLAG_CACHED_WINDOW the profile is that of the cached-window mode;
+ * with RK_FLAG_LOCAL_SIGNAL, the layer-local signal of the ablation.
  * workspace must be at least rk_workspace_size(m, max_rows, max_group,
- * RK_WS_CLEAN_STATE | (p->flags & (RK_FLAG_UNFUSED_KL | RK_FLAG_CACHED_WINDOW))). */
+ * RK_WS_CLEAN_STATE | (p->flags & (RK_FLAG_UNFUSED_KL | RK_FLAG_CACHED_WINDOW |
+ * RK_FLAG_LOCAL_SIGNAL))).                                                     */
 rk_status rk_sensitivity_profile(const rk_model *m, const rk_batch *calib, const int32_t *layers,
                                  int32_t n_A, const float *alphas, int32_t n_alpha,
                                  const rk_perturb_params *p, int64_t max_rows, int32_t max_group,
@@ -363,7 +381,7 @@ rk_status rk_spearman(const double *x, const double *y, int32_t n, double *rho);
  * of that kernel family is bracketed by HIP events recorded on its launch stream
  * (families: "rmsnorm", "gemm_qkv", "noise", "attention", "gemm_o",
  * "gemm_gate_up", "gemm_down", "lm_lse", "lm_kl", "kl_logits", "lm_logits",
- * "snap_scores", "snap_select").
+ * "local", "snap_scores", "snap_select").
  * rk_timing_end waits for the recorded events, returns the number of launches
  * and their summed duration in milliseconds, and stops recording.  Host-side
  * state is process-wide; not for concurrent use from several threads.          */

@@ -26,7 +26,7 @@ from typing import Optional, Sequence
 import numpy as np
 
 __all__ = ["RKError", "load", "Model", "Batch", "layer_budgets", "timing_begin", "timing_end", "LIB_PATH", "RK_FLAG_FULL_RECOMPUTE",
-           "RK_FLAG_UNFUSED_KL", "RK_FLAG_CACHED_WINDOW", "RK_FLAG_GRAPH", "RK_WS_CLEAN_STATE", "RK_MAX_BATCH_SEQS", "RK_MAX_GROUP",
+           "RK_FLAG_UNFUSED_KL", "RK_FLAG_CACHED_WINDOW", "RK_FLAG_GRAPH", "RK_FLAG_LOCAL_SIGNAL", "RK_WS_CLEAN_STATE", "RK_MAX_BATCH_SEQS", "RK_MAX_GROUP",
            "RK_POOL_MAX", "RK_POOL_AVG", "RK_SNAPKV_MAX_PREFIX", "snapkv_layout", "spearman"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librk.so")
@@ -38,6 +38,7 @@ RK_FLAG_FULL_RECOMPUTE = 0x1
 RK_FLAG_UNFUSED_KL = 0x2
 RK_FLAG_CACHED_WINDOW = 0x4
 RK_FLAG_GRAPH = 0x8
+RK_FLAG_LOCAL_SIGNAL = 0x10
 RK_WS_CLEAN_STATE = 0x100
 RK_MAX_BATCH_SEQS = 64
 RK_MAX_GROUP = 16

@@ -97,7 +97,8 @@ static WinPlan win_plan(const rk_model* m, int64_t R) {
 }
 
 struct WsPlan {
-  size_t h, x, qkv, att, ff, xp, part, logits_c, logits_p, kl, rope, rope_pos, dbatch, sacc, vpert, cpre, clean, total;
+  size_t h, x, qkv, att, ff, xp, part, logits_c, logits_p, kl, rope, rope_pos, dbatch, sacc, vpert, cpre, hloc, clean,
+      total;
   bool unfused;
 };
 
@@ -107,7 +108,9 @@ static WsPlan ws_plan(const rk_model* m, int64_t R, int G, uint32_t flags) {
   const rk_model_config& c = m->cfg;
   const size_t a = act_bytes(m);
   WsPlan p;
-  p.unfused = !m->bf16 || (flags & RK_FLAG_UNFUSED_KL);
+  // the layer-local signal evaluates no LM head: no logits, no LM partials
+  const bool local = (flags & RK_FLAG_LOCAL_SIGNAL) != 0;
+  p.unfused = !local && (!m->bf16 || (flags & RK_FLAG_UNFUSED_KL));
   size_t o = 0;
   p.h = o;        o += align256((size_t)R * c.d_model * 4);
   const int64_t Rp = pad_rows(R);
@@ -117,7 +120,7 @@ static WsPlan ws_plan(const rk_model* m, int64_t R, int G, uint32_t flags) {
   p.ff = o;       o += align256((size_t)Rp * c.d_ff * a);
   p.xp = o;       o += align256((size_t)G * Rp * c.d_model * a);
   p.part = o;
-  if (m->bf16) {
+  if (m->bf16 && !local) {
     // lm_chunks(rows) * rows <= min(n_vt * 128 * n_tt, (2048 + n_tt) * 128) and
     // lm_kl_chunks(rows) * rows <= min(n_vt * 256 * n_tb, (1024 + n_tb) * 256) for rows <= R
     const size_t n_vt = c.vocab / 128, n_tt = (R + 127) / 128, n_tb = (R + 255) / 256;
@@ -138,6 +141,8 @@ static WsPlan ws_plan(const rk_model* m, int64_t R, int G, uint32_t flags) {
   if (flags & RK_FLAG_CACHED_WINDOW) o += align256((size_t)R * (kv_cols(m) / 2) * a);
   p.cpre = o;   // a compressed prompt cache (K and V columns)
   if (flags & RK_FLAG_CACHED_WINDOW) o += align256((size_t)R * kv_cols(m) * a);
+  p.hloc = o;  // the clean output of the last block (layer-local signal)
+  if (local) o += align256((size_t)R * c.d_model * 4);
   p.clean = o;
   if (flags & RK_WS_CLEAN_STATE)
     o += (flags & RK_FLAG_CACHED_WINDOW) ? win_plan(m, R).total : clean_plan(m, R).total;
@@ -152,6 +157,7 @@ struct Bufs {
   double* sacc;
   void* vpert;
   void* cpre;
+  float* hloc;
   char* clean;
 };
 
@@ -162,7 +168,8 @@ static Bufs carve(const WsPlan& p, void* ws) {
   u.xp = b + p.xp; u.part = (float2*)(b + p.part); u.logits_c = (float*)(b + p.logits_c);
   u.logits_p = (float*)(b + p.logits_p); u.kl = (float*)(b + p.kl); u.rope = (float2*)(b + p.rope);
   u.rope_pos = (int32_t*)(b + p.rope_pos);
-  u.dbatch = (float*)(b + p.dbatch); u.sacc = (double*)(b + p.sacc); u.vpert = b + p.vpert; u.cpre = b + p.cpre; u.clean = b + p.clean;
+  u.dbatch = (float*)(b + p.dbatch); u.sacc = (double*)(b + p.sacc); u.vpert = b + p.vpert; u.cpre = b + p.cpre;
+  u.hloc = (float*)(b + p.hloc); u.clean = b + p.clean;
   return u;
 }
 
@@ -298,31 +305,33 @@ static rk_status run_block(const rk_model* m, int l, const float* h_in, float* h
   return RK_OK;
 }
 
+// With h_last the last block's output is kept there; without lse the clean
+// log-sum-exp is not formed (the layer-local signal needs neither LM head).
 static rk_status reference_forward(const rk_model* m, const int32_t* tokens, const SeqTable& st, const Clean& cl,
-                                   const Bufs& b, hipStream_t s) {
+                                   const Bufs& b, hipStream_t s, float* h_last = nullptr, bool lse = true) {
   const rk_model_config& c = m->cfg;
   const int64_t R = st.rows, d = c.d_model;
+  float* last = h_last ? h_last : b.h;
   RK_TRY(launch_rope_table(b.rope, b.rope_pos, st, c.head_dim, c.rope_theta, s));
   RK_TRY(launch_embed(m->tok_emb, m->bf16, tokens, cl.h, (int)R, (int)d, s));
   for (int l = 0; l < c.n_layers; ++l) {
-    float* out = (l + 1 < c.n_layers) ? cl.h + (size_t)(l + 1) * R * d : b.h;
+    float* out = (l + 1 < c.n_layers) ? cl.h + (size_t)(l + 1) * R * d : last;
     rk_status e = run_block(m, l, cl.h + (size_t)l * R * d, out, b, st, nullptr, s);
     if (e != RK_OK) return e;
   }
-  RK_TRY(launch_rmsnorm(b.h, m->final_norm, cl.xf, m->bf16, (int)R, (int)d, c.rms_eps, s));
-  if (m->bf16) {
+  RK_TRY(launch_rmsnorm(last, m->final_norm, cl.xf, m->bf16, (int)R, (int)d, c.rms_eps, s));
+  if (m->bf16 && lse) {
     Timed t("lm_lse", s);
     RK_TRY(launch_lm_lse((const bf16_t*)cl.xf, (const bf16_t*)m->lm_head, (int)R, (int)d, c.vocab, b.part, cl.lse, s));
   }
   return RK_OK;
 }
 
-// PerturbedPredict up to the final normalised hidden state (written to xf_out).
-static rk_status perturbed_final(const rk_model* m, const int32_t* tokens, const SeqTable& st, const Clean& cl,
-                                 int layer, float alpha, const rk_perturb_params* p, void* xf_out, const Bufs& b,
-                                 hipStream_t s) {
-  const rk_model_config& c = m->cfg;
-  const int64_t R = st.rows, d = c.d_model;
+// Block `layer` with its Values perturbed, from the cached h_l (or from a
+// recomputation of the layers below it); the output is left in b.h.
+static rk_status perturbed_block(const rk_model* m, const int32_t* tokens, const SeqTable& st, const Clean& cl,
+                                 int layer, float alpha, const rk_perturb_params* p, const Bufs& b, hipStream_t s) {
+  const int64_t R = st.rows, d = m->cfg.d_model;
   const float* h_in = cl.h + (size_t)layer * R * d;
   if (p->flags & RK_FLAG_FULL_RECOMPUTE) {
     RK_TRY(launch_embed(m->tok_emb, m->bf16, tokens, b.h, (int)R, (int)d, s));
@@ -333,13 +342,38 @@ static rk_status perturbed_final(const rk_model* m, const int32_t* tokens, const
     h_in = b.h;
   }
   Noise nz{alpha, p};
-  rk_status e = run_block(m, layer, h_in, b.h, b, st, &nz, s);
+  return run_block(m, layer, h_in, b.h, b, st, &nz, s);
+}
+
+// PerturbedPredict up to the final normalised hidden state (written to xf_out).
+static rk_status perturbed_final(const rk_model* m, const int32_t* tokens, const SeqTable& st, const Clean& cl,
+                                 int layer, float alpha, const rk_perturb_params* p, void* xf_out, const Bufs& b,
+                                 hipStream_t s) {
+  const rk_model_config& c = m->cfg;
+  const int64_t R = st.rows, d = c.d_model;
+  rk_status e = perturbed_block(m, tokens, st, cl, layer, alpha, p, b, s);
   if (e != RK_OK) return e;
   for (int l = layer + 1; l < c.n_layers; ++l) {
     e = run_block(m, l, b.h, b.h, b, st, nullptr, s);
     if (e != RK_OK) return e;
   }
   RK_TRY(launch_rmsnorm(b.h, m->final_norm, xf_out, m->bf16, (int)R, (int)d, c.rms_eps, s));
+  return RK_OK;
+}
+
+// Layer-local signal of one pass ("w/o DS" ablation): block `layer` alone with
+// its Values perturbed, compared row by row with its clean output (the cached
+// input of the next block, or h_last after the last block): r_out[row] =
+// ||h~_{l+1} - h_{l+1}||^2 / ||h_{l+1}||^2.
+static rk_status local_pass(const rk_model* m, const int32_t* tokens, const SeqTable& st, const Clean& cl, int layer,
+                            float alpha, const rk_perturb_params* p, const float* h_last, float* r_out, const Bufs& b,
+                            hipStream_t s) {
+  const int64_t R = st.rows, d = m->cfg.d_model;
+  rk_status e = perturbed_block(m, tokens, st, cl, layer, alpha, p, b, s);
+  if (e != RK_OK) return e;
+  const float* ref = (layer + 1 < m->cfg.n_layers) ? cl.h + (size_t)(layer + 1) * R * d : h_last;
+  Timed t("local", s);
+  RK_TRY(launch_local_response(b.h, ref, (int)R, (int)d, r_out, s));
   return RK_OK;
 }
 
@@ -425,7 +459,8 @@ static KvPrefix cache_prefix(const rk_model* m, const Win& wn, const SeqTable& p
 // layer once and leave their K and V; the windows are then evaluated against the
 // intact cache, keeping each block's input, the final hidden state and A_t.
 static rk_status window_reference(const rk_model* m, const int32_t* tokens, const SeqTable& st, const SeqTable& pst,
-                                  const SeqTable& wst, const Win& wn, const Bufs& b, hipStream_t s) {
+                                  const SeqTable& wst, const Win& wn, const Bufs& b, hipStream_t s,
+                                  float* h_last = nullptr, bool lse = true) {
   const rk_model_config& c = m->cfg;
   const int64_t d = c.d_model, Rp = pst.rows, Rw = wst.rows, kvb = kv_cols(m) * act_bytes(m);
   const int P = pst.max_len;
@@ -439,11 +474,12 @@ static rk_status window_reference(const rk_model* m, const int32_t* tokens, cons
   RK_TRY(launch_embed_gather(m->tok_emb, m->bf16, tokens, st, wst, P, wn.w.h, (int)d, s));
   for (int l = 0; l < c.n_layers; ++l) {
     const KvPrefix pk = cache_prefix(m, wn, pst, l, nullptr);
-    float* out = (l + 1 < c.n_layers) ? wn.w.h + (size_t)(l + 1) * Rw * d : b.h;
+    float* out = (l + 1 < c.n_layers) ? wn.w.h + (size_t)(l + 1) * Rw * d : (h_last ? h_last : b.h);
     rk_status e = run_block(m, l, wn.w.h + (size_t)l * Rw * d, out, b, wst, nullptr, s, &pk);
     if (e != RK_OK) return e;
   }
-  RK_TRY(launch_rmsnorm(b.h, m->final_norm, wn.w.xf, m->bf16, (int)Rw, (int)d, c.rms_eps, s));
+  RK_TRY(launch_rmsnorm(h_last ? h_last : b.h, m->final_norm, wn.w.xf, m->bf16, (int)Rw, (int)d, c.rms_eps, s));
+  if (!lse) return RK_OK;
   Timed t("lm_lse", s);
   RK_TRY(launch_lm_lse((const bf16_t*)wn.w.xf, (const bf16_t*)m->lm_head, (int)Rw, (int)d, c.vocab, b.part,
                        wn.w.lse, s));
@@ -454,9 +490,9 @@ static rk_status window_reference(const rk_model* m, const int32_t* tokens, cons
 // Values get the noise (a copy: the cache itself stays clean), the window rows
 // resume from their input to that block and read the frozen caches above it.
 // The rotary table must hold the window positions.
-static rk_status window_perturbed_final(const rk_model* m, const SeqTable& pst, const SeqTable& wst, const Win& wn,
-                                        int layer, float alpha, const rk_perturb_params* p, void* xf_out,
-                                        const Bufs& b, hipStream_t s) {
+static rk_status window_perturbed_block(const rk_model* m, const SeqTable& pst, const SeqTable& wst, const Win& wn,
+                                        int layer, float alpha, const rk_perturb_params* p, const Bufs& b,
+                                        hipStream_t s) {
   const rk_model_config& c = m->cfg;
   const int64_t d = c.d_model, Rp = pst.rows, Rw = wst.rows, a = act_bytes(m), kc = kv_cols(m);
   const char* kv_l = (const char*)wn.kv + (size_t)layer * Rp * kc * a;
@@ -466,14 +502,37 @@ static rk_status window_perturbed_final(const rk_model* m, const SeqTable& pst, 
     RK_TRY(launch_value_noise(b.vpert, m->bf16, kc / 2, pst, c.n_kv_heads, c.head_dim, layer, alpha, p->seed,
                               p->protect_head, p->protect_tail, s));
   }
-  KvPrefix pk = cache_prefix(m, wn, pst, layer, b.vpert);
-  rk_status e = run_block(m, layer, wn.w.h + (size_t)layer * Rw * d, b.h, b, wst, nullptr, s, &pk);
+  const KvPrefix pk = cache_prefix(m, wn, pst, layer, b.vpert);
+  return run_block(m, layer, wn.w.h + (size_t)layer * Rw * d, b.h, b, wst, nullptr, s, &pk);
+}
+
+static rk_status window_perturbed_final(const rk_model* m, const SeqTable& pst, const SeqTable& wst, const Win& wn,
+                                        int layer, float alpha, const rk_perturb_params* p, void* xf_out,
+                                        const Bufs& b, hipStream_t s) {
+  const rk_model_config& c = m->cfg;
+  const int64_t d = c.d_model, Rw = wst.rows;
+  rk_status e = window_perturbed_block(m, pst, wst, wn, layer, alpha, p, b, s);
   if (e != RK_OK) return e;
   for (int l = layer + 1; l < c.n_layers; ++l) {
-    pk = cache_prefix(m, wn, pst, l, nullptr);
+    const KvPrefix pk = cache_prefix(m, wn, pst, l, nullptr);
     if ((e = run_block(m, l, b.h, b.h, b, wst, nullptr, s, &pk)) != RK_OK) return e;
   }
   RK_TRY(launch_rmsnorm(b.h, m->final_norm, xf_out, m->bf16, (int)Rw, (int)d, c.rms_eps, s));
+  return RK_OK;
+}
+
+// Layer-local signal of one cached-window pass: block `layer` on the window rows
+// against the cache with its prefix Values perturbed, compared with its output
+// against the intact cache (the next block's cached window input, or h_last).
+static rk_status window_local_pass(const rk_model* m, const SeqTable& pst, const SeqTable& wst, const Win& wn,
+                                   int layer, float alpha, const rk_perturb_params* p, const float* h_last,
+                                   float* r_out, const Bufs& b, hipStream_t s) {
+  const int64_t d = m->cfg.d_model, Rw = wst.rows;
+  rk_status e = window_perturbed_block(m, pst, wst, wn, layer, alpha, p, b, s);
+  if (e != RK_OK) return e;
+  const float* ref = (layer + 1 < m->cfg.n_layers) ? wn.w.h + (size_t)(layer + 1) * Rw * d : h_last;
+  Timed t("local", s);
+  RK_TRY(launch_local_response(b.h, ref, (int)Rw, (int)d, r_out, s));
   return RK_OK;
 }
 
@@ -544,8 +603,13 @@ static rk_status check_params(const rk_perturb_params* p) {
     set_error("window_start / protect_head / protect_tail must be >= 0");
     return RK_ERR_ARG;
   }
-  if (p->flags & ~(RK_FLAG_FULL_RECOMPUTE | RK_FLAG_UNFUSED_KL | RK_FLAG_CACHED_WINDOW | RK_FLAG_GRAPH)) {
+  if (p->flags & ~(RK_FLAG_FULL_RECOMPUTE | RK_FLAG_UNFUSED_KL | RK_FLAG_CACHED_WINDOW | RK_FLAG_GRAPH |
+                   RK_FLAG_LOCAL_SIGNAL)) {
     set_error("unknown flags");
+    return RK_ERR_ARG;
+  }
+  if ((p->flags & RK_FLAG_LOCAL_SIGNAL) && (p->flags & RK_FLAG_UNFUSED_KL)) {
+    set_error("RK_FLAG_LOCAL_SIGNAL evaluates no LM head (RK_FLAG_UNFUSED_KL does not apply)");
     return RK_ERR_ARG;
   }
   if ((p->flags & RK_FLAG_CACHED_WINDOW) && (p->flags & RK_FLAG_FULL_RECOMPUTE)) {
@@ -982,38 +1046,63 @@ rk_status rk_profile_layer(const rk_model* m, const rk_batch* batch, int32_t lay
   if (!(alpha >= 0.0f) || !isfinite(alpha)) { set_error("alpha must be finite and >= 0"); return RK_ERR_ARG; }
   SeqTable st;
   if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
-  const bool unfused = !m->bf16 || logits_out || (p->flags & RK_FLAG_UNFUSED_KL);
+  const bool local = (p->flags & RK_FLAG_LOCAL_SIGNAL) != 0;
+  if (local && logits_out) { set_error("RK_FLAG_LOCAL_SIGNAL produces no logits"); return RK_ERR_ARG; }
+  const bool unfused = !local && (!m->bf16 || logits_out || (p->flags & RK_FLAG_UNFUSED_KL));
+  const uint32_t wf = (unfused ? RK_FLAG_UNFUSED_KL : 0) | (local ? RK_FLAG_LOCAL_SIGNAL : 0);
+  const int L = m->cfg.n_layers;
+  const int64_t d = m->cfg.d_model;
   if (p->flags & RK_FLAG_CACHED_WINDOW) {
     if ((e = check_window_model(m)) != RK_OK) return e;
     SeqTable pst, wst;
     if ((e = window_tables(st, p->window_start, &pst, &wst)) != RK_OK) return e;
     if (clean_bytes < win_plan(m, st.rows).total) { set_error("window state too small"); return RK_ERR_WORKSPACE; }
-    const WsPlan wp = ws_plan(m, st.rows, 1, (unfused ? RK_FLAG_UNFUSED_KL : 0) | RK_FLAG_CACHED_WINDOW);
+    const WsPlan wp = ws_plan(m, st.rows, 1, wf | RK_FLAG_CACHED_WINDOW);
     if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
     const Bufs b = carve(wp, workspace);
     const Win wn = win_view(m, st.rows, clean_state);
     hipStream_t s = (hipStream_t)stream;
     RK_TRY(launch_rope_table(b.rope, b.rope_pos, wst, m->cfg.head_dim, m->cfg.rope_theta, s, p->window_start));
-    if ((e = window_perturbed_final(m, pst, wst, wn, layer, alpha, p, b.xp, b, s)) != RK_OK) return e;
     float* kl = kl_pos ? kl_pos : b.kl;
-    if (unfused && (e = clean_logits(m, wst, wn.w, b.logits_c, s)) != RK_OK) return e;
-    if ((e = score_group(m, wst, wn.w, b.xp, 1, unfused, logits_out ? logits_out : b.logits_p, kl, b, s)) != RK_OK)
-      return e;
+    if (local) {
+      const float* h_last = nullptr;
+      if (layer + 1 == L) {  // the state keeps no output of the last block: run it clean
+        const KvPrefix pk = cache_prefix(m, wn, pst, layer, nullptr);
+        if ((e = run_block(m, layer, wn.w.h + (size_t)layer * wst.rows * d, b.hloc, b, wst, nullptr, s, &pk)) != RK_OK)
+          return e;
+        h_last = b.hloc;
+      }
+      if ((e = window_local_pass(m, pst, wst, wn, layer, alpha, p, h_last, kl, b, s)) != RK_OK) return e;
+    } else {
+      if ((e = window_perturbed_final(m, pst, wst, wn, layer, alpha, p, b.xp, b, s)) != RK_OK) return e;
+      if (unfused && (e = clean_logits(m, wst, wn.w, b.logits_c, s)) != RK_OK) return e;
+      if ((e = score_group(m, wst, wn.w, b.xp, 1, unfused, logits_out ? logits_out : b.logits_p, kl, b, s)) != RK_OK)
+        return e;
+    }
     RK_TRY(launch_window_mean(kl, wst.rows, 1, wst, 0, d_out, s));
     return RK_OK;
   }
   if (clean_bytes < clean_plan(m, st.rows).total) { set_error("clean state too small"); return RK_ERR_WORKSPACE; }
-  const WsPlan wp = ws_plan(m, st.rows, 1, unfused ? RK_FLAG_UNFUSED_KL : 0);
+  const WsPlan wp = ws_plan(m, st.rows, 1, wf);
   if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
   const Bufs b = carve(wp, workspace);
   const Clean cl = clean_view(m, st.rows, clean_state);
   hipStream_t s = (hipStream_t)stream;
   RK_TRY(launch_rope_table(b.rope, b.rope_pos, st, m->cfg.head_dim, m->cfg.rope_theta, s));
-  if ((e = perturbed_final(m, batch->tokens, st, cl, layer, alpha, p, b.xp, b, s)) != RK_OK) return e;
   float* kl = kl_pos ? kl_pos : b.kl;
-  if (unfused && (e = clean_logits(m, st, cl, b.logits_c, s)) != RK_OK) return e;
-  if ((e = score_group(m, st, cl, b.xp, 1, unfused, logits_out ? logits_out : b.logits_p, kl, b, s)) != RK_OK)
-    return e;
+  if (local) {
+    const float* h_last = nullptr;
+    if (layer + 1 == L) {  // the clean state keeps no output of the last block: run it clean
+      if ((e = run_block(m, layer, cl.h + (size_t)layer * st.rows * d, b.hloc, b, st, nullptr, s)) != RK_OK) return e;
+      h_last = b.hloc;
+    }
+    if ((e = local_pass(m, batch->tokens, st, cl, layer, alpha, p, h_last, kl, b, s)) != RK_OK) return e;
+  } else {
+    if ((e = perturbed_final(m, batch->tokens, st, cl, layer, alpha, p, b.xp, b, s)) != RK_OK) return e;
+    if (unfused && (e = clean_logits(m, st, cl, b.logits_c, s)) != RK_OK) return e;
+    if ((e = score_group(m, st, cl, b.xp, 1, unfused, logits_out ? logits_out : b.logits_p, kl, b, s)) != RK_OK)
+      return e;
+  }
   RK_TRY(launch_window_mean(kl, st.rows, 1, st, p->window_start, d_out, s));
   return RK_OK;
 }
@@ -1050,10 +1139,12 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
       return RK_ERR_SHAPE;
     }
   }
-  const bool unfused = !m->bf16 || (p->flags & RK_FLAG_UNFUSED_KL);
+  const bool local = (p->flags & RK_FLAG_LOCAL_SIGNAL) != 0;
+  const bool unfused = !local && (!m->bf16 || (p->flags & RK_FLAG_UNFUSED_KL));
   const bool cw = (p->flags & RK_FLAG_CACHED_WINDOW) != 0;
   if (cw && (e = check_window_model(m)) != RK_OK) return e;
-  const uint32_t wflags = RK_WS_CLEAN_STATE | (unfused ? RK_FLAG_UNFUSED_KL : 0) | (cw ? RK_FLAG_CACHED_WINDOW : 0);
+  const uint32_t wflags = RK_WS_CLEAN_STATE | (unfused ? RK_FLAG_UNFUSED_KL : 0) | (cw ? RK_FLAG_CACHED_WINDOW : 0) |
+                          (local ? RK_FLAG_LOCAL_SIGNAL : 0);
   const WsPlan wp = ws_plan(m, max_rows, max_group, wflags);
   if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
 
@@ -1081,7 +1172,8 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
       SeqTable pst, wst;
       if ((e = window_tables(st, p->window_start, &pst, &wst)) != RK_OK) return e;
       const Win wn = win_view(m, R, b.clean);
-      if ((e = window_reference(m, tokens, st, pst, wst, wn, b, s)) != RK_OK) return e;
+      if ((e = window_reference(m, tokens, st, pst, wst, wn, b, s, local ? b.hloc : nullptr, !local)) != RK_OK)
+        return e;
       if (unfused && (e = clean_logits(m, wst, wn.w, b.logits_c, s)) != RK_OK) return e;
       const int64_t Rw = wst.rows;
       for (int g0 = 0; g0 < n_pass; g0 += max_group) {
@@ -1092,12 +1184,18 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
         pm.d_seq_stride = n_A;
         for (int k = 0; k < G; ++k) {
           const int idx = g0 + k, a = idx / n_A, j = idx % n_A;
-          void* xf = (char*)b.xp + (size_t)k * pad_rows(Rw) * m->cfg.d_model * act_bytes(m);
-          if ((e = window_perturbed_final(m, pst, wst, wn, layers[j], alphas[a], p, xf, b, s)) != RK_OK) return e;
+          if (local) {
+            if ((e = window_local_pass(m, pst, wst, wn, layers[j], alphas[a], p, b.hloc, b.kl + (size_t)k * Rw, b,
+                                       s)) != RK_OK)
+              return e;
+          } else {
+            void* xf = (char*)b.xp + (size_t)k * pad_rows(Rw) * m->cfg.d_model * act_bytes(m);
+            if ((e = window_perturbed_final(m, pst, wst, wn, layers[j], alphas[a], p, xf, b, s)) != RK_OK) return e;
+          }
           pm.d_base[k] = (int64_t)a * N * n_A + j;
           pm.s_index[k] = a * n_A + j;
         }
-        if ((e = score_group(m, wst, wn.w, b.xp, G, unfused, b.logits_p, b.kl, b, s)) != RK_OK) return e;
+        if (!local && (e = score_group(m, wst, wn.w, b.xp, G, unfused, b.logits_p, b.kl, b, s)) != RK_OK) return e;
         RK_TRY(launch_window_mean(b.kl, Rw, G, wst, 0, b.dbatch, s));
         RK_TRY(launch_accumulate(b.dbatch, st.n, pm, d_out, b.sacc, s));
       }
@@ -1105,7 +1203,7 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
       continue;
     }
     const Clean cl = clean_view(m, R, b.clean);
-    if ((e = reference_forward(m, tokens, st, cl, b, s)) != RK_OK) return e;
+    if ((e = reference_forward(m, tokens, st, cl, b, s, local ? b.hloc : nullptr, !local)) != RK_OK) return e;
     if (unfused && (e = clean_logits(m, st, cl, b.logits_c, s)) != RK_OK) return e;
     for (int g0 = 0; g0 < n_pass; g0 += max_group) {
       const int G = (n_pass - g0 < max_group) ? n_pass - g0 : max_group;
@@ -1115,12 +1213,18 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
       pm.d_seq_stride = n_A;
       for (int k = 0; k < G; ++k) {
         const int idx = g0 + k, a = idx / n_A, j = idx % n_A;
-        void* xf = (char*)b.xp + (size_t)k * pad_rows(R) * m->cfg.d_model * act_bytes(m);
-        if ((e = perturbed_final(m, tokens, st, cl, layers[j], alphas[a], p, xf, b, s)) != RK_OK) return e;
+        if (local) {
+          if ((e = local_pass(m, tokens, st, cl, layers[j], alphas[a], p, b.hloc, b.kl + (size_t)k * R, b, s)) !=
+              RK_OK)
+            return e;
+        } else {
+          void* xf = (char*)b.xp + (size_t)k * pad_rows(R) * m->cfg.d_model * act_bytes(m);
+          if ((e = perturbed_final(m, tokens, st, cl, layers[j], alphas[a], p, xf, b, s)) != RK_OK) return e;
+        }
         pm.d_base[k] = (int64_t)a * N * n_A + j;
         pm.s_index[k] = a * n_A + j;
       }
-      if ((e = score_group(m, st, cl, b.xp, G, unfused, b.logits_p, b.kl, b, s)) != RK_OK) return e;
+      if (!local && (e = score_group(m, st, cl, b.xp, G, unfused, b.logits_p, b.kl, b, s)) != RK_OK) return e;
       RK_TRY(launch_window_mean(b.kl, R, G, st, p->window_start, b.dbatch, s));
       RK_TRY(launch_accumulate(b.dbatch, st.n, pm, d_out, b.sacc, s));
     }

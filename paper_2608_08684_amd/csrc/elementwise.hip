@@ -116,6 +116,42 @@ hipError_t launch_rmsnorm(const float* h, const float* g, void* out, bool out_bf
   return hipGetLastError();
 }
 
+// --------------------------------------------------------------------------- layer-local response
+// The layer-local signal of the "w/o DS" ablation: r[row] = ||hp - hc||^2 / ||hc||^2
+// for the perturbed and clean outputs of one block (fp32 rows of d values), 0 for a
+// zero clean row.  One wave per row; each lane sums its float4 columns in order,
+// then a fixed butterfly combines the lanes, so the result is repeatable.
+__global__ __launch_bounds__(256) void local_response_kernel(const float* __restrict__ hp,
+                                                             const float* __restrict__ hc, int rows, int d,
+                                                             float* __restrict__ r) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const float4* a = reinterpret_cast<const float4*>(hp + (int64_t)row * d);
+  const float4* c = reinterpret_cast<const float4*>(hc + (int64_t)row * d);
+  const int n4 = d >> 2;
+  float num = 0.f, den = 0.f;
+  for (int i = lane; i < n4; i += 64) {
+    const float4 x = a[i], y = c[i];
+    const float e0 = x.x - y.x, e1 = x.y - y.y, e2 = x.z - y.z, e3 = x.w - y.w;
+    num += e0 * e0 + e1 * e1 + e2 * e2 + e3 * e3;
+    den += y.x * y.x + y.y * y.y + y.z * y.z + y.w * y.w;
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    num += __shfl_xor(num, m, 64);
+    den += __shfl_xor(den, m, 64);
+  }
+  if (lane == 0) r[row] = den > 0.f ? num / den : 0.f;
+}
+
+hipError_t launch_local_response(const float* hp, const float* hc, int rows, int d, float* r, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (d & 3) return hipErrorInvalidValue;
+  local_response_kernel<<<(rows + 3) / 4, 256, 0, s>>>(hp, hc, rows, d, r);
+  return hipGetLastError();
+}
+
 // --------------------------------------------------------------------------- rotary table
 // tab[t * (dh/2) + j] = (cos, sin)(t * theta^(-2j/dh)) for t < max_len; the angle is
 // formed and reduced modulo 2*pi in double precision before the fp32 rounding.

@@ -134,6 +134,10 @@ hipError_t launch_lm_kl(const bf16_t* xc, const bf16_t* xp, int64_t pass_stride,
 hipError_t launch_kl_logits(const float* lc, const float* lp, int64_t pass_stride, int G, int rows, int vocab,
                             float* kl, hipStream_t s);
 
+// Layer-local response of one block: r[row] = ||hp[row] - hc[row]||^2 / ||hc[row]||^2
+// (fp32 rows of d values, d a multiple of 4; 0 for a zero clean row).
+hipError_t launch_local_response(const float* hp, const float* hc, int rows, int d, float* r, hipStream_t s);
+
 // dbatch[g * n_seqs + k] = mean of kl[g * kl_stride + r] over r in [off[k] + window_start, off[k+1]).
 hipError_t launch_window_mean(const float* kl, int64_t kl_stride, int G, const SeqTable& st, int window_start,
                               float* dbatch, hipStream_t s);

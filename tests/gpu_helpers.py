@@ -79,8 +79,11 @@ class Runner:
         import torch
         import paper_2608_08684_amd as rk
         flags = kw.pop("flags", 0)
-        unfused = want_logits or (flags & rk.RK_FLAG_UNFUSED_KL) or self.cfg.dtype == "f32"
-        ws = empty_bytes(self.model.workspace_size(batch.rows, 1, rk.RK_FLAG_UNFUSED_KL if unfused else 0))
+        local = bool(flags & rk.RK_FLAG_LOCAL_SIGNAL)
+        unfused = not local and (want_logits or (flags & rk.RK_FLAG_UNFUSED_KL) or self.cfg.dtype == "f32")
+        wf = rk.RK_FLAG_UNFUSED_KL if unfused else 0
+        ws = empty_bytes(self.model.workspace_size(batch.rows, 1, wf | (flags & (rk.RK_FLAG_LOCAL_SIGNAL |
+                                                                                 rk.RK_FLAG_CACHED_WINDOW))))
         d = torch.empty(batch.n_seqs, dtype=torch.float32, device="cuda")
         kl = torch.empty(batch.rows, dtype=torch.float32, device="cuda") if want_kl else None
         lg = torch.empty(batch.rows, self.cfg.vocab, dtype=torch.float32, device="cuda") if want_logits else None
@@ -97,7 +100,8 @@ class Runner:
         max_rows = max_rows or batch.rows
         flags = kw.get("flags", 0)
         ws = empty_bytes(self.model.workspace_size(
-            max_rows, max_group, rk.RK_WS_CLEAN_STATE | (flags & (rk.RK_FLAG_UNFUSED_KL | rk.RK_FLAG_CACHED_WINDOW))))
+            max_rows, max_group,
+            rk.RK_WS_CLEAN_STATE | (flags & (rk.RK_FLAG_UNFUSED_KL | rk.RK_FLAG_CACHED_WINDOW | rk.RK_FLAG_LOCAL_SIGNAL))))
         s = torch.empty(len(alphas), len(layers), dtype=torch.float32, device="cuda")
         d = torch.empty(len(alphas), batch.n_seqs, len(layers), dtype=torch.float32, device="cuda") if want_d else None
         self.model.sensitivity_profile(batch, layers, alphas, s, ws, max_rows, max_group, d_out=d, **kw)

@@ -349,3 +349,39 @@ def test_compression_damage_validates_before_launching():
     assert lib.rk_compression_damage(h32, ctypes.byref(batch), 50, 0, fake, 20, 10, fake, big, fake, None, fake, big,
                                      None) == rk.RK_ERR_UNSUPPORTED
     lib.rk_model_destroy(h32)
+
+
+def test_local_signal_flag_validates_before_launching():
+    """RK_FLAG_LOCAL_SIGNAL: no logits, not with the unfused-KL flag, its own
+    workspace size (the last block's clean output, no LM-head partials)."""
+    lib = rk.load()
+    st, h = _create(_FakeCfg())
+    assert st == rk.RK_OK
+    fake = ctypes.c_void_p(0x1000)
+    offs = np.array([0, 100, 250], dtype=np.int64)
+    batch = rk._Batch(fake, offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 2, 0)
+    big = 1 << 40
+    loc = rk._Params(2, 0, 0, 0, rk.RK_FLAG_LOCAL_SIGNAL)
+    both = rk._Params(2, 0, 0, 0, rk.RK_FLAG_LOCAL_SIGNAL | rk.RK_FLAG_UNFUSED_KL)
+    # logits requested with the local signal
+    assert lib.rk_profile_layer(h, ctypes.byref(batch), 0, 0.1, ctypes.byref(loc), fake, big, fake, None, fake,
+                                fake, big, None) == rk.RK_ERR_ARG
+    assert lib.rk_profile_layer(h, ctypes.byref(batch), 0, 0.1, ctypes.byref(both), fake, big, fake, None, None,
+                                fake, big, None) == rk.RK_ERR_ARG
+    lay = (ctypes.c_int32 * 2)(0, 1)
+    alp = (ctypes.c_float * 1)(0.1)
+    assert lib.rk_sensitivity_profile(h, ctypes.byref(batch), lay, 2, alp, 1, ctypes.byref(both), 1000, 2, fake,
+                                      None, fake, big, None) == rk.RK_ERR_ARG
+    # the local plan drops the LM-head partials and adds one fp32 row block
+    R, d = 250, _FakeCfg().d_model
+    s_kl = lib.rk_workspace_size(h, R, 4, 0)
+    s_loc = lib.rk_workspace_size(h, R, 4, rk.RK_FLAG_LOCAL_SIGNAL)
+    assert s_loc > 0 and s_loc != s_kl
+    need = lib.rk_workspace_size(h, R, 1, rk.RK_FLAG_LOCAL_SIGNAL)
+    assert lib.rk_profile_layer(h, ctypes.byref(batch), 0, 0.1, ctypes.byref(loc), fake, big, fake, None, None,
+                                fake, need - 1, None) == rk.RK_ERR_WORKSPACE
+    need_p = lib.rk_workspace_size(h, 1000, 2, rk.RK_WS_CLEAN_STATE | rk.RK_FLAG_LOCAL_SIGNAL)
+    assert lib.rk_sensitivity_profile(h, ctypes.byref(batch), lay, 2, alp, 1, ctypes.byref(loc), 1000, 2, fake,
+                                      None, fake, need_p - 1, None) == rk.RK_ERR_WORKSPACE
+    assert need_p >= need + R * d * 4
+    lib.rk_model_destroy(h)

@@ -42,8 +42,9 @@ class WindowRunner(Runner):
         import torch
         import paper_2608_08684_amd as rk
         flags = rk.RK_FLAG_CACHED_WINDOW | kw.pop("flags", 0)
-        unfused = want_logits or (flags & rk.RK_FLAG_UNFUSED_KL)
-        wflags = rk.RK_FLAG_CACHED_WINDOW | (rk.RK_FLAG_UNFUSED_KL if unfused else 0)
+        local = flags & rk.RK_FLAG_LOCAL_SIGNAL
+        unfused = not local and (want_logits or (flags & rk.RK_FLAG_UNFUSED_KL))
+        wflags = rk.RK_FLAG_CACHED_WINDOW | (rk.RK_FLAG_UNFUSED_KL if unfused else 0) | local
         ws = empty_bytes(self.model.workspace_size(batch.rows, 1, wflags))
         Rw = batch.rows - batch.n_seqs * P
         d = torch.empty(batch.n_seqs, dtype=torch.float32, device="cuda")
