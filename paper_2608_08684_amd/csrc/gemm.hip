@@ -191,195 +191,249 @@ __device__ __forceinline__ int b_row(int bn, int n, int d_ff) {
   return bn * 128 + n;
 }
 
-// --------------------------------------------------------------------------- bf16 MFMA kernel
-// PD: distance in tile columns between the two values an epilogue combines (a
-// rotary pair, gate/up); wave wn's two 32-column blocks are c and c + PD with
-// c = (wn / (PD/32)) * 2 PD + (wn % (PD/32)) * 32, so each lane holds both
-// values in registers.  PD = 32 is the plain layout (wave wn: columns 64 wn ..).
-// Waves with three column blocks (NI = 3) take the plain layout, and paired
-// epilogues then combine their values from the staged fp32 tile instead.
-template <int BM, int BN, int BK, int NWM, int NWN, int STAGES, int PD, class E, bool SWIGLU>
-__global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t* __restrict__ A, int64_t lda,
-                                                                  const bf16_t* __restrict__ B, int64_t ldb, int M,
-                                                                  int K, int d_ff, int n_bn, int group_m, E e) {
-  constexpr int NW = NWM * NWN, NT = 64 * NW;
-  constexpr int WTM = BM / NWM, WTN = BN / NWN;   // wave tile
-  constexpr int MI = WTM / 32, NI = WTN / 32;     // 32x32 blocks per wave
-  constexpr int CH = BK / 8;                      // 16-byte chunks per tile row
-  constexpr int AS = BM * CH, BS = BN * CH;       // 16-byte slots per stage
-  constexpr int PIPE = STAGES * (AS + BS);
-  constexpr bool REG_PAIR = E::kPaired && NI == 2;   // pairs combined in registers
-  static_assert((NI == 2 && BN % (2 * PD) == 0 && PD % 32 == 0) || (NI == 3 && PD == 32), "column blocks");
-  static_assert(!SWIGLU || REG_PAIR, "SwiGLU tiles pair gate and up in registers");
+// --------------------------------------------------------------------------- bf16 MFMA kernels
+// Wave layout.  PD: distance in tile columns between the two values an epilogue
+// combines (a rotary pair, gate/up).  A wave with NI = 2 P column blocks (P = 1 or
+// 2) holds P pairs: pair p is the blocks at c_p and c_p + PD, so each lane holds
+// both values in registers.  With PD >= 32 P the first members are contiguous, c_p
+// = wcol + 32 p with wcol = (wn / (PD / 32P)) * 2 PD + (wn % (PD / 32P)) * 32 P;
+// with PD = 32 < 32 P the pairs are adjacent, c_p = wcol + 64 p, wcol = 128 wn.
+// PD = 32 with P = 1 is the plain layout (wave wn: columns 64 wn ..).  Waves with
+// three column blocks (NI = 3) take the plain layout, and paired epilogues then
+// combine their values from the staged fp32 tile instead.
+template <int BM_, int BN_, int BK_, int NWM_, int NWN_, int PD_, class E>
+struct TileGeom {
+  static constexpr int BM = BM_, BN = BN_, BK = BK_, NWM = NWM_, NWN = NWN_, PD = PD_;
+  static constexpr int NW = NWM * NWN, NT = 64 * NW;
+  static constexpr int WTM = BM / NWM, WTN = BN / NWN;   // wave tile
+  static constexpr int MI = WTM / 32, NI = WTN / 32;     // 32x32 blocks per wave
+  static constexpr int CH = BK / 8;                      // 16-byte chunks per tile row
+  static constexpr int AS = BM * CH, BS = BN * CH;       // 16-byte slots of one stage's A and B tiles
+  static constexpr bool REG_PAIR = E::kPaired && (NI == 2 || NI == 4);   // pairs combined in registers
+  static constexpr int NP = NI == 3 ? 1 : NI / 2;                        // pairs per wave
+  static constexpr int PSTEP = PD >= 32 * NP ? 32 : 2 * PD;              // column step between pairs
+  static_assert(((NI == 2 || NI == 4) && BN % (2 * PD) == 0 && PD % 32 == 0 && (PD >= 32 * NP || PD == 32)) ||
+                    (NI == 3 && PD == 32),
+                "column blocks");
   // Epilogue staging: register-paired epilogues stage their outputs (type O), the
-  // others the fp32 accumulators; rows padded by 4 elements; in ROUNDS passes over
-  // the rows when the whole tile would not fit.
+  // others the fp32 accumulators; rows padded by 4 elements.
   using SO = typename std::conditional<REG_PAIR, typename E::stage_t, float>::type;
-  constexpr int OC = REG_PAIR ? E::out_cols(BN) : BN, SP = OC + 4;
-  constexpr int ROUNDS = BM * SP * (int)sizeof(SO) <= 136 * 1024 ? 1 : (BM * SP * (int)sizeof(SO) <= 272 * 1024 ? 2 : 4);
-  static_assert(MI % ROUNDS == 0, "staging rounds split each wave's rows evenly");
-  constexpr int STG = (BM / ROUNDS) * SP * (int)sizeof(SO) / 16;
-  static_assert(PIPE * 16 <= 160 * 1024 && STG * 16 <= 160 * 1024, "LDS");
-  // DMA instructions per thread and stage (A tile, then B tile or its gate and up halves)
-  constexpr int NL = (BM * CH + BN * CH) / (64 * NW);
-  static_assert(STAGES >= 2 && (STAGES - 2) * NL < 16, "ring depth");
-  __shared__ __attribute__((aligned(16))) v4u smem[PIPE > STG ? PIPE : STG];
-  v4u* As = smem;
-  v4u* Bs = smem + STAGES * AS;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31;
-  const int wm = w / NWN, wn = w % NWN;
-  // tile column of column block ni
-  const int wcol = NI == 2 ? (wn / (PD / 32)) * (2 * PD) + (wn % (PD / 32)) * 32 : wn * WTN;
-  auto colblk = [&](int ni) { return NI == 2 ? wcol + ni * PD : wcol + ni * 32; };
-  int bm_, bn;
-  xcd_tile((int)blockIdx.x, (M + BM - 1) / BM, n_bn, group_m, &bm_, &bn);
-  const int m0 = bm_ * BM;
-
-  TileSrcT<BK, NW> sa, sb, su;
-  sa.init(A + (int64_t)m0 * lda, lda, w, lane);
-  if (SWIGLU) {
-    sb.init(B + (int64_t)bn * (BN / 2) * ldb, ldb, w, lane);
-    su.init(B + ((int64_t)d_ff + (int64_t)bn * (BN / 2)) * ldb, ldb, w, lane);
-  } else {
-    sb.init(B + (int64_t)bn * BN * ldb, ldb, w, lane);
+  static constexpr int OC = REG_PAIR ? E::out_cols(BN) : BN, SP = OC + 4;
+  static constexpr int ROW_BYTES = SP * (int)sizeof(SO);
+  // fewest staging rounds (1, 2 or 4, each a whole number of every wave's 32-row
+  // blocks) whose rows fit in `bytes`; 0 if none does
+  static constexpr int rounds_for(int bytes) {
+    return BM * ROW_BYTES <= bytes                        ? 1
+           : (MI % 2 == 0 && BM / 2 * ROW_BYTES <= bytes) ? 2
+           : (MI % 4 == 0 && BM / 4 * ROW_BYTES <= bytes) ? 4
+                                                          : 0;
   }
-  // The NL copy instructions of one stage, numbered: A rounds, then B rounds (for
-  // SwiGLU: gate rounds, then up rounds).  They are spread over the k-slices of
-  // the previous k-step so the vector memory pipe never holds a wave back for long.
-  constexpr int NA = BM * CH / (64 * NW), NB = BN * CH / (64 * NW);
-  auto issue_one = [&](int kt, int stage, int j) {
-    if (j < NA) {
-      sa.load_round(kt, j, As + stage * AS, w);
-    } else if (SWIGLU) {
-      const int jb = j - NA;
-      if (jb < NB / 2) sb.load_round(kt, jb, Bs + stage * BS, w);
-      else su.load_round(kt, jb - NB / 2, Bs + stage * BS + (BN / 2) * CH, w);
+  // copy instructions per thread and stage (A tile, then B tile or its gate and up halves)
+  static constexpr int NA = BM * CH / (64 * NW), NB = BN * CH / (64 * NW), NL = NA + NB;
+  static constexpr int NKS = BK / 16;   // k-slices per k-step
+  static __device__ __forceinline__ int wave_col(int wn) {
+    return NI == 3 ? wn * WTN
+                   : (PD >= 32 * NP ? (wn / (PD / (32 * NP))) * (2 * PD) + (wn % (PD / (32 * NP))) * (32 * NP)
+                                    : wn * WTN);
+  }
+  // tile column of column block ni (blocks ni < NP: first members, ni >= NP: partners)
+  static __device__ __forceinline__ int colblk(int wcol, int ni) {
+    return NI == 3 ? wcol + ni * 32 : wcol + (ni % NP) * PSTEP + (ni / NP) * PD;
+  }
+};
+
+// The global -> LDS copy sources of one tile: A rows m0.., B rows (or gate and up
+// rows) of column block bn.
+template <class G, bool SWIGLU>
+struct TileCopies {
+  TileSrcT<G::BK, G::NW> sa, sb, su;
+  __device__ __forceinline__ void init(const bf16_t* A, int64_t lda, const bf16_t* B, int64_t ldb, int d_ff, int m0,
+                                       int bn, int w, int lane) {
+    sa.init(A + (int64_t)m0 * lda, lda, w, lane);
+    if (SWIGLU) {
+      sb.init(B + (int64_t)bn * (G::BN / 2) * ldb, ldb, w, lane);
+      su.init(B + ((int64_t)d_ff + (int64_t)bn * (G::BN / 2)) * ldb, ldb, w, lane);
     } else {
-      sb.load_round(kt, j - NA, Bs + stage * BS, w);
+      sb.init(B + (int64_t)bn * G::BN * ldb, ldb, w, lane);
     }
-  };
-  auto issue = [&](int kt, int stage) {
-#pragma unroll
-    for (int j = 0; j < NL; ++j) issue_one(kt, stage, j);
-  };
-  constexpr int NKS = BK / 16;                       // k-slices per k-step
-  constexpr int PER = (NL + NKS - 1) / NKS;          // copies issued per k-slice
+  }
+  // copy j (of NL) of k-step kt into the stage whose A tile is at As and B tile at Bs
+  __device__ __forceinline__ void issue_one(int kt, v4u* As, v4u* Bs, int j, int w) const {
+    if (j < G::NA) {
+      sa.load_round(kt, j, As, w);
+    } else if (SWIGLU) {
+      const int jb = j - G::NA;
+      if (jb < G::NB / 2) sb.load_round(kt, jb, Bs, w);
+      else su.load_round(kt, jb - G::NB / 2, Bs + (G::BN / 2) * G::CH, w);
+    } else {
+      sb.load_round(kt, j - G::NA, Bs, w);
+    }
+  }
+};
 
-  f32x16_t acc[MI][NI];
+// One k-step from the stage (At, Bt): fragments double-buffered in registers; the
+// LDS reads of k-slice ks + 1 and this k-step's share of the next copies
+// (copy(ks)) are issued ahead of the MFMAs of slice ks.
+template <class G, class Copy>
+__device__ __forceinline__ void mfma_kstep(f32x16_t (&acc)[G::MI][G::NI], const v4u* At, const v4u* Bt, int wm,
+                                           int wcol, int lane, const Copy& copy) {
+  constexpr int MI = G::MI, NI = G::NI, CH = G::CH;
+  const int l32 = lane & 31;
+  bf16x8_t af[2][MI], bfr[2][NI];
 #pragma unroll
-  for (int mi = 0; mi < MI; ++mi)
+  for (int mi = 0; mi < MI; ++mi) af[0][mi] = frag<CH>(At, wm * G::WTM + mi * 32 + l32, 0, lane);
 #pragma unroll
-    for (int ni = 0; ni < NI; ++ni)
+  for (int ni = 0; ni < NI; ++ni) bfr[0][ni] = frag<CH>(Bt, G::colblk(wcol, ni) + l32, 0, lane);
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int i = 0; i < 16; ++i) acc[mi][ni][i] = 0.f;
-
-  // Ring of STAGES LDS stages: k-step kt + STAGES - 1 is in flight while kt is consumed.
-  const int nk = K / BK;
+  for (int ks = 0; ks < G::NKS; ++ks) {
+    const int c = ks & 1;
+    if (ks + 1 < G::NKS) {
 #pragma unroll
-  for (int p = 0; p < STAGES - 1; ++p)
-    if (p < nk) issue(p, p);
-  // One k-step.  Fragments are double-buffered in registers: the LDS reads of
-  // k-slice ks+1 and this k-step's share of the copies for k-step kt + STAGES - 1
-  // are issued ahead of the MFMAs of slice ks.
-  auto kstep = [&](int kt, int cur, int nxt, bool copy, bool tail) {
-    if (!tail) wait_vmem_le<(STAGES - 2) * NL>(); else wait_vmem();
-    __syncthreads();   // k-step kt is in LDS for every wave; the slot of kt - 1 is free
-    const v4u* At = As + cur * AS;
-    const v4u* Bt = Bs + cur * BS;
-    bf16x8_t af[2][MI], bfr[2][NI];
+      for (int mi = 0; mi < MI; ++mi) af[c ^ 1][mi] = frag<CH>(At, wm * G::WTM + mi * 32 + l32, ks + 1, lane);
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi) af[0][mi] = frag<CH>(At, wm * WTM + mi * 32 + l32, 0, lane);
-#pragma unroll
-    for (int ni = 0; ni < NI; ++ni) bfr[0][ni] = frag<CH>(Bt, colblk(ni) + l32, 0, lane);
+      for (int ni = 0; ni < NI; ++ni) bfr[c ^ 1][ni] = frag<CH>(Bt, G::colblk(wcol, ni) + l32, ks + 1, lane);
+    }
+    copy(ks);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
-      const int c = ks & 1;
-      if (ks + 1 < NKS) {
+    for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-        for (int mi = 0; mi < MI; ++mi) af[c ^ 1][mi] = frag<CH>(At, wm * WTM + mi * 32 + l32, ks + 1, lane);
-#pragma unroll
-        for (int ni = 0; ni < NI; ++ni) bfr[c ^ 1][ni] = frag<CH>(Bt, colblk(ni) + l32, ks + 1, lane);
-      }
-      if (copy) {
-#pragma unroll
-        for (int j = ks * PER; j < (ks + 1) * PER; ++j)
-          if (j < NL) issue_one(kt + STAGES - 1, nxt, j);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < NI; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[c][ni], af[c][mi], acc[mi][ni], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  };
-  int cur = 0, nxt = STAGES - 1, kt = 0;
-  for (; kt + STAGES - 1 < nk; ++kt) {
-    kstep(kt, cur, nxt, true, false);
-    cur = cur == STAGES - 1 ? 0 : cur + 1;
-    nxt = nxt == STAGES - 1 ? 0 : nxt + 1;
+      for (int ni = 0; ni < NI; ++ni)
+        acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[c][ni], af[c][mi], acc[mi][ni], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
   }
-  for (; kt < nk; ++kt) {
-    kstep(kt, cur, nxt, false, true);
-    cur = cur == STAGES - 1 ? 0 : cur + 1;
-  }
-  // Epilogue.  The MFMAs above take B as the first operand, so acc[mi][ni] is the
-  // transposed 32x32 block: lane l holds row l % 32 and, in elements 4g..4g+3,
-  // the four consecutive columns 8 g + 4 (l / 32) .. +3 of the block.  Paired
-  // epilogues combine blocks 0 and 1 (columns c and c + PD) in registers; the
-  // results go through LDS so the global accesses are whole rows.
-  __syncthreads();   // the staging area overlaps the ring
-  SO* Cs = reinterpret_cast<SO*>(smem);
-  constexpr int WR = WTM / ROUNDS, MIR = MI / ROUNDS;   // rows per wave and round, blocks per round
+}
+
+// Epilogue of one tile, staged in ROUNDS passes through the LDS at `stage`.  The
+// MFMAs take B as the first operand, so acc[mi][ni] is the transposed 32x32 block:
+// lane l holds row l % 32 and, in elements 4g..4g+3, the four consecutive columns
+// 8 g + 4 (l / 32) .. +3 of the block.  Paired epilogues combine their two blocks
+// in registers; the results go through LDS so the global accesses are whole
+// rows.  The caller has freed the staging area (barrier) and must place a barrier
+// before the area is written again.
+template <class G, int ROUNDS, class E>
+__device__ __forceinline__ void tile_epilogue(const f32x16_t (&acc)[G::MI][G::NI], v4u* stage, int m0, int bn, int M,
+                                              const E& e, int wm, int wcol, int tid) {
+  using SO = typename G::SO;
+  constexpr int MI = G::MI, NI = G::NI, NP = G::NP, OC = G::OC, SP = G::SP, NT = G::NT, BN = G::BN;
+  static_assert(ROUNDS >= 1 && MI % ROUNDS == 0, "staging rounds split each wave's rows evenly");
+  const int lane = tid & 63, l32 = lane & 31;
+  SO* Cs = reinterpret_cast<SO*>(stage);
+  constexpr int WR = G::WTM / ROUNDS, MIR = MI / ROUNDS;   // rows per wave and round, blocks per round
 #pragma unroll
   for (int h = 0; h < ROUNDS; ++h) {
     if (h) __syncthreads();   // the previous round has been written out
 #pragma unroll
     for (int q = 0; q < MIR; ++q) {
       const int mi = h * MIR + q;
-      const int row = m0 + wm * WTM + mi * 32 + l32;
+      const int row = m0 + wm * G::WTM + mi * 32 + l32;
       SO* cs = Cs + (wm * WR + q * 32 + l32) * SP;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int q4 = g * 8 + (lane >> 5) * 4;
-        if constexpr (REG_PAIR) {
-          const int tc = wcol + q4;
-          const float4 x = make_float4(acc[mi][0][4 * g], acc[mi][0][4 * g + 1], acc[mi][0][4 * g + 2], acc[mi][0][4 * g + 3]);
-          const float4 y = make_float4(acc[mi][1][4 * g], acc[mi][1][4 * g + 1], acc[mi][1][4 * g + 2], acc[mi][1][4 * g + 3]);
-          float4 o0 = make_float4(0.f, 0.f, 0.f, 0.f), o1 = o0;
-          if (row < M) e.template pair<BN>(row, bn, tc, x, y, o0, o1);
-          store4(cs + tc, o0);
-          if constexpr (E::kOut == 2) store4(cs + tc + PD, o1);
+        if constexpr (G::REG_PAIR) {
+#pragma unroll
+          for (int pp = 0; pp < NP; ++pp) {
+            const int tc = G::colblk(wcol, pp) + q4;
+            const f32x16_t& ax = acc[mi][pp];
+            const f32x16_t& ay = acc[mi][pp + NP];
+            const float4 x = make_float4(ax[4 * g], ax[4 * g + 1], ax[4 * g + 2], ax[4 * g + 3]);
+            const float4 y = make_float4(ay[4 * g], ay[4 * g + 1], ay[4 * g + 2], ay[4 * g + 3]);
+            float4 o0 = make_float4(0.f, 0.f, 0.f, 0.f), o1 = o0;
+            if (row < M) e.template pair<BN>(row, bn, tc, x, y, o0, o1);
+            store4(cs + tc, o0);   // SwiGLU: gate columns [0, PD) are the output columns
+            if constexpr (E::kOut == 2) store4(cs + tc + G::PD, o1);
+          }
         } else {
 #pragma unroll
           for (int ni = 0; ni < NI; ++ni)
-            store4(cs + colblk(ni) + q4, make_float4(acc[mi][ni][4 * g], acc[mi][ni][4 * g + 1],
-                                                     acc[mi][ni][4 * g + 2], acc[mi][ni][4 * g + 3]));
+            store4(cs + G::colblk(wcol, ni) + q4, make_float4(acc[mi][ni][4 * g], acc[mi][ni][4 * g + 1],
+                                                              acc[mi][ni][4 * g + 2], acc[mi][ni][4 * g + 3]));
         }
       }
     }
     __syncthreads();
     // staged row r is tile row (r / WR) * WTM + h * WR + r % WR
-    if constexpr (REG_PAIR) {
+    if constexpr (G::REG_PAIR) {
       constexpr int CE = 16 / (int)sizeof(SO), CPR = OC / CE, RPP = NT / CPR;
       const int c = (tid % CPR) * CE;
       if (tid < RPP * CPR)
-        for (int r = tid / CPR; r < BM / ROUNDS; r += RPP) {
-          const int row = m0 + (r / WR) * WTM + h * WR + r % WR;
+        for (int r = tid / CPR; r < G::BM / ROUNDS; r += RPP) {
+          const int row = m0 + (r / WR) * G::WTM + h * WR + r % WR;
           if (row < M) copy16(e.out + (int64_t)row * e.ldo + (int64_t)bn * OC + c, Cs + r * SP + c);
         }
     } else {
       constexpr int TPR = E::out_cols(BN) / 8, RPP = NT / TPR;
       const int c0 = (tid % TPR) * 8;
       if (tid < RPP * TPR)
-        for (int r = tid / TPR; r < BM / ROUNDS; r += RPP) {
-          const int row = m0 + (r / WR) * WTM + h * WR + r % WR;
+        for (int r = tid / TPR; r < G::BM / ROUNDS; r += RPP) {
+          const int row = m0 + (r / WR) * G::WTM + h * WR + r % WR;
           if (row < M) e.template apply<BN>(row, bn, c0, Cs + r * SP);
         }
     }
   }
+}
+
+// One tile per workgroup, a ring of STAGES LDS stages: k-step kt + STAGES - 1 is in
+// flight while kt is consumed; the copies of a stage are spread over the k-slices
+// of the k-step before it.
+template <int BM, int BN, int BK, int NWM, int NWN, int STAGES, int PD, class E, bool SWIGLU>
+__global__ __launch_bounds__(64 * NWM * NWN) void gemm_bf16_kernel(const bf16_t* __restrict__ A, int64_t lda,
+                                                                  const bf16_t* __restrict__ B, int64_t ldb, int M,
+                                                                  int K, int d_ff, int n_bn, int group_m, E e) {
+  using G = TileGeom<BM, BN, BK, NWM, NWN, PD, E>;
+  constexpr int PIPE = STAGES * (G::AS + G::BS);
+  constexpr int ROUNDS = G::rounds_for(160 * 1024);
+  static_assert(ROUNDS > 0, "staging");
+  constexpr int STG = G::BM / ROUNDS * G::ROW_BYTES / 16;
+  static_assert(PIPE * 16 <= 160 * 1024 && STG * 16 <= 160 * 1024, "LDS");
+  static_assert(!SWIGLU || G::REG_PAIR, "SwiGLU tiles pair gate and up in registers");
+  constexpr int NL = G::NL;
+  static_assert(STAGES >= 2 && (STAGES - 2) * NL < 16, "ring depth");
+  __shared__ __attribute__((aligned(16))) v4u smem[PIPE > STG ? PIPE : STG];
+  v4u* As = smem;
+  v4u* Bs = smem + STAGES * G::AS;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wm = w / NWN, wn = w % NWN;
+  const int wcol = G::wave_col(wn);
+  int bm_, bn;
+  xcd_tile((int)blockIdx.x, (M + BM - 1) / BM, n_bn, group_m, &bm_, &bn);
+  const int m0 = bm_ * BM;
+  TileCopies<G, SWIGLU> src;
+  src.init(A, lda, B, ldb, d_ff, m0, bn, w, lane);
+  constexpr int PER = (NL + 1) / 2;   // copies issued per k-slice: over the first two slices
+
+  f32x16_t acc[G::MI][G::NI];
+#pragma unroll
+  for (int mi = 0; mi < G::MI; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < G::NI; ++ni)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[mi][ni][i] = 0.f;
+
+  const int nk = K / BK;
+#pragma unroll
+  for (int p = 0; p < STAGES - 1; ++p)
+    if (p < nk)
+#pragma unroll
+      for (int j = 0; j < NL; ++j) src.issue_one(p, As + p * G::AS, Bs + p * G::BS, j, w);
+  int cur = 0, nxt = STAGES - 1;
+  for (int kt = 0; kt < nk; ++kt) {
+    const bool copy = kt + STAGES - 1 < nk;
+    if (copy) wait_vmem_le<(STAGES - 2) * NL>(); else wait_vmem();
+    __syncthreads();   // k-step kt is in LDS for every wave; the slot of kt - 1 is free
+    mfma_kstep<G>(acc, As + cur * G::AS, Bs + cur * G::BS, wm, wcol, lane, [&](int ks) {
+      if (copy)
+#pragma unroll
+        for (int j = ks * PER; j < (ks + 1) * PER; ++j)
+          if (j < NL) src.issue_one(kt + STAGES - 1, As + nxt * G::AS, Bs + nxt * G::BS, j, w);
+    });
+    cur = cur == STAGES - 1 ? 0 : cur + 1;
+    nxt = nxt == STAGES - 1 ? 0 : nxt + 1;
+  }
+  __syncthreads();   // the staging area overlaps the ring
+  tile_epilogue<G, ROUNDS>(acc, smem, m0, bn, M, e, wm, wcol, tid);
 }
 
 // --------------------------------------------------------------------------- fp32 VALU kernel
@@ -484,7 +538,8 @@ static void go_pd(const GemmArgs& a, const E& e, hipStream_t s) {
 // the pair distance each epilogue needs (plain layout when it pairs nothing)
 template <int BM, int BN, int BK, int ST, class E, bool SWIGLU, int NWM = 2, int NWN = 2>
 static hipError_t go_bf16(const GemmArgs& a, const E& e, hipStream_t s) {
-  if constexpr (BN / NWN != 64) {
+  constexpr int WTN = BN / NWN;
+  if constexpr (WTN != 64 && WTN != 128) {   // three column blocks per wave: pairs via the staged tile
     if constexpr (SWIGLU) {
       return hipErrorInvalidValue;   // SwiGLU needs the paired layout
     } else {

@@ -31,11 +31,12 @@ constexpr int kBK = 64;  // default K elements per pipeline stage
 
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// s_waitcnt vmcnt(N) for N < 16 (gfx9 encoding; expcnt and lgkmcnt left at their maximum)
+// s_waitcnt vmcnt(N) for N < 64 (gfx9 encoding: vmcnt bits 3:0 and 15:14; expcnt and
+// lgkmcnt left at their maximum)
 template <int N>
 __device__ __forceinline__ void wait_vmem_le() {
-  static_assert(N >= 0 && N < 16, "vmcnt field");
-  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
 }
 
 // Chunk swizzle of a tile row with CH 16-byte chunks (CH = BK / 8).
