@@ -533,19 +533,23 @@ def main():
     # carry HIP events on the launch stream; with a replayed graph the events are
     # nodes of the graph), so warm-up also captures the graph that the timed steps
     # replay.
-    for _ in range(args.warmup):
+    for k in range(args.warmup):
+        tw = time.perf_counter()
         rk.timing_begin(args.family)
         step()
         rk.timing_end()
+        log(f"warm-up step {k + 1}/{args.warmup}: {time.perf_counter() - tw:.2f} s")
     torch.cuda.synchronize()
     launches, fam_ms = 0, 0.0
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for k in range(args.steps):
         rk.timing_begin(args.family)
         step()
         n, ms = rk.timing_end()
         launches += n
         fam_ms += ms
+        if args.steps <= 3 or k + 1 == args.steps:
+            log(f"timed step {k + 1}/{args.steps} done at {time.perf_counter() - t0:.2f} s")
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
