@@ -129,22 +129,33 @@ def cpu_baseline_window(w, W, toks, window: int):
                       f"oracle: {dt:.1f} s for {n} window token-layers (prefix prefill and reference included)"}
 
 
-def cpu_baseline(w, W, toks, prefix: int = 2048, local: bool = False):
-    """Oracle (as it stands) on a bounded sample: the first `prefix` tokens of
-    sequence 0 (a causal prefix computes exactly the same per-position values),
-    every layer, the largest alpha, clean pass included (the layer-local signal
-    with `local`)."""
+def cpu_sample(cfg):
+    """The oracle's bounded sample of a workload: (tokens of sequence 0, layers).
+    Every layer of a 2048-token prefix for the small models; for the 7-8B shapes
+    (about 0.44 GFLOP per token and layer) a 256-token prefix and the last and
+    middle layers, so the host run stays within tens of seconds."""
+    if cfg.d_model <= 1024:
+        return 2048, list(range(cfg.n_layers))
+    return 256, [cfg.n_layers - 1, cfg.n_layers // 2]
+
+
+def cpu_baseline(w, W, toks, local: bool = False):
+    """Oracle (as it stands) on a bounded sample: the first tokens of sequence 0
+    (a causal prefix computes exactly the same per-position values) and a set of
+    layers (cpu_sample), the largest alpha, clean pass included (the layer-local
+    signal with `local`)."""
     from oracle import model as OM
     from oracle import profile as OPR
     from tests.gpu_helpers import f32_weights  # noqa: E402  (exact fp32 view of the bf16 weights)
     cfg = w.model
+    prefix, layers = cpu_sample(cfg)
     m = OM.Model(cfg, f32_weights(cfg, W), np.float32)
     t = toks[0][:prefix]
     alpha = max(w.alphas)
     t0 = time.perf_counter()
     st = OM.clean_pass(m, t)
     one = OPR.local_profile_layer if local else OPR.profile_layer
-    for l in range(cfg.n_layers):
+    for l in layers:
         one(m, st, t, 0, l, OPR.PerturbParams(alpha))
     dt = time.perf_counter() - t0
     try:
@@ -152,9 +163,10 @@ def cpu_baseline(w, W, toks, prefix: int = 2048, local: bool = False):
         cores = max(int(x.get("num_threads", 1)) for x in threadpool_info()) if threadpool_info() else os.cpu_count()
     except Exception:
         cores = os.cpu_count()
-    n = len(t) * cfg.n_layers
+    n = len(t) * len(layers)
+    which = f"all {cfg.n_layers} layers" if len(layers) == cfg.n_layers else f"layers {layers}"
     return {"value": n / dt, "unit": "perturbed token-layers/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"first {len(t)} tokens of sequence 0, all {cfg.n_layers} layers, alpha={alpha}, float32 oracle"
+            "sample": f"first {len(t)} tokens of sequence 0, {which}, alpha={alpha}, float32 oracle"
                       f"{' (layer-local signal)' if local else ''}: {dt:.1f} s for {n} token-layers (clean pass "
                       f"included)"}
 
