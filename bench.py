@@ -82,6 +82,91 @@ def derive_traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, family)
             "fetch_scale": f_scale, "write_scale": w_scale, "sources": sources_hash()}
 
 
+# kernel families of the profile, by a substring of the kernel name (first match wins)
+FAMILIES = [("gemm_gate_up", "EpiSwiGLU"), ("gemm_qkv", "EpiRope"), ("gemm_o_down", "EpiResidual"),
+            ("lm_kl", "lm_kl_kernel"), ("lm_lse", "lm_lse_kernel"), ("attention", "attn_bf16_kernel"),
+            ("rmsnorm", "rmsnorm_kernel"), ("noise", "value_noise_kernel"), ("kl_merge", "kl_merge_kernel"),
+            ("local_response", "local_response_kernel")]
+
+
+def family_of(name: str):
+    for fam, key in FAMILIES:
+        if key in name:
+            return fam
+    return None
+
+
+def derive_counters(dirs):
+    """Per kernel family, from rocprofv3 --pmc csv directories of this benchmark:
+    mean counters per dispatch and mean dispatch duration, with MFMA-busy share
+    of the CU-busy cycles (SQ_VALU_MFMA_BUSY_CYCLES counts per SIMD, four per CU),
+    the share of wave cycles spent waiting, and the clock implied by
+    GRBM_GUI_ACTIVE (summed over the 8 XCDs) over the duration, which is only
+    meaningful for dispatches much longer than the profiler's own overhead (ms,
+    not us).  Prints a markdown table."""
+    import csv
+    import glob
+    from collections import defaultdict
+    vals = defaultdict(lambda: defaultdict(list))
+    durs = defaultdict(list)
+    for d in dirs:
+        for f in glob.glob(os.path.join(d, "*counter_collection.csv")):
+            for r in csv.DictReader(open(f)):
+                fam = family_of(r["Kernel_Name"])
+                if fam is None:
+                    continue
+                vals[fam][r["Counter_Name"]].append(float(r["Counter_Value"]))
+                durs[fam].append((float(r["End_Timestamp"]) - float(r["Start_Timestamp"])))
+    mean = lambda x: sum(x) / len(x) if x else float("nan")
+    print("| family | dispatches | avg us | MFMA busy / CU busy | waiting / wave cycles | clock GHz |")
+    print("|---|---|---|---|---|---|")
+    for fam, _ in FAMILIES:
+        if fam not in vals:
+            continue
+        v = {k: mean(x) for k, x in vals[fam].items()}
+        n = max(len(x) for x in vals[fam].values())
+        dur = mean(durs[fam])
+        mf = v.get("SQ_VALU_MFMA_BUSY_CYCLES", float("nan")) / (4.0 * v.get("SQ_BUSY_CU_CYCLES", float("nan")))
+        wt = v.get("SQ_WAIT_ANY", float("nan")) / v.get("SQ_WAVE_CYCLES", float("nan"))
+        ck = v.get("GRBM_GUI_ACTIVE", float("nan")) / 8.0 / dur
+        print(f"| {fam} | {n} | {dur / 1e3:.1f} | {mf:.3f} | {wt:.3f} | {ck:.2f} |")
+
+
+def derive_traffic_table(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir):
+    """Per kernel family: HBM bytes per dispatch (FETCH_SIZE and WRITE_SIZE scaled
+    by the 1 GiB copy calibration) and the rate over the mean dispatch duration
+    of the same counter runs.  Prints a markdown table."""
+    import csv
+    import glob
+    from collections import defaultdict
+
+    def per_family(d, calib):
+        out, durs = defaultdict(list), defaultdict(list)
+        for f in glob.glob(os.path.join(d, "*counter_collection.csv")):
+            for r in csv.DictReader(open(f)):
+                fam = "copy" if calib and "copyBuffer" in r["Kernel_Name"] else family_of(r["Kernel_Name"])
+                if fam is None:
+                    continue
+                out[fam].append(float(r["Counter_Value"]) * 1024.0)
+                durs[fam].append(float(r["End_Timestamp"]) - float(r["Start_Timestamp"]))
+        return ({k: sum(x) / len(x) for k, x in out.items()}, {k: sum(x) / len(x) for k, x in durs.items()})
+
+    cf, _ = per_family(copy_fetch_dir, True)
+    cw, _ = per_family(copy_write_dir, True)
+    fs, ws = float(1 << 30) / cf["copy"], float(1 << 30) / cw["copy"]
+    fetch, df = per_family(fetch_dir, False)
+    write, dw = per_family(write_dir, False)
+    print(f"| family | HBM read MB | HBM write MB | avg us | GB/s | of 8 TB/s |  (FETCH x {fs:.3f}, WRITE x {ws:.3f})")
+    print("|---|---|---|---|---|---|")
+    for fam, _ in FAMILIES:
+        if fam not in fetch or fam not in write:
+            continue
+        rd, wr = fetch[fam] * fs, write[fam] * ws
+        dur = (df[fam] + dw[fam]) / 2.0
+        gbs = (rd + wr) / dur
+        print(f"| {fam} | {rd / 1e6:.1f} | {wr / 1e6:.1f} | {dur / 1e3:.1f} | {gbs:.0f} | {gbs / HBM_PEAK_GBS:.2f} |")
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -471,9 +556,20 @@ def main():
                     help="only run a plain 1 GiB device-to-device copy (calibrates HBM byte counters)")
     ap.add_argument("--derive-traffic", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
                     help="print the per-launch HBM bytes of --family from rocprofv3 --pmc csv directories")
+    ap.add_argument("--derive-traffic-table", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
+                    help="print HBM bytes and GB/s of every kernel family from the same four directories")
+    ap.add_argument("--derive-counters", nargs="+", metavar="DIR",
+                    help="print MFMA-busy, waiting and clock figures per kernel family from rocprofv3 --pmc "
+                         "csv directories")
     args = ap.parse_args()
     if args.derive_traffic:
         print(json.dumps(derive_traffic(*args.derive_traffic, args.family)))
+        return
+    if args.derive_traffic_table:
+        derive_traffic_table(*args.derive_traffic_table)
+        return
+    if args.derive_counters:
+        derive_counters(args.derive_counters)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the profile's passes are independent and "
