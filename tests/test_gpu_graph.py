@@ -1,4 +1,5 @@
-"""HIP-graph replay of rk_sensitivity_profile (RK_FLAG_GRAPH).
+"""HIP-graph replay of rk_sensitivity_profile (RK_FLAG_GRAPH), in both modes and
+with both signals (the final-distribution KL and the layer-local response).
 
 The graphed call must give bitwise the eager results on every replay, with the
 program's own eager work and synchronisations between the replays; a change of
@@ -23,14 +24,14 @@ def _setup(window=False):
     return cfg, run, make_batch(toks)
 
 
-@pytest.mark.parametrize("window", [False, True])
-def test_graph_replays_match_eager(window):
+@pytest.mark.parametrize("window,local", [(False, False), (True, False), (False, True), (True, True)])
+def test_graph_replays_match_eager(window, local):
     import torch
     import paper_2608_08684_amd as rk
     cfg, run, batch = _setup()
     layers, alphas = [0, 1, 2], [0.05, 0.1]
-    mode = rk.RK_FLAG_CACHED_WINDOW if window else 0
-    kw = dict(window_start=70, flags=mode) if window else {}
+    mode = (rk.RK_FLAG_CACHED_WINDOW if window else 0) | (rk.RK_FLAG_LOCAL_SIGNAL if local else 0)
+    kw = dict(window_start=70 if window else 0, flags=mode)
     s_e, d_e = run.profile(batch, layers, alphas, max_group=4, **kw)          # eager reference
     m = run.model
     rows = batch.rows
@@ -53,7 +54,8 @@ def test_graph_replays_match_eager(window):
                           window_start=70 if window else 0)
     torch.cuda.synchronize()
     assert np.array_equal(s.cpu().numpy().astype(np.float64), s_e[::-1])
-    log(f"graph replays ({'cached window' if window else 'resumed'}) match the eager profile bitwise")
+    log(f"graph replays ({'cached window' if window else 'resumed'}{', local signal' if local else ''}) match the "
+        f"eager profile bitwise")
 
 
 def test_graph_timing_sessions():
