@@ -468,6 +468,13 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
     Bs[(kq + 0) * 132 + lrow + 64] = b1.x; Bs[(kq + 1) * 132 + lrow + 64] = b1.y;
     Bs[(kq + 2) * 132 + lrow + 64] = b1.z; Bs[(kq + 3) * 132 + lrow + 64] = b1.w;
     __syncthreads();
+    // blocked summation: each 16-wide k-chunk in a fresh partial, then added to
+    // the running sum, so the rounding error grows with K / 16 + 16 terms, not K
+    float part[4][8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) part[i][j] = 0.f;
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
       float av[4], bv[8];
@@ -478,8 +485,12 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+        for (int j = 0; j < 8; ++j) part[i][j] = fmaf(av[i], bv[j], part[i][j]);
     }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[i][j] += part[i][j];
   }
   __syncthreads();
   float* Cs = smem;
