@@ -666,8 +666,20 @@ def main():
     value = tokens_layers / (ms_per_step / 1e3)
 
     fam_avg_ms = fam_ms / max(launches, 1)
-    n_pass_lm = G  # perturbed passes scored per LM-head launch (algorithmic: pert logits only)
-    flops = family_flops(args.family, cfg, eval_rows, n_pass_lm)
+    if args.family == "lm_kl":
+        n_pass_lm = G  # perturbed passes scored per LM-head launch (algorithmic: pert logits only)
+        flops = family_flops(args.family, cfg, eval_rows, n_pass_lm)
+    else:
+        # a projection family's rows over the step: the reference pass (the prefix
+        # prefill and the window in the cached-window mode) and every resumed layer
+        # of every pass; in the cached-window mode one launch carries the window
+        # rows of several passes, so the flops per launch are the step's over its
+        # launches
+        L = cfg.n_layers
+        pass_layers = sum(L - l for l in layers) * len(alphas)
+        rows_total = rows * L + eval_rows * pass_layers if window == 0 else \
+            (rows - eval_rows) * L + eval_rows * L + eval_rows * pass_layers
+        flops = family_flops(args.family, cfg, rows_total, 1) * args.steps / max(launches, 1)
     achieved = flops / (fam_avg_ms / 1e3) / 1e12
     traffic = None
     rec = TRAFFIC.get((args.family, w.name))

@@ -251,6 +251,23 @@ struct ObsCapture {
   int w;
 };
 
+// Cached-window passes evaluated together (layer-synchronous batch): pass q of the
+// batch owns rows [q * rw, (q + 1) * rw) of the block's buffers, and its
+// attention reads layer l's prefix cache, with its own perturbed Values when l is
+// the pass's layer.
+struct WinBatch {
+  const Win* wn;
+  const SeqTable* pst;   // prefix rows: cache layout and noise keys
+  const SeqTable* wst;   // the window rows of one pass
+  const SeqTable* bt;    // the window rows of all n passes (pass q's sequences at q * wst->n ..)
+  int n;                 // passes in the batch
+  const int* layer;      // perturbed layer of each pass
+  const float* alpha;
+  const rk_perturb_params* p;
+  int64_t rw;            // window rows per pass
+};
+static rk_status batch_attention(const rk_model* m, int l, const Bufs& b, const WinBatch& wb, hipStream_t s);
+
 // One decoder block from h_in to h_out (h_out may equal h_in); `noise` perturbs
 // the block's Values between the q|k|v projection and attention.
 // With `pre`, the block's rows are the window rows of a cached-window batch and
@@ -258,7 +275,7 @@ struct ObsCapture {
 // block's K and V columns, row by row, and `obs` the observation queries.
 static rk_status run_block(const rk_model* m, int l, const float* h_in, float* h_out, const Bufs& b,
                            const SeqTable& st, const Noise* noise, hipStream_t s, const KvPrefix* pre = nullptr,
-                           void* kv_out = nullptr, const ObsCapture* obs = nullptr) {
+                           void* kv_out = nullptr, const ObsCapture* obs = nullptr, const WinBatch* wb = nullptr) {
   const rk_model_config& c = m->cfg;
   const int R = st.rows, d = c.d_model;
   { Timed t("rmsnorm", s); RK_TRY(launch_rmsnorm(h_in, m->attn_norm[l], b.x, m->bf16, R, d, c.rms_eps, s)); }
@@ -284,7 +301,10 @@ static rk_status run_block(const rk_model* m, int l, const float* h_in, float* h
     RK_TRY(launch_value_noise(v, m->bf16, m->qkv_cols, st, c.n_kv_heads, c.head_dim, l, noise->alpha,
                               noise->p->seed, noise->p->protect_head, noise->p->protect_tail, s));
   }
-  {
+  if (wb) {
+    rk_status e = batch_attention(m, l, b, *wb, s);
+    if (e != RK_OK) return e;
+  } else {
     Timed t("attention", s);
     RK_TRY(launch_attention(b.qkv, m->qkv_cols, b.att, m->attn_cols, st, c.n_heads, c.n_kv_heads, c.head_dim,
                             m->bf16, s, pre));
@@ -441,7 +461,8 @@ static rk_status window_tables(const SeqTable& st, int P, SeqTable* pst, SeqTabl
 static KvPrefix cache_prefix(const rk_model* m, const Win& wn, const SeqTable& pst, int l, const void* vpert) {
   const int64_t kc = kv_cols(m);
   const bf16_t* kv = (const bf16_t*)wn.kv + (size_t)l * pst.rows * kc;
-  KvPrefix pk;
+  KvPrefix pk{};
+  pk.alt_pass = -1;
   pk.k = kv;
   pk.ldk = kc;
   pk.P = pst.max_len;
@@ -536,6 +557,116 @@ static rk_status window_local_pass(const rk_model* m, const SeqTable& pst, const
   return RK_OK;
 }
 
+static rk_status batch_attention(const rk_model* m, int l, const Bufs& b, const WinBatch& wb, hipStream_t s) {
+  const rk_model_config& c = m->cfg;
+  const int64_t a = act_bytes(m), kc = kv_cols(m), Rp = wb.pst->rows;
+  int n_at_l = 0, alt = -1;
+  for (int q = 0; q < wb.n; ++q)
+    if (wb.layer[q] == l) { ++n_at_l; alt = q; }
+  if (n_at_l <= 1) {
+    // one launch over every pass's window rows; at most one pass reads perturbed Values
+    KvPrefix pk = cache_prefix(m, *wb.wn, *wb.pst, l, nullptr);
+    pk.n_seq = wb.wst->n;
+    if (alt >= 0) {
+      const char* kv_l = (const char*)wb.wn->kv + (size_t)l * Rp * kc * a;
+      RK_TRY(launch_copy_cols(kv_l, kc * a, (kc / 2) * a, b.vpert, (kc / 2) * a, (kc / 2) * a, (int)Rp, s));
+      Timed t("noise", s);
+      RK_TRY(launch_value_noise(b.vpert, m->bf16, kc / 2, *wb.pst, c.n_kv_heads, c.head_dim, l, wb.alpha[alt],
+                                wb.p->seed, wb.p->protect_head, wb.p->protect_tail, s));
+      pk.alt_pass = alt;
+      pk.v_alt = (const bf16_t*)b.vpert;
+      pk.ldv_alt = kc / 2;
+    }
+    Timed t("attention", s);
+    RK_TRY(launch_attention(b.qkv, m->qkv_cols, b.att, m->attn_cols, *wb.bt, c.n_heads, c.n_kv_heads, c.head_dim,
+                            m->bf16, s, &pk));
+    return RK_OK;
+  }
+  for (int q = 0; q < wb.n; ++q) {
+    const void* vp = nullptr;
+    if (wb.layer[q] == l) {   // this pass's layer: a perturbed copy of the cached prefix Values
+      const char* kv_l = (const char*)wb.wn->kv + (size_t)l * Rp * kc * a;
+      RK_TRY(launch_copy_cols(kv_l, kc * a, (kc / 2) * a, b.vpert, (kc / 2) * a, (kc / 2) * a, (int)Rp, s));
+      Timed t("noise", s);
+      RK_TRY(launch_value_noise(b.vpert, m->bf16, kc / 2, *wb.pst, c.n_kv_heads, c.head_dim, l, wb.alpha[q],
+                                wb.p->seed, wb.p->protect_head, wb.p->protect_tail, s));
+      vp = b.vpert;
+    }
+    const KvPrefix pk = cache_prefix(m, *wb.wn, *wb.pst, l, vp);
+    Timed t("attention", s);
+    RK_TRY(launch_attention((const char*)b.qkv + (size_t)q * wb.rw * m->qkv_cols * a, m->qkv_cols,
+                            (char*)b.att + (size_t)q * wb.rw * m->attn_cols * a, m->attn_cols, *wb.wst, c.n_heads,
+                            c.n_kv_heads, c.head_dim, m->bf16, s, &pk));
+  }
+  return RK_OK;
+}
+
+// A group of cached-window passes, layer-synchronously (the survey's pass
+// batching): the passes, ordered by their perturbed layer, join the batch at that
+// layer from the window's cached block input, and from then on every norm,
+// projection and feed-forward of a layer runs once over the window rows of all
+// active passes (up to max_rows rows and RK_MAX_BATCH_SEQS sequences per batch;
+// larger groups go in consecutive batches).  Every kernel is row-wise or per pass,
+// so each pass's result is bitwise that of window_perturbed_final.  Pass k's final
+// hidden state goes to slot k of xp (stride pad_rows(Rw) rows).  The rotary table
+// must hold the window positions; it does again on return.
+static rk_status window_group_final(const rk_model* m, const SeqTable& pst, const SeqTable& wst, const Win& wn,
+                                    int G, const int* layers, const float* alphas, const rk_perturb_params* p,
+                                    int64_t max_rows, void* xp, const Bufs& b, hipStream_t s) {
+  const rk_model_config& c = m->cfg;
+  const int64_t d = c.d_model, Rw = wst.rows, xstride = pad_rows(Rw) * d * act_bytes(m);
+  const int L = c.n_layers, P = pst.max_len;
+  int B = (int)std::min<int64_t>(G, max_rows / Rw);
+  B = std::min(B, RK_MAX_BATCH_SEQS / wst.n);
+  if (B < 2) {
+    for (int k = 0; k < G; ++k) {
+      rk_status e = window_perturbed_final(m, pst, wst, wn, layers[k], alphas[k], p, (char*)xp + (size_t)k * xstride,
+                                           b, s);
+      if (e != RK_OK) return e;
+    }
+    return RK_OK;
+  }
+  std::vector<int> order(G);
+  for (int k = 0; k < G; ++k) order[k] = k;
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return layers[x] < layers[y]; });
+  for (int c0 = 0; c0 < G; c0 += B) {
+    const int cb = std::min(B, G - c0);
+    int lay[RK_MAX_GROUP];
+    float al[RK_MAX_GROUP];
+    for (int q = 0; q < cb; ++q) {
+      lay[q] = layers[order[c0 + q]];
+      al[q] = alphas[order[c0 + q]];
+    }
+    // batch table: sequence i of pass slot q at rows q * Rw + wst.off[i]
+    SeqTable bst = wst;
+    bst.n = cb * wst.n;
+    for (int q = 0; q < cb; ++q)
+      for (int i = 0; i < wst.n; ++i) bst.off[q * wst.n + i] = (int32_t)(q * Rw) + wst.off[i];
+    bst.off[bst.n] = (int32_t)(cb * Rw);
+    bst.rows = (int32_t)(cb * Rw);
+    RK_TRY(launch_rope_table(b.rope, b.rope_pos, bst, c.head_dim, c.rope_theta, s, P));
+    int active = 0;
+    for (int j = lay[0]; j < L; ++j) {
+      while (active < cb && lay[active] == j) {   // joins at its layer
+        RK_TRY(hipMemcpyAsync(b.h + (size_t)active * Rw * d, wn.w.h + (size_t)j * Rw * d, (size_t)Rw * d * 4,
+                              hipMemcpyDeviceToDevice, s));
+        ++active;
+      }
+      SeqTable at = bst;   // the active passes' rows
+      at.n = active * wst.n;
+      at.rows = (int32_t)(active * Rw);
+      const WinBatch wb{&wn, &pst, &wst, &at, active, lay, al, p, Rw};
+      rk_status e = run_block(m, j, b.h, b.h, b, at, nullptr, s, nullptr, nullptr, nullptr, &wb);
+      if (e != RK_OK) return e;
+    }
+    for (int q = 0; q < cb; ++q)
+      RK_TRY(launch_rmsnorm(b.h + (size_t)q * Rw * d, m->final_norm, (char*)xp + (size_t)order[c0 + q] * xstride,
+                            m->bf16, (int)Rw, (int)d, c.rms_eps, s));
+  }
+  RK_TRY(launch_rope_table(b.rope, b.rope_pos, wst, c.head_dim, c.rope_theta, s, P));
+  return RK_OK;
+}
+
 // Compression damage of layer `layer` (Section 2, Eq. layer-compression-damage):
 // the window rows resume from their input to that block with its prompt cache
 // replaced by the b retained positions of every KV head (gathered into a b-row
@@ -549,7 +680,8 @@ static rk_status window_compressed_final(const rk_model* m, const SeqTable& pst,
   const char* kv_l = (const char*)wn.kv + (size_t)layer * Rp * kc * a;
   RK_TRY(launch_prefix_gather(kv_l, kc, pst.n, pst.max_len, c.n_kv_heads, c.head_dim, pos, seq_stride, b, bf.cpre,
                               s));
-  KvPrefix pk;
+  KvPrefix pk{};
+  pk.alt_pass = -1;
   pk.k = (const bf16_t*)bf.cpre;
   pk.v = (const bf16_t*)bf.cpre + kc / 2;
   pk.ldk = pk.ldv = kc;
@@ -1182,19 +1314,21 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
         pm.G = G;
         pm.seq_index0 = first;
         pm.d_seq_stride = n_A;
+        int glay[RK_MAX_GROUP];
+        float galpha[RK_MAX_GROUP];
         for (int k = 0; k < G; ++k) {
           const int idx = g0 + k, a = idx / n_A, j = idx % n_A;
-          if (local) {
-            if ((e = window_local_pass(m, pst, wst, wn, layers[j], alphas[a], p, b.hloc, b.kl + (size_t)k * Rw, b,
-                                       s)) != RK_OK)
-              return e;
-          } else {
-            void* xf = (char*)b.xp + (size_t)k * pad_rows(Rw) * m->cfg.d_model * act_bytes(m);
-            if ((e = window_perturbed_final(m, pst, wst, wn, layers[j], alphas[a], p, xf, b, s)) != RK_OK) return e;
-          }
+          glay[k] = layers[j];
+          galpha[k] = alphas[a];
+          if (local &&
+              (e = window_local_pass(m, pst, wst, wn, layers[j], alphas[a], p, b.hloc, b.kl + (size_t)k * Rw, b,
+                                     s)) != RK_OK)
+            return e;
           pm.d_base[k] = (int64_t)a * N * n_A + j;
           pm.s_index[k] = a * n_A + j;
         }
+        if (!local && (e = window_group_final(m, pst, wst, wn, G, glay, galpha, p, max_rows, b.xp, b, s)) != RK_OK)
+          return e;
         if (!local && (e = score_group(m, wst, wn.w, b.xp, G, unfused, b.logits_p, b.kl, b, s)) != RK_OK) return e;
         RK_TRY(launch_window_mean(b.kl, Rw, G, wst, 0, b.dbatch, s));
         RK_TRY(launch_accumulate(b.dbatch, st.n, pm, d_out, b.sacc, s));

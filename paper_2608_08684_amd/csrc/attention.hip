@@ -149,14 +149,20 @@ __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_ker
   const int P = PREFIX ? pk.P : 0;
   i32x4_t rk_p = rsrc, rv_p = rsrc;
   uint32_t koff_p[PREFIX ? NLD : 1], voff_p[PREFIX ? NLD : 1];
+  int64_t ldv_p = pk.ldv;
   if constexpr (PREFIX) {
-    rk_p = make_rsrc(pk.k + (int64_t)k * P * pk.ldk, (int64_t)P * pk.ldk * 2);
-    rv_p = make_rsrc(pk.v + (int64_t)k * P * pk.ldv, (int64_t)P * pk.ldv * 2);
+    // the prefix of this sequence (of sequence k % n_seq when several passes share a launch)
+    const int ps = pk.n_seq > 0 ? k % pk.n_seq : k;
+    const bool alt = pk.n_seq > 0 && k / pk.n_seq == pk.alt_pass;
+    const bf16_t* vb = alt ? pk.v_alt : pk.v;
+    ldv_p = alt ? pk.ldv_alt : pk.ldv;
+    rk_p = make_rsrc(pk.k + (int64_t)ps * P * pk.ldk, (int64_t)P * pk.ldk * 2);
+    rv_p = make_rsrc(vb + (int64_t)ps * P * ldv_p, (int64_t)P * ldv_p * 2);
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
       const int slot = (i * 4 + w) * 64 + lane, r = slot / CH, ph = slot % CH;
       koff_p[i] = (uint32_t)(r * pk.ldk * 2 + (hk * DH + (ph ^ k_swz<DH>(r)) * 8) * 2);
-      voff_p[i] = (uint32_t)(r * pk.ldv * 2 + (hk * DH + (ph ^ v_swz<DH>(r)) * 8) * 2);
+      voff_p[i] = (uint32_t)(r * ldv_p * 2 + (hk * DH + (ph ^ v_swz<DH>(r)) * 8) * 2);
     }
   }
   const int n_pre = (P + BKV - 1) / BKV;   // prefix tiles, visited before the window's own
@@ -166,7 +172,7 @@ __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_ker
   auto issue = [&](int t, int b) {
     if (PREFIX && t < n_pre) {
       const int sk = __builtin_amdgcn_readfirstlane(t * BKV * (int)pk.ldk * 2);
-      const int sv = __builtin_amdgcn_readfirstlane(t * BKV * (int)pk.ldv * 2);
+      const int sv = __builtin_amdgcn_readfirstlane(t * BKV * (int)ldv_p * 2);
 #pragma unroll
       for (int i = 0; i < NLD; ++i) {
         const uint32_t o = (uint32_t)((b * SLOTS + (i * 4 + w) * 64) * 16);
@@ -402,7 +408,10 @@ hipError_t launch_attention(const void* qkv, int64_t ldq, void* out, int64_t ldo
     KvPrefix pk{};
     if (pre) {
       pk = *prefix;
-      if ((int64_t)st.n * pk.P * std::max(pk.ldk, pk.ldv) * 2 >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+      const int64_t n_pre_seqs = pk.n_seq > 0 ? pk.n_seq : st.n;
+      const int64_t ld = std::max(std::max(pk.ldk, pk.ldv), pk.alt_pass >= 0 && pk.n_seq > 0 ? pk.ldv_alt : 0);
+      if (n_pre_seqs * pk.P * ld * 2 >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+      if (pk.n_seq > 0 && (st.n % pk.n_seq != 0 || (pk.alt_pass >= 0 && !pk.v_alt))) return hipErrorInvalidValue;
     }
 #define RK_ATTN(D, PRE)                                                                                      \
   attn_bf16_kernel<D, PRE><<<grid, 256, 0, s>>>((const bf16_t*)qkv, ldq, (bf16_t*)out, ldo, st, wk, n_heads, \

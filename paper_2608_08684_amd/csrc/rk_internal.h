@@ -115,6 +115,14 @@ struct KvPrefix {
   const bf16_t* v;
   int64_t ldk, ldv;
   int32_t P;
+  // Several passes' window rows in one launch (n_seq > 0): sequence s of the table
+  // reads the cached prefix of sequence s % n_seq, and the sequences of pass
+  // alt_pass (s / n_seq == alt_pass; -1 for none) read their Values from v_alt
+  // (row stride ldv_alt) instead of v.  n_seq = 0: sequence s reads prefix s.
+  const bf16_t* v_alt;
+  int64_t ldv_alt;
+  int32_t n_seq;
+  int32_t alt_pass;
 };
 
 hipError_t launch_attention(const void* qkv, int64_t ldq, void* out, int64_t ldo, const SeqTable& st,
