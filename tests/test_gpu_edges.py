@@ -1,0 +1,82 @@
+"""GPU parity on the edge cases of the sensitivity profile.
+
+* sequences of one and two tokens, and lengths on and next to the 64-key and
+  128-query tile boundaries, in one batch (bf16 GQA model and the fp32 model):
+  d_{i,l} and the KL of every position against the oracle;
+* windows that are empty (window_start >= T_i gives d = 0 by definition) or hold
+  a single position; an eligible range that is empty (protect_head >= T_i) gives
+  exactly 0;
+* a calibration set of 70 sequences, more than one batch holds (64), split by
+  rk_sensitivity_profile into consecutive batches: s is the unweighted mean of
+  the 70 per-sequence values, each equal to its single-batch value.
+"""
+import numpy as np
+import pytest
+
+import fixtures as F
+from oracle import model as OM
+from oracle import profile as OPR
+
+from gpu_helpers import Runner, f32_weights, log, make_batch
+from test_gpu_parity import assert_kl_close
+
+pytestmark = pytest.mark.gpu
+
+BF16 = F.small_model(n_layers=3, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=512, vocab=1024,
+                     rope_theta=1.0e4, dtype="bf16")
+F32 = F.small_model(n_layers=2, d_model=128, n_heads=4, n_kv_heads=4, head_dim=32, d_ff=256, vocab=512,
+                    rope_theta=1.0e4, dtype="f32")
+LENS = [1, 2, 63, 64, 65, 1, 128, 129]
+
+
+def _kl_rows_close(got, ref, what):
+    err = np.abs(got - ref)
+    ok = (err <= 0.05 * np.abs(ref)) | (err <= 1e-5)
+    assert ok.all(), f"{what}: {np.count_nonzero(~ok)} positions off (max err {err.max():.3e})"
+
+
+@pytest.mark.parametrize("cfg", [BF16, F32], ids=["bf16", "f32"])
+def test_short_and_boundary_lengths(cfg):
+    W = F.make_weights(cfg)
+    run = Runner(cfg, W)
+    m = OM.Model(cfg, f32_weights(cfg, W), np.float64)
+    toks = F.make_tokens(F.make_workload("edge", cfg, LENS, seed_id=71))
+    batch = make_batch(toks)
+    cs = run.clean(batch)
+    off = np.concatenate([[0], np.cumsum(LENS)])
+    sts = [OM.clean_pass(m, t) for t in toks]
+    for l in range(cfg.n_layers):
+        for ws in (0, 1, 64):
+            d, kl, _ = run.layer(batch, cs, l, 0.1, window_start=ws)
+            ref = []
+            for k, t in enumerate(toks):
+                dk, klk = OPR.profile_layer(m, sts[k], t, k, l, OPR.PerturbParams(0.1, window_start=ws))
+                ref.append(dk)
+                _kl_rows_close(kl[off[k]:off[k + 1]], klk, f"{cfg.dtype} layer {l} seq {k} (T={LENS[k]})")
+                if ws >= LENS[k]:
+                    assert d[k] == 0.0, "an empty window gives d = 0"
+            assert_kl_close(d, ref, f"{cfg.dtype} layer {l} window_start {ws}")
+        # nothing eligible: exactly zero everywhere
+        d0, kl0, _ = run.layer(batch, cs, l, 0.5, protect_head=max(LENS))
+        assert np.all(d0 == 0.0) and np.all(kl0 == 0.0)
+    log(f"{cfg.dtype}: lengths {LENS} match the oracle at every layer and window start")
+
+
+def test_more_sequences_than_one_batch():
+    cfg = BF16
+    W = F.make_weights(cfg)
+    run = Runner(cfg, W)
+    m = OM.Model(cfg, f32_weights(cfg, W), np.float64)
+    rng = np.random.default_rng([5, 70])
+    lens = [int(x) for x in rng.integers(1, 40, size=70)]
+    toks = F.make_tokens(F.make_workload("many", cfg, lens, seed_id=72))
+    batch = make_batch(toks)
+    layers = [0, 2]
+    s, d = run.profile(batch, layers, [0.1], max_rows=sum(lens), max_group=2)
+    ref = OPR.sensitivity_profile(m, toks, layers, [0.1])
+    assert_kl_close(d[0], ref["d"][0], "70 sequences: d")
+    assert_kl_close(s[0], ref["s"][0], "70 sequences: s")
+    assert np.allclose(s[0], d[0].mean(axis=0), rtol=1e-6)
+    # the first 64 as their own batch: the same per-sequence values
+    s64, d64 = run.profile(make_batch(toks[:64]), layers, [0.1], max_rows=sum(lens), max_group=2)
+    assert np.array_equal(d64[0], d[0][:64])
