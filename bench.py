@@ -39,8 +39,8 @@ HBM_PEAK_GBS = 8000.0         # MI355X HBM3E
 # profiles/).  Keyed by (family, workload); valid only while the kernel sources
 # hash to the recorded value, so a changed kernel reports null until re-measured.
 TRAFFIC = {
-    ("gemm_gate_up", "gpt2s-bf16"): {"bytes_per_launch": 327069541, "fetch_bytes": 226406245, "write_bytes": 100663296,
-                                     "sources": "5c5faf7cea8ac063"},
+    ("gemm_gate_up", "gpt2s-bf16"): {"bytes_per_launch": 327069819, "fetch_bytes": 226406523,
+                                     "write_bytes": 100663296, "sources": "9f818d8415c40766"},
 }
 KERNEL_SOURCES = ["paper_2608_08684_amd/csrc/gemm.hip", "paper_2608_08684_amd/csrc/mfma_tile.h",
                   "paper_2608_08684_amd/csrc/rk_internal.h"]
@@ -439,7 +439,8 @@ def damage_main(args):
     SnapKV with the same budget b at every layer, one layer at a time, the window
     [P, T) evaluated against the caches; then Spearman's rho of the damage profile
     against the cached-window sensitivity profile.  One step = the damage of every
-    layer for all sequences plus the rank correlation."""
+    layer for all sequences (one rk_compression_damage_layers call: each layer's
+    pass joins the batch at that layer) plus the rank correlation."""
     import torch
     import fixtures as F
     import paper_2608_08684_amd as rk
@@ -459,7 +460,7 @@ def damage_main(args):
     rows = batch.rows
     # the prompts' caches and the window reference
     state = torch.empty(model.window_state_size(rows), dtype=torch.uint8, device="cuda")
-    ws = torch.empty(model.workspace_size(rows, 1, rk.RK_FLAG_CACHED_WINDOW), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(model.workspace_size(rows, L, rk.RK_FLAG_CACHED_WINDOW), dtype=torch.uint8, device="cuda")
     model.window_reference(batch, P, state, ws)
     # SnapKV on the prompts with the same budget at every layer (the base compressor)
     pb = make_batch([t[:P] for t in toks])
@@ -485,9 +486,8 @@ def damage_main(args):
     log(f"damage inputs ready in {time.perf_counter() - t0:.1f} s (prompt {P}, window {window}, b = {b})")
 
     def step():
-        for l in range(L):
-            model.compression_damage(batch, P, l, pos[l * Hkv * b:], b, state, d_all[l], ws,
-                                     seq_stride=L * Hkv * b)
+        model.compression_damage_layers(batch, P, list(range(L)), pos, Hkv * b, b, state, d_all, ws,
+                                        seq_stride=L * Hkv * b)
         D = d_all.mean(dim=1).cpu().numpy().astype(np.float64)     # synchronises
         return D, rk.spearman(s_prof, D)
 
@@ -509,7 +509,10 @@ def damage_main(args):
     eval_rows = sum(T - P for T in lens)
     value = eval_rows * L / (ms_per_step / 1e3)
     avg = fam_ms / max(launches, 1)
-    flops = family_flops(args.family, cfg, eval_rows, 1)
+    if args.family == "lm_kl":   # the step's L passes scored over the window rows
+        flops = family_flops(args.family, cfg, eval_rows * L, 1) * args.steps / max(launches, 1)
+    else:   # layer l's pass runs blocks l .. L-1 over the window rows: L (L + 1) / 2 block-passes
+        flops = family_flops(args.family, cfg, eval_rows * L * (L + 1) // 2, 1) * args.steps / max(launches, 1)
     achieved = flops / (avg / 1e3) / 1e12
     roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
             "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": args.family,
@@ -522,7 +525,7 @@ def damage_main(args):
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic (random-init N(0,0.02) weights, Zipf(1.1) tokens)",
         "config": {"workload": f"{w.name} compression damage: {L}L d{cfg.d_model} {cfg.n_heads}x{dh}; "
                                f"{batch.n_seqs}x{max(lens)} tokens, prompt {P} + window {window}; SnapKV b = {b} "
-                               f"(window {DMG_OBS}, max pooling 7) at one layer at a time",
+                               f"(window {DMG_OBS}, max pooling 7) at one layer at a time, all layers in one call",
                    "spearman_rho": None if np.isnan(rho) else round(float(rho), 4)},
         "roofline": roof,
     }

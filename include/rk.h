@@ -370,6 +370,23 @@ rk_status rk_compression_damage(const rk_model *m, const rk_batch *batch, int32_
                                 size_t state_bytes, float *d_out, float *kl_pos, void *workspace, size_t ws_bytes,
                                 void *stream);
 
+/* The damage of several layers in one call: d_out[k * n_seqs + i] is
+ * rk_compression_damage's d_i for layer layers[k] (HOST int32 [n_layers], 1 ..
+ * 16 entries), whose retained positions start at positions + layers[k] *
+ * layer_stride (per sequence at seq_stride, as for rk_compression_damage; with
+ * the outputs of rk_snapkv_compress for prompts of P tokens and the same budget b
+ * at every layer: layer_stride = n_kv_heads * b, seq_stride = n_layers *
+ * n_kv_heads * b).  kl_pos: DEVICE fp32 [n_layers, window rows] or NULL.  The
+ * layers are evaluated together, each joining at its own layer, so the
+ * projections run once per layer over the window rows of every layer being
+ * evaluated; the results are bitwise those of separate rk_compression_damage
+ * calls.  Workspace: rk_workspace_size(m, rows, n_layers, RK_FLAG_CACHED_WINDOW).  */
+rk_status rk_compression_damage_layers(const rk_model *m, const rk_batch *batch, int32_t window_start,
+                                       const int32_t *layers, int32_t n_layers, const int32_t *positions,
+                                       int64_t layer_stride, int64_t seq_stride, int32_t n_keep, const void *state,
+                                       size_t state_bytes, float *d_out, float *kl_pos, void *workspace,
+                                       size_t ws_bytes, void *stream);
+
 /* Spearman's rho of two profiles x, y [n] (Section 2, Table
  * sensitivity-correlation): the Pearson correlation of their ranks, ties sharing
  * the mean rank; NaN when a profile is constant.  Host only, float64.          */

@@ -120,6 +120,8 @@ def load() -> ctypes.CDLL:
         "rk_timing_end": (st, [ctypes.POINTER(i64), ctypes.POINTER(f64)]),
         "rk_compression_damage": (st, [vp, ctypes.POINTER(_Batch), i32, i32, vp, i64, i32, vp, sz, vp, vp, vp, sz,
                                        vp]),
+        "rk_compression_damage_layers": (st, [vp, ctypes.POINTER(_Batch), i32, ctypes.POINTER(i32), i32, vp, i64,
+                                              i64, i32, vp, sz, vp, vp, vp, sz, vp]),
         "rk_spearman": (st, [ctypes.POINTER(f64), ctypes.POINTER(f64), i32, ctypes.POINTER(f64)]),
         "rk_snapkv_state_size": (sz, [vp, i64, i32, i32]),
         "rk_snapkv_workspace_size": (sz, [vp, i64, i32, i32]),
@@ -264,6 +266,18 @@ class Model:
                                             state.numel() * state.element_size(), _ptr(d_out), _ptr(kl_pos),
                                             _ptr(workspace), workspace.numel() * workspace.element_size(),
                                             _stream(stream)))
+
+    def compression_damage_layers(self, batch: Batch, window_start: int, layers: Sequence[int], positions,
+                                  layer_stride: int, n_keep: int, state, d_out, workspace, seq_stride=None,
+                                  kl_pos=None, stream=None):
+        """rk_compression_damage_layers: d_out [len(layers), n_seqs]."""
+        stride = int(self.cfg.n_kv_heads * n_keep if seq_stride is None else seq_stride)
+        lay = (ctypes.c_int32 * len(layers))(*[int(x) for x in layers])
+        _check(load().rk_compression_damage_layers(self._h, ctypes.byref(batch._c), int(window_start), lay,
+                                                   len(layers), _ptr(positions), int(layer_stride), stride,
+                                                   int(n_keep), _ptr(state), state.numel() * state.element_size(),
+                                                   _ptr(d_out), _ptr(kl_pos), _ptr(workspace),
+                                                   workspace.numel() * workspace.element_size(), _stream(stream)))
 
     # -- SnapKV consumer of the budgets
     def snapkv_state_size(self, rows: int, n_seqs: int, obs_window: int) -> int:

@@ -265,6 +265,12 @@ struct WinBatch {
   const float* alpha;
   const rk_perturb_params* p;
   int64_t rw;            // window rows per pass
+  // compression damage instead of Value noise: at its layer, pass q reads the
+  // n_keep retained prompt positions of every KV head, pos[q] (per sequence at
+  // seq_stride), gathered from that layer's cache
+  const int32_t* const* pos;
+  int64_t seq_stride;
+  int n_keep;
 };
 static rk_status batch_attention(const rk_model* m, int l, const Bufs& b, const WinBatch& wb, hipStream_t s);
 
@@ -563,6 +569,37 @@ static rk_status batch_attention(const rk_model* m, int l, const Bufs& b, const 
   int n_at_l = 0, alt = -1;
   for (int q = 0; q < wb.n; ++q)
     if (wb.layer[q] == l) { ++n_at_l; alt = q; }
+  if (wb.pos) {
+    // the passes ordered by layer: those below l read the full cache in one launch,
+    // those starting at l (the last ones) their own compressed prompt cache
+    const int full = wb.n - n_at_l;
+    if (full > 0) {
+      SeqTable ft = *wb.bt;
+      ft.n = full * wb.wst->n;
+      ft.rows = (int32_t)(full * wb.rw);
+      KvPrefix pk = cache_prefix(m, *wb.wn, *wb.pst, l, nullptr);
+      pk.n_seq = wb.wst->n;
+      Timed t("attention", s);
+      RK_TRY(launch_attention(b.qkv, m->qkv_cols, b.att, m->attn_cols, ft, c.n_heads, c.n_kv_heads, c.head_dim,
+                              m->bf16, s, &pk));
+    }
+    const char* kv_l = (const char*)wb.wn->kv + (size_t)l * Rp * kc * a;
+    for (int q = full; q < wb.n; ++q) {
+      RK_TRY(launch_prefix_gather(kv_l, kc, wb.pst->n, wb.pst->max_len, c.n_kv_heads, c.head_dim, wb.pos[q],
+                                  wb.seq_stride, wb.n_keep, b.cpre, s));
+      KvPrefix pk{};
+      pk.alt_pass = -1;
+      pk.k = (const bf16_t*)b.cpre;
+      pk.v = (const bf16_t*)b.cpre + kc / 2;
+      pk.ldk = pk.ldv = kc;
+      pk.P = wb.n_keep;
+      Timed t("attention", s);
+      RK_TRY(launch_attention((const char*)b.qkv + (size_t)q * wb.rw * m->qkv_cols * a, m->qkv_cols,
+                              (char*)b.att + (size_t)q * wb.rw * m->attn_cols * a, m->attn_cols, *wb.wst, c.n_heads,
+                              c.n_kv_heads, c.head_dim, m->bf16, s, &pk));
+    }
+    return RK_OK;
+  }
   if (n_at_l <= 1) {
     // one launch over every pass's window rows; at most one pass reads perturbed Values
     KvPrefix pk = cache_prefix(m, *wb.wn, *wb.pst, l, nullptr);
@@ -601,6 +638,10 @@ static rk_status batch_attention(const rk_model* m, int l, const Bufs& b, const 
   return RK_OK;
 }
 
+static rk_status window_compressed_final(const rk_model* m, const SeqTable& pst, const SeqTable& wst, const Win& wn,
+                                         int layer, const int32_t* pos, int64_t seq_stride, int b, void* xf_out,
+                                         const Bufs& bf, hipStream_t s);
+
 // A group of cached-window passes, layer-synchronously (the survey's pass
 // batching): the passes, ordered by their perturbed layer, join the batch at that
 // layer from the window's cached block input, and from then on every norm,
@@ -612,7 +653,8 @@ static rk_status batch_attention(const rk_model* m, int l, const Bufs& b, const 
 // must hold the window positions; it does again on return.
 static rk_status window_group_final(const rk_model* m, const SeqTable& pst, const SeqTable& wst, const Win& wn,
                                     int G, const int* layers, const float* alphas, const rk_perturb_params* p,
-                                    int64_t max_rows, void* xp, const Bufs& b, hipStream_t s) {
+                                    int64_t max_rows, void* xp, const Bufs& b, hipStream_t s,
+                                    const int32_t* const* pos = nullptr, int64_t seq_stride = 0, int n_keep = 0) {
   const rk_model_config& c = m->cfg;
   const int64_t d = c.d_model, Rw = wst.rows, xstride = pad_rows(Rw) * d * act_bytes(m);
   const int L = c.n_layers, P = pst.max_len;
@@ -620,8 +662,9 @@ static rk_status window_group_final(const rk_model* m, const SeqTable& pst, cons
   B = std::min(B, RK_MAX_BATCH_SEQS / wst.n);
   if (B < 2) {
     for (int k = 0; k < G; ++k) {
-      rk_status e = window_perturbed_final(m, pst, wst, wn, layers[k], alphas[k], p, (char*)xp + (size_t)k * xstride,
-                                           b, s);
+      void* xk = (char*)xp + (size_t)k * xstride;
+      rk_status e = pos ? window_compressed_final(m, pst, wst, wn, layers[k], pos[k], seq_stride, n_keep, xk, b, s)
+                        : window_perturbed_final(m, pst, wst, wn, layers[k], alphas[k], p, xk, b, s);
       if (e != RK_OK) return e;
     }
     return RK_OK;
@@ -633,9 +676,11 @@ static rk_status window_group_final(const rk_model* m, const SeqTable& pst, cons
     const int cb = std::min(B, G - c0);
     int lay[RK_MAX_GROUP];
     float al[RK_MAX_GROUP];
+    const int32_t* ps[RK_MAX_GROUP];
     for (int q = 0; q < cb; ++q) {
       lay[q] = layers[order[c0 + q]];
-      al[q] = alphas[order[c0 + q]];
+      al[q] = alphas ? alphas[order[c0 + q]] : 0.0f;
+      ps[q] = pos ? pos[order[c0 + q]] : nullptr;
     }
     // batch table: sequence i of pass slot q at rows q * Rw + wst.off[i]
     SeqTable bst = wst;
@@ -655,7 +700,7 @@ static rk_status window_group_final(const rk_model* m, const SeqTable& pst, cons
       SeqTable at = bst;   // the active passes' rows
       at.n = active * wst.n;
       at.rows = (int32_t)(active * Rw);
-      const WinBatch wb{&wn, &pst, &wst, &at, active, lay, al, p, Rw};
+      const WinBatch wb{&wn, &pst, &wst, &at, active, lay, al, p, Rw, pos ? ps : nullptr, seq_stride, n_keep};
       rk_status e = run_block(m, j, b.h, b.h, b, at, nullptr, s, nullptr, nullptr, nullptr, &wb);
       if (e != RK_OK) return e;
     }
@@ -1145,6 +1190,45 @@ rk_status rk_compression_damage(const rk_model* m, const rk_batch* batch, int32_
   float* kl = kl_pos ? kl_pos : b.kl;
   if ((e = score_group(m, wst, wn.w, b.xp, 1, false, b.logits_p, kl, b, s)) != RK_OK) return e;
   RK_TRY(launch_window_mean(kl, wst.rows, 1, wst, 0, d_out, s));
+  return RK_OK;
+}
+
+rk_status rk_compression_damage_layers(const rk_model* m, const rk_batch* batch, int32_t window_start,
+                                       const int32_t* layers, int32_t n_sel, const int32_t* positions,
+                                       int64_t layer_stride, int64_t seq_stride, int32_t n_keep, const void* state,
+                                       size_t state_bytes, float* d_out, float* kl_pos, void* workspace,
+                                       size_t ws_bytes, void* stream) {
+  rk_status e = check_batch(m, batch);
+  if (e != RK_OK) return e;
+  if ((e = check_window_model(m)) != RK_OK) return e;
+  if (!layers || !positions || !state || !d_out || !workspace) {
+    set_error("null layers, positions, state, d_out or workspace");
+    return RK_ERR_ARG;
+  }
+  if (n_sel < 1 || n_sel > RK_MAX_GROUP) { set_error("n_layers must be in [1, %d]", RK_MAX_GROUP); return RK_ERR_ARG; }
+  for (int k = 0; k < n_sel; ++k)
+    if (layers[k] < 0 || layers[k] >= m->cfg.n_layers) { set_error("layer %d out of range", layers[k]); return RK_ERR_ARG; }
+  if (n_keep < 1 || n_keep > window_start) { set_error("n_keep must be in [1, window_start]"); return RK_ERR_ARG; }
+  if (seq_stride < (int64_t)m->cfg.n_kv_heads * n_keep) { set_error("seq_stride below n_kv_heads * n_keep"); return RK_ERR_ARG; }
+  if (layer_stride < 0) { set_error("layer_stride must be >= 0"); return RK_ERR_ARG; }
+  SeqTable st, pst, wst;
+  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  if ((e = window_tables(st, window_start, &pst, &wst)) != RK_OK) return e;
+  if (state_bytes < win_plan(m, st.rows).total) { set_error("window state too small"); return RK_ERR_WORKSPACE; }
+  const WsPlan wp = ws_plan(m, st.rows, n_sel, RK_FLAG_CACHED_WINDOW);
+  if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
+  const Bufs b = carve(wp, workspace);
+  const Win wn = win_view(m, st.rows, state);
+  hipStream_t s = (hipStream_t)stream;
+  RK_TRY(launch_rope_table(b.rope, b.rope_pos, wst, m->cfg.head_dim, m->cfg.rope_theta, s, window_start));
+  const int32_t* ps[RK_MAX_GROUP];
+  for (int k = 0; k < n_sel; ++k) ps[k] = positions + (int64_t)layers[k] * layer_stride;
+  if ((e = window_group_final(m, pst, wst, wn, n_sel, layers, nullptr, nullptr, st.rows, b.xp, b, s, ps, seq_stride,
+                              n_keep)) != RK_OK)
+    return e;
+  float* kl = kl_pos ? kl_pos : b.kl;
+  if ((e = score_group(m, wst, wn.w, b.xp, n_sel, false, b.logits_p, kl, b, s)) != RK_OK) return e;
+  RK_TRY(launch_window_mean(kl, wst.rows, n_sel, wst, 0, d_out, s));
   return RK_OK;
 }
 

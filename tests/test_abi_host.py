@@ -351,6 +351,42 @@ def test_compression_damage_validates_before_launching():
     lib.rk_model_destroy(h32)
 
 
+def test_compression_damage_layers_validates_before_launching():
+    lib = rk.load()
+    fake = ctypes.c_void_p(0x1000)
+    offs = np.array([0, 100, 250], dtype=np.int64)
+    batch = rk._Batch(fake, offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 2, 0)
+    big = 1 << 40
+    st, h = _create(_FakeCfg())
+    assert st == rk.RK_OK
+
+    def call(layers=(0, 1), P=50, keep=10, lstride=20, stride=40, sb=big, wb=big, pos=fake):
+        lay = (ctypes.c_int32 * max(1, len(layers)))(*layers)
+        return lib.rk_compression_damage_layers(h, ctypes.byref(batch), P, lay, len(layers), pos, lstride, stride,
+                                                keep, fake, sb, fake, None, fake, wb, None)
+    assert call(layers=()) == rk.RK_ERR_ARG               # no layer
+    assert call(layers=tuple([0, 1] * 9)) == rk.RK_ERR_ARG  # more than a group holds
+    assert call(layers=(0, 2)) == rk.RK_ERR_ARG           # layer out of range
+    assert call(layers=(-1,)) == rk.RK_ERR_ARG
+    assert call(keep=0) == rk.RK_ERR_ARG
+    assert call(keep=51) == rk.RK_ERR_ARG
+    assert call(stride=19) == rk.RK_ERR_ARG
+    assert call(lstride=-1) == rk.RK_ERR_ARG
+    assert call(pos=None) == rk.RK_ERR_ARG
+    assert call(P=100) == rk.RK_ERR_SHAPE
+    assert call(sb=16) == rk.RK_ERR_WORKSPACE
+    assert call(wb=16) == rk.RK_ERR_WORKSPACE
+    # the workspace of a two-layer call is that of a group of two cached-window passes
+    need = lib.rk_workspace_size(h, 250, 2, rk.RK_FLAG_CACHED_WINDOW)
+    assert need > lib.rk_workspace_size(h, 250, 1, rk.RK_FLAG_CACHED_WINDOW)
+    lib.rk_model_destroy(h)
+    st, h32 = _create(_FakeCfg(dtype="f32"))
+    lay = (ctypes.c_int32 * 1)(0)
+    assert lib.rk_compression_damage_layers(h32, ctypes.byref(batch), 50, lay, 1, fake, 20, 20, 10, fake, big, fake,
+                                            None, fake, big, None) == rk.RK_ERR_UNSUPPORTED
+    lib.rk_model_destroy(h32)
+
+
 def test_local_signal_flag_validates_before_launching():
     """RK_FLAG_LOCAL_SIGNAL: no logits, not with the unfused-KL flag, its own
     workspace size (the last block's clean output, no LM-head partials)."""

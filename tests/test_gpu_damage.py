@@ -118,3 +118,41 @@ def test_snapkv_selection_feeds_the_damage_and_spearman():
     rho = rk.spearman(s, D)
     log(f"damage D = {np.array(D)}, sensitivity s = {s}, Spearman rho = {rho:.3f}")
     assert np.isnan(rho) or -1.0 <= rho <= 1.0
+
+
+@pytest.mark.parametrize("lens,P,keep,layers", [
+    ([260, 300], 200, 37, [2, 0, 1]),        # three windows fit the rows: one layer-synchronous batch
+    ([260, 300], 200, 64, [1, 2, 1, 0, 2]),  # repeated layers, two batches
+    ([200, 260], 70, 23, [0, 2]),            # window longer than half the rows: one pass at a time
+])
+def test_damage_layers_equals_single_layer_calls(lens, P, keep, layers):
+    """rk_compression_damage_layers evaluates its layers together (passes join at
+    their layer, the projections run over all joined passes' window rows); each
+    layer's d and window KL are bitwise those of rk_compression_damage."""
+    import torch
+    cfg = CASES[0][0]
+    L, Hkv, n = cfg.n_layers, cfg.n_kv_heads, len(lens)
+    W = F.make_weights(cfg)
+    run = Runner(cfg, W)
+    toks = F.make_tokens(F.make_workload("dmgl", cfg, lens, seed_id=43))
+    batch = make_batch(toks)
+    state, ws1 = _state(run, batch, P)
+    # the SnapKV output layout: [sequence][layer][KV head][keep]
+    pos = np.stack([F.random_keep(n, Hkv, P, keep, seed_id=100 + l) for l in range(L)], axis=1)
+    pos_d = torch.from_numpy(np.ascontiguousarray(pos).reshape(-1)).cuda()
+    G = len(layers)
+    Rw = batch.rows - n * P
+    import paper_2608_08684_amd as rk
+    wsG = empty_bytes(run.model.workspace_size(batch.rows, G, rk.RK_FLAG_CACHED_WINDOW))
+    d = torch.empty(G, n, dtype=torch.float32, device="cuda")
+    kl = torch.empty(G, Rw, dtype=torch.float32, device="cuda")
+    run.model.compression_damage_layers(batch, P, layers, pos_d, Hkv * keep, keep, state, d, wsG,
+                                        seq_stride=L * Hkv * keep, kl_pos=kl)
+    torch.cuda.synchronize()
+    d, kl = d.cpu().numpy().astype(np.float64), kl.cpu().numpy().astype(np.float64)
+    for k, l in enumerate(layers):
+        d1, kl1 = _damage(run, batch, P, l, pos_d[l * Hkv * keep:], keep, state, ws1, seq_stride=L * Hkv * keep)
+        np.testing.assert_array_equal(d[k], d1, err_msg=f"layer {l} (slot {k}): d")
+        np.testing.assert_array_equal(kl[k], kl1, err_msg=f"layer {l} (slot {k}): window KL")
+        assert np.all(d1 > 0)
+    log(f"lens {lens} P {P} keep {keep} layers {layers}: bitwise equal to single-layer calls; d = {d.tolist()}")
