@@ -55,7 +55,9 @@ typedef enum {
   RK_ERR_SHAPE = -2,        /* inconsistent sizes (offsets, rows, batch too large)   */
   RK_ERR_WORKSPACE = -3,    /* workspace or clean-state buffer smaller than required */
   RK_ERR_HIP = -4,          /* a HIP call or kernel launch failed                    */
-  RK_ERR_UNSUPPORTED = -5   /* model shape outside what the kernels implement        */
+  RK_ERR_UNSUPPORTED = -5,  /* model shape outside what the kernels implement        */
+  RK_ERR_STATE = -6         /* (RK_FLAG_CHECK_STATE) the clean or window state was
+                               produced for another model, batch or window start   */
 } rk_status;
 
 typedef enum { RK_F32 = 0, RK_BF16 = 1 } rk_dtype;
@@ -99,6 +101,17 @@ typedef enum {
                                         distributions.  No layer after l and no LM
                                         head is evaluated.  Not combinable with
                                         RK_FLAG_UNFUSED_KL.                          */
+#define RK_FLAG_CHECK_STATE    0x20u /* rk_profile_layer only (ignored elsewhere):
+                                        before launching anything, compare the
+                                        record that rk_reference_forward /
+                                        rk_window_reference left in the state
+                                        (the model's config and weight pointers,
+                                        the batch's sequence lengths and a digest
+                                        of its tokens, the window start) with the
+                                        call's, and return RK_ERR_STATE if they
+                                        differ.  The record is read back to the
+                                        host, so the call synchronises the stream
+                                        (a debugging aid; not for graph capture). */
 
 /* Most sequences one batch (one call's rows) may hold. */
 #define RK_MAX_BATCH_SEQS 64
@@ -171,15 +184,18 @@ void rk_model_destroy(rk_model *m);
 /* ---------------------------------------------------------------- sizes */
 
 /* Bytes of the clean state of a batch of n_rows rows (Algorithm 1,
- * ReferencePredict): the fp32 input h_l of every block l ([L, n_rows, d_model])
- * and the final normalised hidden state ([n_rows, d_model] in the model dtype).  */
+ * ReferencePredict): the fp32 input h_l of every block l ([L, n_rows, d_model]),
+ * the final normalised hidden state ([n_rows, d_model] in the model dtype), the
+ * clean log-sum-exp and a 256-byte record of the model and batch that produced
+ * it (see RK_FLAG_CHECK_STATE).                                                 */
 size_t rk_clean_state_size(const rk_model *m, int64_t n_rows);
 
 /* Bytes of the state of the cached-window mode for a batch of at most n_rows
  * rows (rk_window_reference): the KV cache of every layer for the prefix rows
  * ([L, prefix rows, 2 * n_kv_heads * head_dim] bf16, K then V), and for the
  * window rows the fp32 input of every block, the final normalised hidden state
- * and the clean log-sum-exp of the LM head.  0 for invalid arguments.          */
+ * and the clean log-sum-exp of the LM head, and the 256-byte record of the
+ * model, batch and window start that produced it.  0 for invalid arguments.    */
 size_t rk_window_state_size(const rk_model *m, int64_t n_rows);
 
 /* Flag of rk_workspace_size: the workspace also holds one clean state

@@ -26,12 +26,12 @@ from typing import Optional, Sequence
 import numpy as np
 
 __all__ = ["RKError", "load", "Model", "Batch", "layer_budgets", "timing_begin", "timing_end", "LIB_PATH", "RK_FLAG_FULL_RECOMPUTE",
-           "RK_FLAG_UNFUSED_KL", "RK_FLAG_CACHED_WINDOW", "RK_FLAG_GRAPH", "RK_FLAG_LOCAL_SIGNAL", "RK_WS_CLEAN_STATE", "RK_MAX_BATCH_SEQS", "RK_MAX_GROUP",
+           "RK_FLAG_UNFUSED_KL", "RK_FLAG_CACHED_WINDOW", "RK_FLAG_GRAPH", "RK_FLAG_LOCAL_SIGNAL", "RK_FLAG_CHECK_STATE", "RK_WS_CLEAN_STATE", "RK_MAX_BATCH_SEQS", "RK_MAX_GROUP",
            "RK_POOL_MAX", "RK_POOL_AVG", "RK_SNAPKV_MAX_PREFIX", "snapkv_layout", "spearman"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librk.so")
 
-RK_OK, RK_ERR_ARG, RK_ERR_SHAPE, RK_ERR_WORKSPACE, RK_ERR_HIP, RK_ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
+RK_OK, RK_ERR_ARG, RK_ERR_SHAPE, RK_ERR_WORKSPACE, RK_ERR_HIP, RK_ERR_UNSUPPORTED, RK_ERR_STATE = 0, -1, -2, -3, -4, -5, -6
 RK_F32, RK_BF16 = 0, 1
 RK_ROUND_LARGEST_REMAINDER, RK_ROUND_NEAREST_EVEN = 0, 1
 RK_FLAG_FULL_RECOMPUTE = 0x1
@@ -39,6 +39,7 @@ RK_FLAG_UNFUSED_KL = 0x2
 RK_FLAG_CACHED_WINDOW = 0x4
 RK_FLAG_GRAPH = 0x8
 RK_FLAG_LOCAL_SIGNAL = 0x10
+RK_FLAG_CHECK_STATE = 0x20
 RK_WS_CLEAN_STATE = 0x100
 RK_MAX_BATCH_SEQS = 64
 RK_MAX_GROUP = 16
@@ -47,7 +48,7 @@ RK_POOL_AVG = 1
 RK_SNAPKV_MAX_PREFIX = 36864
 
 _STATUS = {0: "RK_OK", -1: "RK_ERR_ARG", -2: "RK_ERR_SHAPE", -3: "RK_ERR_WORKSPACE", -4: "RK_ERR_HIP",
-           -5: "RK_ERR_UNSUPPORTED"}
+           -5: "RK_ERR_UNSUPPORTED", -6: "RK_ERR_STATE"}
 
 
 class RKError(RuntimeError):

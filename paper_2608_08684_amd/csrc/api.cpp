@@ -35,6 +35,7 @@ struct rk_model {
   const float* final_norm;
   std::vector<const void*> w_qkv, w_o, w_gate_up, w_down;
   std::vector<const float*> attn_norm, mlp_norm;
+  uint64_t ident;   // digest of the config and the weight pointers (state tags)
 };
 
 namespace rk {
@@ -52,6 +53,14 @@ void set_error(const char* fmt, ...) {
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// FNV-1a (64-bit) over a byte range
+static const uint64_t kFnvBasis = 0xcbf29ce484222325ull;
+static uint64_t fnv(uint64_t h, const void* p, size_t n) {
+  const unsigned char* c = (const unsigned char*)p;
+  for (size_t i = 0; i < n; ++i) h = (h ^ c[i]) * 0x100000001b3ull;
+  return h;
+}
+
 static size_t act_bytes(const rk_model* m) { return m->bf16 ? 2 : 4; }
 
 // Buffers read as GEMM A operands hold whole 256-row tiles (the tile loads are
@@ -60,7 +69,7 @@ static int64_t pad_rows(int64_t R) { return (R + 255) / 256 * 256; }
 
 // ----------------------------------------------------------------------------- memory plans
 struct CleanPlan {
-  size_t h, xf, lse, total;
+  size_t h, xf, lse, tag, total;
 };
 
 static CleanPlan clean_plan(const rk_model* m, int64_t R) {
@@ -70,6 +79,7 @@ static CleanPlan clean_plan(const rk_model* m, int64_t R) {
   p.h = o;   o += align256((size_t)m->cfg.n_layers * R * d * 4);
   p.xf = o;  o += align256((size_t)pad_rows(R) * d * act_bytes(m));
   p.lse = o; o += align256((size_t)R * 4);
+  p.tag = o; o += 256;
   p.total = o;
   return p;
 }
@@ -79,7 +89,7 @@ static CleanPlan clean_plan(const rk_model* m, int64_t R) {
 // for the window rows the input of every block, the final hidden state and the
 // clean log-sum-exp.
 struct WinPlan {
-  size_t kv, h, xf, lse, total;
+  size_t kv, h, xf, lse, tag, total;
 };
 
 static int64_t kv_cols(const rk_model* m) { return 2 * (int64_t)m->cfg.n_kv_heads * m->cfg.head_dim; }
@@ -92,13 +102,14 @@ static WinPlan win_plan(const rk_model* m, int64_t R) {
   p.h = o;   o += align256((size_t)L * R * d * 4);
   p.xf = o;  o += align256((size_t)pad_rows(R) * d * act_bytes(m));
   p.lse = o; o += align256((size_t)R * 4);
+  p.tag = o; o += 256;
   p.total = o;
   return p;
 }
 
 struct WsPlan {
-  size_t h, x, qkv, att, ff, xp, part, logits_c, logits_p, kl, rope, rope_pos, dbatch, sacc, vpert, cpre, hloc, clean,
-      total;
+  size_t h, x, qkv, att, ff, xp, part, logits_c, logits_p, kl, rope, rope_pos, dbatch, sacc, tag, vpert, cpre, hloc,
+      clean, total;
   bool unfused;
 };
 
@@ -137,6 +148,7 @@ static WsPlan ws_plan(const rk_model* m, int64_t R, int G, uint32_t flags) {
   p.rope_pos = o; o += align256((size_t)R * 4);
   p.dbatch = o;   o += align256((size_t)G * RK_MAX_BATCH_SEQS * 4);
   p.sacc = o;     o += align256((size_t)kMaxSAcc * 8);
+  p.tag = o;      o += 256;
   p.vpert = o;
   if (flags & RK_FLAG_CACHED_WINDOW) o += align256((size_t)R * (kv_cols(m) / 2) * a);
   p.cpre = o;   // a compressed prompt cache (K and V columns)
@@ -155,6 +167,7 @@ struct Bufs {
   float* h; void* x; void* qkv; void* att; void* ff; void* xp;
   float2* part; float* logits_c; float* logits_p; float* kl; float2* rope; int32_t* rope_pos; float* dbatch;
   double* sacc;
+  uint64_t* tag;
   void* vpert;
   void* cpre;
   float* hloc;
@@ -168,7 +181,7 @@ static Bufs carve(const WsPlan& p, void* ws) {
   u.xp = b + p.xp; u.part = (float2*)(b + p.part); u.logits_c = (float*)(b + p.logits_c);
   u.logits_p = (float*)(b + p.logits_p); u.kl = (float*)(b + p.kl); u.rope = (float2*)(b + p.rope);
   u.rope_pos = (int32_t*)(b + p.rope_pos);
-  u.dbatch = (float*)(b + p.dbatch); u.sacc = (double*)(b + p.sacc); u.vpert = b + p.vpert; u.cpre = b + p.cpre;
+  u.dbatch = (float*)(b + p.dbatch); u.sacc = (double*)(b + p.sacc); u.tag = (uint64_t*)(b + p.tag); u.vpert = b + p.vpert; u.cpre = b + p.cpre;
   u.hloc = (float*)(b + p.hloc); u.clean = b + p.clean;
   return u;
 }
@@ -774,6 +787,46 @@ static rk_status check_batch(const rk_model* m, const rk_batch* b) {
   return RK_OK;
 }
 
+// ----------------------------------------------------------------------------- state tags
+// Each state written by rk_reference_forward (window start -1) or
+// rk_window_reference records which model and batch produced it: the model
+// digest, the sequence lengths and the window start (host side), and a digest of
+// the tokens (device side).  RK_FLAG_CHECK_STATE compares the record with the
+// call's before anything is launched.
+static const uint64_t kTagMagic = 0x524B535441544501ull;
+
+static uint64_t host_ident(const rk_model* m, const SeqTable& st, int32_t window_start) {
+  uint64_t h = fnv(kFnvBasis, &m->ident, sizeof(m->ident));
+  h = fnv(h, &st.n, sizeof(st.n));
+  h = fnv(h, st.off, sizeof(int32_t) * (size_t)(st.n + 1));
+  return fnv(h, &window_start, sizeof(window_start));
+}
+
+static rk_status write_state_tag(const rk_model* m, const int32_t* tokens, const SeqTable& st, int32_t window_start,
+                                 void* tag, hipStream_t s) {
+  RK_TRY(launch_state_tag(tokens, st.rows, kTagMagic, host_ident(m, st, window_start), (uint64_t*)tag, s));
+  return RK_OK;
+}
+
+// Synchronises the stream: the two records are read back to the host.
+static rk_status check_state_tag(const rk_model* m, const int32_t* tokens, const SeqTable& st, int32_t window_start,
+                                 const void* tag, uint64_t* scratch, hipStream_t s) {
+  RK_TRY(launch_state_tag(tokens, st.rows, kTagMagic, host_ident(m, st, window_start), scratch, s));
+  uint64_t have[4], want[4];
+  RK_TRY(hipMemcpyAsync(have, tag, sizeof(have), hipMemcpyDeviceToHost, s));
+  RK_TRY(hipMemcpyAsync(want, scratch, sizeof(want), hipMemcpyDeviceToHost, s));
+  RK_TRY(hipStreamSynchronize(s));
+  if (have[0] != kTagMagic) {
+    set_error("the state was not written by rk_reference_forward or rk_window_reference");
+    return RK_ERR_STATE;
+  }
+  if (memcmp(have, want, sizeof(have)) != 0) {
+    set_error("the state belongs to another model, batch (tokens, lengths) or window start");
+    return RK_ERR_STATE;
+  }
+  return RK_OK;
+}
+
 static rk_status check_params(const rk_perturb_params* p) {
   if (!p) { set_error("null perturbation params"); return RK_ERR_ARG; }
   if (p->window_start < 0 || p->protect_head < 0 || p->protect_tail < 0) {
@@ -781,7 +834,7 @@ static rk_status check_params(const rk_perturb_params* p) {
     return RK_ERR_ARG;
   }
   if (p->flags & ~(RK_FLAG_FULL_RECOMPUTE | RK_FLAG_UNFUSED_KL | RK_FLAG_CACHED_WINDOW | RK_FLAG_GRAPH |
-                   RK_FLAG_LOCAL_SIGNAL)) {
+                   RK_FLAG_LOCAL_SIGNAL | RK_FLAG_CHECK_STATE)) {
     set_error("unknown flags");
     return RK_ERR_ARG;
   }
@@ -1012,6 +1065,18 @@ rk_status rk_model_create(const rk_model_config* cfg, const rk_model_weights* w,
   m->w_down.assign(w->w_down, w->w_down + c.n_layers);
   m->attn_norm.assign(w->attn_norm, w->attn_norm + c.n_layers);
   m->mlp_norm.assign(w->mlp_norm, w->mlp_norm + c.n_layers);
+  uint64_t h = kFnvBasis;
+  const int32_t dims[8] = {c.n_layers, c.d_model, c.n_heads, c.n_kv_heads, c.head_dim, c.d_ff, c.vocab, (int32_t)c.dtype};
+  h = fnv(h, dims, sizeof(dims));
+  h = fnv(h, &c.rope_theta, sizeof(float));
+  h = fnv(h, &c.rms_eps, sizeof(float));
+  const void* top[3] = {m->tok_emb, m->lm_head, m->final_norm};
+  h = fnv(h, top, sizeof(top));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const void* lw[6] = {m->w_qkv[l], m->w_o[l], m->w_gate_up[l], m->w_down[l], m->attn_norm[l], m->mlp_norm[l]};
+    h = fnv(h, lw, sizeof(lw));
+  }
+  m->ident = h;
   *out = m;
   return RK_OK;
 }
@@ -1041,7 +1106,9 @@ rk_status rk_window_reference(const rk_model* m, const rk_batch* batch, int32_t 
   const WsPlan wp = ws_plan(m, st.rows, 1, RK_FLAG_CACHED_WINDOW);
   if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
   const Bufs b = carve(wp, workspace);
-  return window_reference(m, batch->tokens, st, pst, wst, win_view(m, st.rows, state), b, (hipStream_t)stream);
+  hipStream_t s = (hipStream_t)stream;
+  if ((e = window_reference(m, batch->tokens, st, pst, wst, win_view(m, st.rows, state), b, s)) != RK_OK) return e;
+  return write_state_tag(m, batch->tokens, st, window_start, (char*)state + win_plan(m, st.rows).tag, s);
 }
 
 size_t rk_snapkv_state_size(const rk_model* m, int64_t n_rows, int32_t n_seqs, int32_t obs_window) {
@@ -1248,7 +1315,9 @@ rk_status rk_reference_forward(const rk_model* m, const rk_batch* batch, void* c
   const WsPlan wp = ws_plan(m, st.rows, 1, 0);
   if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
   const Bufs b = carve(wp, workspace);
-  return reference_forward(m, batch->tokens, st, clean_view(m, st.rows, clean_state), b, (hipStream_t)stream);
+  hipStream_t s = (hipStream_t)stream;
+  if ((e = reference_forward(m, batch->tokens, st, clean_view(m, st.rows, clean_state), b, s)) != RK_OK) return e;
+  return write_state_tag(m, batch->tokens, st, -1, (char*)clean_state + clean_plan(m, st.rows).tag, s);
 }
 
 rk_status rk_profile_layer(const rk_model* m, const rk_batch* batch, int32_t layer, float alpha,
@@ -1278,6 +1347,10 @@ rk_status rk_profile_layer(const rk_model* m, const rk_batch* batch, int32_t lay
     const Bufs b = carve(wp, workspace);
     const Win wn = win_view(m, st.rows, clean_state);
     hipStream_t s = (hipStream_t)stream;
+    if ((p->flags & RK_FLAG_CHECK_STATE) &&
+        (e = check_state_tag(m, batch->tokens, st, p->window_start,
+                             (const char*)clean_state + win_plan(m, st.rows).tag, b.tag, s)) != RK_OK)
+      return e;
     RK_TRY(launch_rope_table(b.rope, b.rope_pos, wst, m->cfg.head_dim, m->cfg.rope_theta, s, p->window_start));
     float* kl = kl_pos ? kl_pos : b.kl;
     if (local) {
@@ -1304,6 +1377,10 @@ rk_status rk_profile_layer(const rk_model* m, const rk_batch* batch, int32_t lay
   const Bufs b = carve(wp, workspace);
   const Clean cl = clean_view(m, st.rows, clean_state);
   hipStream_t s = (hipStream_t)stream;
+  if ((p->flags & RK_FLAG_CHECK_STATE) &&
+      (e = check_state_tag(m, batch->tokens, st, -1, (const char*)clean_state + clean_plan(m, st.rows).tag, b.tag,
+                           s)) != RK_OK)
+    return e;
   RK_TRY(launch_rope_table(b.rope, b.rope_pos, st, m->cfg.head_dim, m->cfg.rope_theta, s));
   float* kl = kl_pos ? kl_pos : b.kl;
   if (local) {

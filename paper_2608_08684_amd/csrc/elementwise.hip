@@ -273,6 +273,42 @@ hipError_t launch_value_noise(void* v, bool bf16, int64_t row_stride, const SeqT
                                protect_tail, s);
 }
 
+// --------------------------------------------------------------------------- state tag
+// The identity record of a clean or window state: {magic, host identity, token
+// digest, rows}.  The digest is a wrapping sum over positions i of
+// splitmix64((i << 32) | token_i) (the splitmix64 finaliser of Steele, Lea and
+// Flood), so it depends on every token and its position and not on the order of
+// the summation.
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {
+  z += 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+__global__ __launch_bounds__(256) void state_tag_kernel(const int32_t* __restrict__ tok, int64_t rows,
+                                                        uint64_t magic, uint64_t host, uint64_t* __restrict__ out) {
+  __shared__ uint64_t part[256];
+  uint64_t acc = 0;
+  for (int64_t i = threadIdx.x; i < rows; i += 256) acc += mix64(((uint64_t)i << 32) | (uint32_t)tok[i]);
+  part[threadIdx.x] = acc;
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if ((int)threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x < 4) {
+    const uint64_t v[4] = {magic, host, part[0], (uint64_t)rows};
+    out[threadIdx.x] = v[threadIdx.x];
+  }
+}
+
+hipError_t launch_state_tag(const int32_t* tokens, int64_t rows, uint64_t magic, uint64_t host, uint64_t* out,
+                            hipStream_t s) {
+  state_tag_kernel<<<1, 256, 0, s>>>(tokens, rows, magic, host, out);
+  return hipGetLastError();
+}
+
 // --------------------------------------------------------------------------- means
 // d[g * n + k] = mean of kl[g * kl_stride + r] for r in [off[k] + window_start, off[k+1]);
 // 0 for an empty window.  Fixed-order double accumulation.

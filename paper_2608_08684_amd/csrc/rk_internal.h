@@ -147,6 +147,9 @@ hipError_t launch_kl_logits(const float* lc, const float* lp, int64_t pass_strid
 hipError_t launch_local_response(const float* hp, const float* hc, int rows, int d, float* r, hipStream_t s);
 
 // dbatch[g * n_seqs + k] = mean of kl[g * kl_stride + r] over r in [off[k] + window_start, off[k+1]).
+// {magic, host, digest of tokens[0, rows), rows} into out[0..3] (one block)
+hipError_t launch_state_tag(const int32_t* tokens, int64_t rows, uint64_t magic, uint64_t host, uint64_t* out,
+                            hipStream_t s);
 hipError_t launch_window_mean(const float* kl, int64_t kl_stride, int G, const SeqTable& st, int window_start,
                               float* dbatch, hipStream_t s);
 

@@ -387,6 +387,23 @@ def test_compression_damage_layers_validates_before_launching():
     lib.rk_model_destroy(h32)
 
 
+def test_unknown_flag_bits_are_rejected():
+    lib = rk.load()
+    st, h = _create(_FakeCfg())
+    assert st == rk.RK_OK
+    fake = ctypes.c_void_p(0x1000)
+    offs = np.array([0, 100, 250], dtype=np.int64)
+    batch = rk._Batch(fake, offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 2, 0)
+    big = 1 << 40
+    bad = rk._Params(2, 0, 0, 0, 0x40)
+    assert lib.rk_profile_layer(h, ctypes.byref(batch), 0, 0.1, ctypes.byref(bad), fake, big, fake, None, None,
+                                fake, big, None) == rk.RK_ERR_ARG
+    # the state record adds 256 bytes to both states
+    L, d = 2, 256
+    assert lib.rk_clean_state_size(h, 250) >= L * 250 * d * 4 + 256
+    lib.rk_model_destroy(h)
+
+
 def test_local_signal_flag_validates_before_launching():
     """RK_FLAG_LOCAL_SIGNAL: no logits, not with the unfused-KL flag, its own
     workspace size (the last block's clean output, no LM-head partials)."""
