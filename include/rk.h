@@ -79,7 +79,9 @@ typedef enum {
                                         while every argument (device pointers, sizes,
                                         host arrays) stays the same;
                                         one graph per process, replaced when the
-                                        arguments change.  Saves the per-launch
+                                        arguments change (graphed calls from
+                                        several threads are serialised while
+                                        they record or launch).  Saves the per-launch
                                         overhead of the ~10^3-10^4 kernels of a
                                         profile.  With kernel timing on, each graphed
                                         call needs its own rk_timing_begin.         */

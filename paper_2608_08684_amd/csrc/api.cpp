@@ -21,6 +21,7 @@
 
 #include <algorithm>
 #include <functional>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -925,9 +926,11 @@ struct GraphCache {
   size_t timed = 0;   // timing event pairs inside the graph
 };
 static GraphCache g_graph;
+static std::mutex g_graph_mu;   // the cache is shared by every thread of the process
 
 template <class F>
 static rk_status run_graphed(std::vector<uint64_t> key, F&& run, hipStream_t s) {
+  std::lock_guard<std::mutex> lock(g_graph_mu);
   key.push_back(g_timing.on ? std::hash<std::string>()(g_timing.family) : 0);
   if (g_timing.on && g_timing.used != 0) {
     set_error("a graphed call needs a fresh timing session (rk_timing_begin) when timing is on");
