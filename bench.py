@@ -187,6 +187,28 @@ def family_flops(fam: str, cfg, rows: int, n_vocab_pass: int) -> float:
     raise ValueError(fam)
 
 
+def step_flops(cfg, lens, layers, alphas, P: int = 0, local: bool = False) -> float:
+    """Algorithmic MFMA work of one profile call: the clean pass (every layer over
+    every row, plus the clean LM head over the evaluated rows) and, per pass (alpha, l), layers l .. L-1
+    over the evaluated rows with their causal attention plus the perturbed LM
+    head (the clean logits the fused kernel recomputes are not counted).  In the
+    cached-window mode the evaluated rows are [P, T_i) attending to the whole
+    prefix; with the layer-local signal a pass runs layer l only, and no LM head."""
+    d, H, Hkv, dh, ff, V, L = cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.d_ff, cfg.vocab, cfg.n_layers
+    lin = 2.0 * d * (H + 2 * Hkv) * dh + 2.0 * H * dh * d + 2.0 * d * 2 * ff + 2.0 * ff * d   # per row and layer
+
+    def attn(q0):   # causal attention of query rows [q0, T) of every sequence, one layer
+        return sum(4.0 * H * dh * ((T * (T + 1) - q0 * (q0 + 1)) / 2) for T in lens)
+    rows_all, rows_eval = sum(lens), sum(T - P for T in lens)
+    clean = L * (lin * rows_all + attn(0)) + (0.0 if local else 2.0 * rows_eval * d * V)
+    per_layer_pass = lin * rows_eval + attn(P)
+    if local:
+        passes = len(alphas) * len(layers) * per_layer_pass
+    else:
+        passes = len(alphas) * sum((L - l) * per_layer_pass + 2.0 * rows_eval * d * V for l in layers)
+    return clean + passes
+
+
 def cpu_baseline_window(w, W, toks, window: int):
     """Oracle cached-window profile of sequence 0 (prefix prefill and window
     reference included), every layer, the largest alpha."""
@@ -693,6 +715,11 @@ def main():
             "kernel": args.family, "launches": launches, "avg_ms": round(fam_avg_ms, 4),
             "flop_per_launch": flops}
     log(f"{args.family}: {launches} launches, avg {fam_avg_ms:.4f} ms, {achieved:.1f} TFLOP/s")
+    # the whole step's MFMA utilisation: its algorithmic work over the step time
+    sf = step_flops(cfg, w.lengths(), layers, alphas, P, local)
+    util = {"step_tflop": round(sf / 1e12, 2), "achieved": round(sf / (ms_per_step / 1e3) / 1e12, 1),
+            "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(sf / (ms_per_step / 1e3) / 1e12 / BF16_PEAK_TFLOPS, 4)}
 
     mode = "" if window == 0 else f"; cached window: prefix {P}, window {window} per sequence"
     mode += "; layer-local signal (w/o DS ablation)" if local else ""
@@ -719,6 +746,7 @@ def main():
                                f"alpha {alphas}; all layers; ratios {list(w.ratios)}; budgets {budgets}{mode}",
                    "perturbed_token_layers_per_step": tokens_layers, "profile_wall_ms": round(ms_per_step, 3)},
         "roofline": roof,
+        "mfma_util": util,
     }
     if not args.no_cpu_baseline:
         if window == 0:
