@@ -54,6 +54,10 @@ void set_error(const char* fmt, ...) {
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Rows of a batch are int32 throughout (offsets, kernel row indices); size
+// queries beyond that return 0 so no buffer plan can overflow.
+static const int64_t kMaxRows = 0x7fffffff;
+
 // FNV-1a (64-bit) over a byte range
 static const uint64_t kFnvBasis = 0xcbf29ce484222325ull;
 static uint64_t fnv(uint64_t h, const void* p, size_t n) {
@@ -1087,12 +1091,12 @@ rk_status rk_model_create(const rk_model_config* cfg, const rk_model_weights* w,
 void rk_model_destroy(rk_model* m) { delete m; }
 
 size_t rk_clean_state_size(const rk_model* m, int64_t n_rows) {
-  if (!m || n_rows < 1) return 0;
+  if (!m || n_rows < 1 || n_rows > kMaxRows) return 0;
   return clean_plan(m, n_rows).total;
 }
 
 size_t rk_window_state_size(const rk_model* m, int64_t n_rows) {
-  if (!m || n_rows < 1 || !m->bf16) return 0;
+  if (!m || n_rows < 1 || n_rows > kMaxRows || !m->bf16) return 0;
   return win_plan(m, n_rows).total;
 }
 
@@ -1115,12 +1119,12 @@ rk_status rk_window_reference(const rk_model* m, const rk_batch* batch, int32_t 
 }
 
 size_t rk_snapkv_state_size(const rk_model* m, int64_t n_rows, int32_t n_seqs, int32_t obs_window) {
-  if (!m || !m->bf16 || n_rows < 1 || n_seqs < 1 || obs_window < 1) return 0;
+  if (!m || !m->bf16 || n_rows < 1 || n_rows > kMaxRows || n_seqs < 1 || obs_window < 1) return 0;
   return snap_plan(m, n_rows, n_seqs, obs_window).total;
 }
 
 size_t rk_snapkv_workspace_size(const rk_model* m, int64_t n_rows, int32_t n_seqs, int32_t obs_window) {
-  if (!m || !m->bf16 || n_rows < 1 || n_seqs < 1 || obs_window < 1) return 0;
+  if (!m || !m->bf16 || n_rows < 1 || n_rows > kMaxRows || n_seqs < 1 || obs_window < 1) return 0;
   return std::max(ws_plan(m, n_rows, 1, 0).total, snap_scratch(m, n_rows, n_seqs, obs_window).total);
 }
 
@@ -1303,7 +1307,7 @@ rk_status rk_compression_damage_layers(const rk_model* m, const rk_batch* batch,
 }
 
 size_t rk_workspace_size(const rk_model* m, int64_t max_rows, int32_t max_group, uint32_t flags) {
-  if (!m || max_rows < 1 || max_group < 1 || max_group > RK_MAX_GROUP) return 0;
+  if (!m || max_rows < 1 || max_rows > kMaxRows || max_group < 1 || max_group > RK_MAX_GROUP) return 0;
   return ws_plan(m, max_rows, max_group, flags).total;
 }
 
@@ -1422,7 +1426,7 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
   for (int a = 0; a < n_alpha; ++a)
     if (!(alphas[a] >= 0.0f) || !isfinite(alphas[a])) { set_error("alphas must be finite and >= 0"); return RK_ERR_ARG; }
   if (max_group < 1 || max_group > RK_MAX_GROUP) { set_error("max_group must be in [1, %d]", RK_MAX_GROUP); return RK_ERR_ARG; }
-  if (max_rows < 1) { set_error("max_rows must be >= 1"); return RK_ERR_ARG; }
+  if (max_rows < 1 || max_rows > kMaxRows) { set_error("max_rows must be in [1, 2^31 - 1]"); return RK_ERR_ARG; }
   const int N = calib->n_seqs;
   for (int i = 0; i < N; ++i) {
     const int64_t len = calib->offsets[i + 1] - calib->offsets[i];

@@ -387,6 +387,27 @@ def test_compression_damage_layers_validates_before_launching():
     lib.rk_model_destroy(h32)
 
 
+def test_size_queries_reject_rows_beyond_int32():
+    lib = rk.load()
+    st, h = _create(_FakeCfg())
+    assert st == rk.RK_OK
+    big = 1 << 31
+    assert lib.rk_clean_state_size(h, big) == 0 and lib.rk_clean_state_size(h, big - 1) > 0
+    assert lib.rk_window_state_size(h, big) == 0
+    assert lib.rk_workspace_size(h, big, 1, 0) == 0 and lib.rk_workspace_size(h, 1 << 62, 16, 0) == 0
+    assert lib.rk_snapkv_state_size(h, big, 1, 16) == 0
+    assert lib.rk_snapkv_workspace_size(h, big, 1, 16) == 0
+    fake = ctypes.c_void_p(0x1000)
+    offs = np.array([0, 100, 250], dtype=np.int64)
+    batch = rk._Batch(fake, offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 2, 0)
+    lay = (ctypes.c_int32 * 1)(0)
+    alp = (ctypes.c_float * 1)(0.1)
+    p = rk._Params(2, 0, 0, 0, 0)
+    assert lib.rk_sensitivity_profile(h, ctypes.byref(batch), lay, 1, alp, 1, ctypes.byref(p), 1 << 40, 1, fake, None,
+                                      fake, 1 << 60, None) == rk.RK_ERR_ARG
+    lib.rk_model_destroy(h)
+
+
 def test_unknown_flag_bits_are_rejected():
     lib = rk.load()
     st, h = _create(_FakeCfg())
