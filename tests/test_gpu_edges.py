@@ -8,7 +8,9 @@
   exactly 0;
 * a calibration set of 70 sequences, more than one batch holds (64), split by
   rk_sensitivity_profile into consecutive batches: s is the unweighted mean of
-  the 70 per-sequence values, each equal to its single-batch value.
+  the 70 per-sequence values, each equal to its single-batch value;
+* the largest group (16 passes scored by one LM-head + KL launch) against
+  smaller groups and single-layer calls, bit for bit.
 """
 import numpy as np
 import pytest
@@ -80,3 +82,36 @@ def test_more_sequences_than_one_batch():
     # the first 64 as their own batch: the same per-sequence values
     s64, d64 = run.profile(make_batch(toks[:64]), layers, [0.1], max_rows=sum(lens), max_group=2)
     assert np.array_equal(d64[0], d[0][:64])
+
+
+def test_largest_group_in_one_lm_launch():
+    """16 passes (8 layers x 2 alphas) scored by one fused LM-head + KL launch
+    (RK_MAX_GROUP) give the same d as groups of 5, 5, 5, 1 and as single-layer
+    calls (the vocab-tile order of every pass's partials is the same), and the
+    oracle's on sampled cells; a group above RK_MAX_GROUP is refused."""
+    import paper_2608_08684_amd as rk
+    cfg = F.small_model(n_layers=8, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=512, vocab=1024,
+                        rope_theta=1.0e4, dtype="bf16")
+    W = F.make_weights(cfg)
+    run = Runner(cfg, W)
+    lens = [150, 90]
+    toks = F.make_tokens(F.make_workload("g16", cfg, lens, seed_id=91))
+    batch = make_batch(toks)
+    layers = list(range(cfg.n_layers))
+    alphas = [0.05, 0.1]
+    s16, d16 = run.profile(batch, layers, alphas, max_group=rk.RK_MAX_GROUP)
+    s5, d5 = run.profile(batch, layers, alphas, max_group=5)
+    np.testing.assert_array_equal(d16, d5)
+    np.testing.assert_array_equal(s16, s5)
+    cs = run.clean(batch)
+    for a, alpha in enumerate(alphas):
+        for l in (0, 3, 7):
+            d1, _, _ = run.layer(batch, cs, l, alpha)
+            np.testing.assert_array_equal(d1, d16[a, :, l])
+    m = OM.Model(cfg, f32_weights(cfg, W), np.float64)
+    st0 = OM.clean_pass(m, toks[0])
+    for l in (0, 7):
+        ref, _ = OPR.profile_layer(m, st0, toks[0], 0, l, OPR.PerturbParams(0.1))
+        assert_kl_close([d16[1, 0, l]], [ref], f"group of 16: layer {l}")
+    assert run.model.workspace_size(batch.rows, rk.RK_MAX_GROUP + 1, 0) == 0
+    log(f"group of {rk.RK_MAX_GROUP}: d equal to groups of 5 and to single-layer calls; s = {s16[1].tolist()}")
