@@ -77,42 +77,91 @@ hipError_t launch_copy_cols(const void* src, int64_t ld_src_bytes, int64_t off_b
 }
 
 // --------------------------------------------------------------------------- RMSNorm
-// One wave per row: out = h / sqrt(mean(h^2) + eps) * g.  fp32 in, act out.
-template <typename O>
+// One wave per row: out = h / sqrt(mean(h^2) + eps) * g.  fp32 in, act out.  With
+// NV > 0 the row stays in registers (NV float4 per lane) between the sum of
+// squares and the scaled store, and each lane writes its four outputs with one
+// 16-byte (fp32) or 8-byte (bf16) store; NV = 0 streams the row twice (any d).
+__device__ __forceinline__ void store4v(float* p, float a, float b, float c, float d) {
+  *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+}
+__device__ __forceinline__ void store4v(bf16_t* p, float a, float b, float c, float d) {
+  uint2 u;
+  u.x = (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+  u.y = (uint32_t)f2bf(c) | ((uint32_t)f2bf(d) << 16);
+  *reinterpret_cast<uint2*>(p) = u;
+}
+
+template <typename O, int NV>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ h, const float* __restrict__ g,
                                                       O* __restrict__ out, int rows, int d, float eps) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
   const float4* hr = reinterpret_cast<const float4*>(h + (int64_t)row * d);
-  const int n4 = d >> 2;
-  float ss = 0.f;
-  for (int i = lane; i < n4; i += 64) {
-    float4 v = hr[i];
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-  }
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
-  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
   const float4* g4 = reinterpret_cast<const float4*>(g);
   O* orow = out + (int64_t)row * d;
-  for (int i = lane; i < n4; i += 64) {
-    float4 v = hr[i], w = g4[i];
-    Act<O>::store(orow + 4 * i + 0, v.x * inv * w.x);
-    Act<O>::store(orow + 4 * i + 1, v.y * inv * w.y);
-    Act<O>::store(orow + 4 * i + 2, v.z * inv * w.z);
-    Act<O>::store(orow + 4 * i + 3, v.w * inv * w.w);
+  const int n4 = d >> 2;
+  float ss = 0.f;
+  if constexpr (NV > 0) {
+    float4 v[NV];
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int i = lane + 64 * j;
+      v[j] = i < n4 ? hr[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int j = 0; j < NV; ++j) ss += v[j].x * v[j].x + v[j].y * v[j].y + v[j].z * v[j].z + v[j].w * v[j].w;
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
+    const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int i = lane + 64 * j;
+      if (i < n4) {
+        const float4 w = g4[i];
+        store4v(orow + 4 * i, v[j].x * inv * w.x, v[j].y * inv * w.y, v[j].z * inv * w.z, v[j].w * inv * w.w);
+      }
+    }
+  } else {
+    for (int i = lane; i < n4; i += 64) {
+      const float4 v = hr[i];
+      ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
+    const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+    for (int i = lane; i < n4; i += 64) {
+      const float4 v = hr[i], w = g4[i];
+      store4v(orow + 4 * i, v.x * inv * w.x, v.y * inv * w.y, v.z * inv * w.z, v.w * inv * w.w);
+    }
+  }
+}
+
+template <typename O>
+static void rmsnorm_go(const float* h, const float* g, O* out, int rows, int d, float eps, hipStream_t s) {
+  const int blocks = (rows + 3) / 4;
+  const int nv = (d / 4 + 63) / 64;   // float4 per lane
+  switch (nv) {
+    case 1: rmsnorm_kernel<O, 1><<<blocks, 256, 0, s>>>(h, g, out, rows, d, eps); break;
+    case 2: rmsnorm_kernel<O, 2><<<blocks, 256, 0, s>>>(h, g, out, rows, d, eps); break;
+    case 3: rmsnorm_kernel<O, 3><<<blocks, 256, 0, s>>>(h, g, out, rows, d, eps); break;
+    case 4: rmsnorm_kernel<O, 4><<<blocks, 256, 0, s>>>(h, g, out, rows, d, eps); break;
+    case 5: case 6: rmsnorm_kernel<O, 6><<<blocks, 256, 0, s>>>(h, g, out, rows, d, eps); break;
+    case 7: case 8: rmsnorm_kernel<O, 8><<<blocks, 256, 0, s>>>(h, g, out, rows, d, eps); break;
+    case 9: case 10: case 11: case 12: rmsnorm_kernel<O, 12><<<blocks, 256, 0, s>>>(h, g, out, rows, d, eps); break;
+    case 13: case 14: case 15: case 16: rmsnorm_kernel<O, 16><<<blocks, 256, 0, s>>>(h, g, out, rows, d, eps); break;
+    default: rmsnorm_kernel<O, 0><<<blocks, 256, 0, s>>>(h, g, out, rows, d, eps); break;
   }
 }
 
 hipError_t launch_rmsnorm(const float* h, const float* g, void* out, bool out_bf16, int rows, int d, float eps,
                           hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  const int blocks = (rows + 3) / 4;
+  if (d & 3) return hipErrorInvalidValue;
   if (out_bf16)
-    rmsnorm_kernel<bf16_t><<<blocks, 256, 0, s>>>(h, g, (bf16_t*)out, rows, d, eps);
+    rmsnorm_go<bf16_t>(h, g, (bf16_t*)out, rows, d, eps, s);
   else
-    rmsnorm_kernel<float><<<blocks, 256, 0, s>>>(h, g, (float*)out, rows, d, eps);
+    rmsnorm_go<float>(h, g, (float*)out, rows, d, eps, s);
   return hipGetLastError();
 }
 
