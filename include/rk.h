@@ -280,7 +280,8 @@ rk_status rk_sensitivity_profile(const rk_model *m, const rk_batch *calib, const
  * one layer for a batch, row r at v + r * row_stride elements, n_kv_heads *
  * head_dim contiguous values per row; they are replaced in place by
  * v + alpha * ||v||_2 * eps on the eligible positions.  eps is the Philox stream
- * of (seed, sequence index, layer, KV head, position).                          */
+ * of (seed, sequence index, layer, KV head, position).  v must be 8-byte (bf16)
+ * or 16-byte (fp32) aligned and row_stride a multiple of 4 (RK_ERR_ARG).       */
 rk_status rk_perturb_values(const rk_model *m, const rk_batch *batch, int32_t layer, float alpha,
                             const rk_perturb_params *p, void *v, int64_t row_stride, void *stream);
 

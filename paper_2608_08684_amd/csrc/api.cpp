@@ -1568,6 +1568,11 @@ rk_status rk_perturb_values(const rk_model* m, const rk_batch* batch, int32_t la
   if (layer < 0 || layer >= m->cfg.n_layers) { set_error("layer %d out of range", layer); return RK_ERR_ARG; }
   if (!(alpha >= 0.0f) || !isfinite(alpha)) { set_error("alpha must be finite and >= 0"); return RK_ERR_ARG; }
   if (row_stride < (int64_t)m->cfg.n_kv_heads * m->cfg.head_dim) { set_error("row_stride too small"); return RK_ERR_SHAPE; }
+  // four values per vector access: 8-byte (bf16) or 16-byte (fp32) aligned rows
+  if (row_stride % 4 != 0 || (uintptr_t)v % (m->bf16 ? 8 : 16) != 0) {
+    set_error("v must be %d-byte aligned and row_stride a multiple of 4", m->bf16 ? 8 : 16);
+    return RK_ERR_ARG;
+  }
   SeqTable st;
   if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
   const rk_model_config& c = m->cfg;

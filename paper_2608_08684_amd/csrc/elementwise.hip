@@ -253,6 +253,17 @@ __device__ __forceinline__ float to_uniform(uint32_t x) {
   return (float)(2u * (x >> 9) + 1u) * 5.9604644775390625e-8f;
 }
 
+// Four consecutive values as one 16-byte (fp32) or 8-byte (bf16) access.
+__device__ __forceinline__ void load4v(const float* p, float& a, float& b, float& c, float& d) {
+  const float4 v = *reinterpret_cast<const float4*>(p);
+  a = v.x; b = v.y; c = v.z; d = v.w;
+}
+__device__ __forceinline__ void load4v(const bf16_t* p, float& a, float& b, float& c, float& d) {
+  const uint2 u = *reinterpret_cast<const uint2*>(p);
+  a = __uint_as_float(u.x << 16); b = __uint_as_float(u.x & 0xffff0000u);
+  c = __uint_as_float(u.y << 16); d = __uint_as_float(u.y & 0xffff0000u);
+}
+
 // One thread owns four consecutive coordinates j = 4g..4g+3 of one (row, KV head)
 // Value vector; TPV = head_dim / 4 threads cooperate on the vector's norm.
 template <typename T, int TPV>
@@ -271,10 +282,7 @@ __global__ __launch_bounds__(256) void value_noise_kernel(T* __restrict__ v, int
   const int len = st.off[k + 1] - st.off[k];
   T* p = v + (int64_t)row * row_stride + (int64_t)head * (TPV * 4) + sub * 4;
   float x0 = 0.f, x1 = 0.f, x2 = 0.f, x3 = 0.f;
-  if (live) {
-    x0 = Act<T>::load(p + 0); x1 = Act<T>::load(p + 1);
-    x2 = Act<T>::load(p + 2); x3 = Act<T>::load(p + 3);
-  }
+  if (live) load4v(p, x0, x1, x2, x3);
   float ss = x0 * x0 + x1 * x1 + x2 * x2 + x3 * x3;
 #pragma unroll
   for (int m = TPV / 2; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
@@ -289,10 +297,7 @@ __global__ __launch_bounds__(256) void value_noise_kernel(T* __restrict__ v, int
   float s0, co0, s1, co1;
   sincospif(2.0f * to_uniform(c1), &s0, &co0);
   sincospif(2.0f * to_uniform(c3), &s1, &co1);
-  Act<T>::store(p + 0, fmaf(an, r0 * co0, x0));
-  Act<T>::store(p + 1, fmaf(an, r0 * s0, x1));
-  Act<T>::store(p + 2, fmaf(an, r1 * co1, x2));
-  Act<T>::store(p + 3, fmaf(an, r1 * s1, x3));
+  store4v(p, fmaf(an, r0 * co0, x0), fmaf(an, r0 * s0, x1), fmaf(an, r1 * co1, x2), fmaf(an, r1 * s1, x3));
 }
 
 template <typename T>

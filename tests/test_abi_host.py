@@ -194,6 +194,12 @@ def test_profile_entry_points_validate_before_launching():
                                       None, fake, 16, None) == rk.RK_ERR_WORKSPACE
     # perturb_values: row stride too small
     assert lib.rk_perturb_values(h, ctypes.byref(batch), 0, 0.1, ctypes.byref(p), fake, 10, None) == rk.RK_ERR_SHAPE
+    # ... not a multiple of 4, or a misaligned buffer (four values per vector access)
+    wide = 4096
+    assert lib.rk_perturb_values(h, ctypes.byref(batch), 0, 0.1, ctypes.byref(p), fake, wide + 2,
+                                 None) == rk.RK_ERR_ARG
+    assert lib.rk_perturb_values(h, ctypes.byref(batch), 0, 0.1, ctypes.byref(p), ctypes.c_void_p(0x1004), wide,
+                                 None) == rk.RK_ERR_ARG
     lib.rk_model_destroy(h)
 
 
