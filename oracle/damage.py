@@ -1,6 +1,7 @@
 """Isolated single-layer compression damage and its rank agreement with the
 sensitivity profile (Section 2: Eq. layer-compression-damage, Eq.
-perturbation-response, Table sensitivity-correlation).
+perturbation-response, Table sensitivity-correlation), and the damage of a
+whole per-layer budget policy (every layer compressed at once).
 
 Test infrastructure (the oracle of the GPU path): plain numpy in float64.  Only
 tests, the package smoke check and the benchmark's CPU baseline use it.
@@ -63,6 +64,34 @@ def damage_layer(m: M.Model, ws: PR.WindowState, layer: int, positions):
     """(d_{i,l}, KL_t for t in the window): the KL of the full-cache window
     distributions to the ones with layer ``layer`` compressed."""
     xc = window_compressed_final(m, ws, layer, positions)
+    kl = PR.kl_per_position(m, ws.xfinal, xc)
+    return float(np.mean(kl)), kl
+
+
+def window_policy_final(m: M.Model, ws: PR.WindowState, positions_by_layer) -> np.ndarray:
+    """Final normalised hidden state of the window rows when every layer's prompt
+    cache is compressed at once (the deployment of a per-layer budget policy,
+    Section 4.4): layer l keeps, per KV head, the positions
+    ``positions_by_layer[l]`` (None keeps that layer's full prompt cache).  The
+    prompt's Keys and Values are those of the full prefill; compression only
+    removes entries, so the window is evaluated from block 0 on."""
+    P = ws.P
+    T = P + ws.hs[0].shape[0]
+    pos = np.arange(P, T)
+    h = ws.hs[0]
+    for l in range(m.cfg.n_layers):
+        keep = positions_by_layer[l]
+        kv = ws.kv[l] if keep is None else compressed_prefix(ws.kv[l], keep)
+        h = M.block(m, l, h, pos, prefix_kv=kv)
+    return M.final_hidden(m, h)
+
+
+def policy_damage(m: M.Model, ws: PR.WindowState, positions_by_layer):
+    """(d_i, KL_t for t in the window): the KL of the full-cache window
+    distributions to the ones with every layer compressed to its retained
+    positions (Eq. perturbation-response with the whole compression policy as
+    the perturbation)."""
+    xc = window_policy_final(m, ws, positions_by_layer)
     kl = PR.kl_per_position(m, ws.xfinal, xc)
     return float(np.mean(kl)), kl
 

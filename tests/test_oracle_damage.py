@@ -41,6 +41,15 @@ def _random_positions(rng, P, Hkv, b):
 
 def _hf_masked_window_logits(hf, toks, P, layer, positions, monkeypatch):
     """HF window logits with layer `layer`'s dropped prompt positions masked per head."""
+    keep = [None] * SMALL.n_layers
+    keep[layer] = positions
+    return _hf_policy_window_logits(hf, toks, P, keep, monkeypatch)
+
+
+def _hf_policy_window_logits(hf, toks, P, keep, monkeypatch):
+    """HF window logits with, in every layer l whose keep[l] is not None, the
+    prompt positions outside keep[l] (per KV head) masked for every query head of
+    that KV head (an additive -inf mask in the eager attention)."""
     from transformers import DynamicCache
     from transformers.models.llama import modeling_llama as ml
     H, Hkv = SMALL.n_heads, SMALL.n_kv_heads
@@ -48,7 +57,8 @@ def _hf_masked_window_logits(hf, toks, P, layer, positions, monkeypatch):
     plain = ml.eager_attention_forward
 
     def masked(module, query, key, value, attention_mask, scaling, dropout=0.0, **kw):
-        if module.layer_idx == layer and key.shape[2] > query.shape[2]:     # the window against the cache
+        positions = keep[module.layer_idx]
+        if positions is not None and key.shape[2] > query.shape[2]:     # the window against the cache
             extra = torch.zeros(1, H, 1, key.shape[2], dtype=query.dtype)
             for h in range(H):
                 drop = np.setdiff1d(np.arange(P), positions[h // group])
@@ -135,3 +145,48 @@ def test_spearman_matches_scipy_and_closed_forms():
     assert D.spearman(z, -np.exp(z)) == pytest.approx(-1.0)
     assert np.isnan(D.spearman(z, np.ones(10)))
     np.testing.assert_array_equal(D.average_ranks([2.0, 1.0, 2.0, 5.0]), [2.5, 1.0, 2.5, 4.0])
+
+
+def test_policy_window_matches_hf_masking(small, monkeypatch):
+    """Every layer compressed at once, with a different budget per layer (one
+    layer left whole): the oracle's gathered caches against HF masking, and the
+    policy damage against the KL of those distributions."""
+    W, m, toks = small
+    hf = _hf_model(SMALL, W)
+    t = toks[0]
+    rng = np.random.default_rng(11)
+    keep = [_random_positions(rng, PREFIX, SMALL.n_kv_heads, 9), None,
+            _random_positions(rng, PREFIX, SMALL.n_kv_heads, 40)]
+    ws = P.window_clean_state(m, t, PREFIX)
+    ours = M.logits(m, D.window_policy_final(m, ws, keep))
+    ref = _hf_policy_window_logits(hf, t, PREFIX, keep, monkeypatch)
+    assert np.max(np.abs(ours - ref)) < 1e-6 * max(1.0, np.abs(ref).max())
+    d, kl = D.policy_damage(m, ws, keep)
+    lp = torch.log_softmax(torch.from_numpy(M.logits(m, ws.xfinal)), -1)
+    lq = torch.log_softmax(torch.from_numpy(ref), -1)
+    kl_ref = torch.nn.functional.kl_div(lq, lp, reduction="none", log_target=True).sum(-1).numpy()
+    assert np.max(np.abs(kl - kl_ref)) < 1e-6 * max(1e-3, kl_ref.max())
+    assert d == float(np.mean(kl)) and d > 0
+
+
+def test_policy_reduces_to_whole_caches_and_single_layers(small):
+    """No layer compressed (or every position kept) gives exactly 0; compressing
+    one layer only is that layer's isolated damage, exactly (the layers below it
+    recompute the window's cached block inputs bit for bit)."""
+    W, m, toks = small
+    t = toks[1]
+    ws = P.window_clean_state(m, t, PREFIX)
+    L, Hkv = SMALL.n_layers, SMALL.n_kv_heads
+    d0, kl0 = D.policy_damage(m, ws, [None] * L)
+    assert d0 == 0.0 and np.all(kl0 == 0.0)
+    dall, klall = D.policy_damage(m, ws, [[np.arange(PREFIX)] * Hkv] * L)
+    assert dall == 0.0 and np.all(klall == 0.0)
+    rng = np.random.default_rng(12)
+    for layer in range(L):
+        pos = _random_positions(rng, PREFIX, Hkv, 13)
+        keep = [None] * L
+        keep[layer] = pos
+        d, kl = D.policy_damage(m, ws, keep)
+        d1, kl1 = D.damage_layer(m, ws, layer, pos)
+        assert d == d1 and np.array_equal(kl, kl1)
+
