@@ -406,6 +406,34 @@ rk_status rk_compression_damage_layers(const rk_model *m, const rk_batch *batch,
                                        size_t state_bytes, float *d_out, float *kl_pos, void *workspace,
                                        size_t ws_bytes, void *stream);
 
+/* The damage of a whole per-layer budget policy (Section 4.4: the budgets
+ * deployed, every layer's prompt cache compressed at once): the window rows
+ * [window_start, T_i) run from block 0 with block l attending to the n_keep[l]
+ * retained prompt positions of each KV head, or to the whole prompt cache when
+ * n_keep[l] is 0; d_out[i] is the window mean of KL(full-cache || compressed)
+ * per position, as for rk_compression_damage.  The prompt caches are those of
+ * the full prefill in state (rk_window_reference with the same window_start).
+ *   positions:     DEVICE int32; layer l, sequence i, KV head h, entry j at
+ *                  positions[layer_offsets[l] + i * seq_stride + h * n_keep[l] + j]
+ *                  (clamped to [0, window_start)); NULL allowed when every
+ *                  n_keep is 0.  With the outputs of rk_snapkv_compress for
+ *                  budgets that are the same for every sequence:
+ *                  layer_offsets[l] = n_kv_heads * sum_{l' < l} b_l',
+ *                  seq_stride = n_kv_heads * sum_l b_l.
+ *   layer_offsets: HOST int64 [n_layers]; n_keep: HOST int32 [n_layers], each in
+ *                  [0, window_start].
+ *   kl_pos:        DEVICE fp32 [window rows] or NULL.
+ *   logits_out:    DEVICE fp32 [window rows, vocab] or NULL: the compressed
+ *                  model's logits of the window rows (with window_start = T_i - 1,
+ *                  one decode step over the compressed caches); selects the
+ *                  unfused LM head.
+ * Workspace: rk_workspace_size(m, rows, 1, RK_FLAG_CACHED_WINDOW), plus
+ * RK_FLAG_UNFUSED_KL when logits_out is given.                                  */
+rk_status rk_policy_damage(const rk_model *m, const rk_batch *batch, int32_t window_start, const int32_t *positions,
+                           const int64_t *layer_offsets, int64_t seq_stride, const int32_t *n_keep,
+                           const void *state, size_t state_bytes, float *d_out, float *kl_pos, float *logits_out,
+                           void *workspace, size_t ws_bytes, void *stream);
+
 /* Spearman's rho of two profiles x, y [n] (Section 2, Table
  * sensitivity-correlation): the Pearson correlation of their ranks, ties sharing
  * the mean rank; NaN when a profile is constant.  Host only, float64.          */

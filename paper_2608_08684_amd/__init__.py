@@ -123,6 +123,8 @@ def load() -> ctypes.CDLL:
                                        vp]),
         "rk_compression_damage_layers": (st, [vp, ctypes.POINTER(_Batch), i32, ctypes.POINTER(i32), i32, vp, i64,
                                               i64, i32, vp, sz, vp, vp, vp, sz, vp]),
+        "rk_policy_damage": (st, [vp, ctypes.POINTER(_Batch), i32, vp, ctypes.POINTER(i64), i64, ctypes.POINTER(i32),
+                                  vp, sz, vp, vp, vp, vp, sz, vp]),
         "rk_spearman": (st, [ctypes.POINTER(f64), ctypes.POINTER(f64), i32, ctypes.POINTER(f64)]),
         "rk_snapkv_state_size": (sz, [vp, i64, i32, i32]),
         "rk_snapkv_workspace_size": (sz, [vp, i64, i32, i32]),
@@ -279,6 +281,20 @@ class Model:
                                                    int(n_keep), _ptr(state), state.numel() * state.element_size(),
                                                    _ptr(d_out), _ptr(kl_pos), _ptr(workspace),
                                                    workspace.numel() * workspace.element_size(), _stream(stream)))
+
+    def policy_damage(self, batch: Batch, window_start: int, positions, layer_offsets: Sequence[int],
+                      seq_stride: int, n_keep: Sequence[int], state, d_out, workspace, kl_pos=None,
+                      logits_out=None, stream=None):
+        """rk_policy_damage: every layer's prompt cache compressed at once."""
+        L = self.cfg.n_layers
+        if len(layer_offsets) != L or len(n_keep) != L:
+            raise ValueError(f"layer_offsets and n_keep need {L} entries")
+        offs = (ctypes.c_int64 * L)(*[int(x) for x in layer_offsets])
+        keep = (ctypes.c_int32 * L)(*[int(x) for x in n_keep])
+        _check(load().rk_policy_damage(self._h, ctypes.byref(batch._c), int(window_start), _ptr(positions), offs,
+                                       int(seq_stride), keep, _ptr(state), state.numel() * state.element_size(),
+                                       _ptr(d_out), _ptr(kl_pos), _ptr(logits_out), _ptr(workspace),
+                                       workspace.numel() * workspace.element_size(), _stream(stream)))
 
     # -- SnapKV consumer of the budgets
     def snapkv_state_size(self, rows: int, n_seqs: int, obs_window: int) -> int:

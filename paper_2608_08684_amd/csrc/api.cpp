@@ -759,6 +759,41 @@ static rk_status window_compressed_final(const rk_model* m, const SeqTable& pst,
   return RK_OK;
 }
 
+// The window rows with every layer's prompt cache compressed at once (a per-layer
+// budget policy deployed, Section 4.4): block l attends to the n_keep[l] retained
+// prompt positions of each KV head (positions + layer_off[l], per sequence at
+// seq_stride), gathered into a compressed cache, or to the whole prompt cache when
+// n_keep[l] is 0.  The window runs from block 0 (its cached input); the layers'
+// caches are those of the full prefill.  The rotary table must hold the window
+// positions.
+static rk_status window_policy_final(const rk_model* m, const SeqTable& pst, const SeqTable& wst, const Win& wn,
+                                     const int32_t* positions, const int64_t* layer_off, int64_t seq_stride,
+                                     const int32_t* n_keep, void* xf_out, const Bufs& bf, hipStream_t s) {
+  const rk_model_config& c = m->cfg;
+  const int64_t d = c.d_model, Rp = pst.rows, Rw = wst.rows, a = act_bytes(m), kc = kv_cols(m);
+  const float* h_in = wn.w.h;
+  for (int l = 0; l < c.n_layers; ++l) {
+    KvPrefix pk{};
+    if (n_keep[l] > 0) {
+      const char* kv_l = (const char*)wn.kv + (size_t)l * Rp * kc * a;
+      RK_TRY(launch_prefix_gather(kv_l, kc, pst.n, pst.max_len, c.n_kv_heads, c.head_dim, positions + layer_off[l],
+                                  seq_stride, n_keep[l], bf.cpre, s));
+      pk.alt_pass = -1;
+      pk.k = (const bf16_t*)bf.cpre;
+      pk.v = (const bf16_t*)bf.cpre + kc / 2;
+      pk.ldk = pk.ldv = kc;
+      pk.P = n_keep[l];
+    } else {
+      pk = cache_prefix(m, wn, pst, l, nullptr);
+    }
+    rk_status e = run_block(m, l, h_in, bf.h, bf, wst, nullptr, s, &pk);
+    if (e != RK_OK) return e;
+    h_in = bf.h;
+  }
+  RK_TRY(launch_rmsnorm(bf.h, m->final_norm, xf_out, m->bf16, (int)Rw, (int)d, c.rms_eps, s));
+  return RK_OK;
+}
+
 // ----------------------------------------------------------------------------- validation
 static rk_status make_table(const rk_batch* bt, int first, int count, SeqTable* st) {
   if (count < 1 || count > RK_MAX_BATCH_SEQS) {
@@ -1303,6 +1338,51 @@ rk_status rk_compression_damage_layers(const rk_model* m, const rk_batch* batch,
   float* kl = kl_pos ? kl_pos : b.kl;
   if ((e = score_group(m, wst, wn.w, b.xp, n_sel, false, b.logits_p, kl, b, s)) != RK_OK) return e;
   RK_TRY(launch_window_mean(kl, wst.rows, n_sel, wst, 0, d_out, s));
+  return RK_OK;
+}
+
+rk_status rk_policy_damage(const rk_model* m, const rk_batch* batch, int32_t window_start, const int32_t* positions,
+                           const int64_t* layer_offsets, int64_t seq_stride, const int32_t* n_keep, const void* state,
+                           size_t state_bytes, float* d_out, float* kl_pos, float* logits_out, void* workspace,
+                           size_t ws_bytes, void* stream) {
+  rk_status e = check_batch(m, batch);
+  if (e != RK_OK) return e;
+  if ((e = check_window_model(m)) != RK_OK) return e;
+  if (!layer_offsets || !n_keep || !state || !d_out || !workspace) {
+    set_error("null layer_offsets, n_keep, state, d_out or workspace");
+    return RK_ERR_ARG;
+  }
+  const int L = m->cfg.n_layers;
+  int max_keep = 0;
+  for (int l = 0; l < L; ++l) {
+    if (n_keep[l] < 0 || n_keep[l] > window_start) { set_error("n_keep[%d] must be in [0, window_start]", l); return RK_ERR_ARG; }
+    if (n_keep[l] > 0 && layer_offsets[l] < 0) { set_error("layer_offsets[%d] must be >= 0", l); return RK_ERR_ARG; }
+    max_keep = std::max(max_keep, (int)n_keep[l]);
+  }
+  if (max_keep > 0 && !positions) { set_error("null positions"); return RK_ERR_ARG; }
+  if (max_keep > 0 && seq_stride < (int64_t)m->cfg.n_kv_heads * max_keep) {
+    set_error("seq_stride below n_kv_heads * max(n_keep)");
+    return RK_ERR_ARG;
+  }
+  SeqTable st, pst, wst;
+  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  if ((e = window_tables(st, window_start, &pst, &wst)) != RK_OK) return e;
+  if (state_bytes < win_plan(m, st.rows).total) { set_error("window state too small"); return RK_ERR_WORKSPACE; }
+  const uint32_t wf = RK_FLAG_CACHED_WINDOW | (logits_out ? RK_FLAG_UNFUSED_KL : 0);
+  const WsPlan wp = ws_plan(m, st.rows, 1, wf);
+  if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
+  const Bufs b = carve(wp, workspace);
+  const Win wn = win_view(m, st.rows, state);
+  hipStream_t s = (hipStream_t)stream;
+  RK_TRY(launch_rope_table(b.rope, b.rope_pos, wst, m->cfg.head_dim, m->cfg.rope_theta, s, window_start));
+  if ((e = window_policy_final(m, pst, wst, wn, positions, layer_offsets, seq_stride, n_keep, b.xp, b, s)) != RK_OK)
+    return e;
+  float* kl = kl_pos ? kl_pos : b.kl;
+  const bool unfused = logits_out != nullptr;
+  if (unfused && (e = clean_logits(m, wst, wn.w, b.logits_c, s)) != RK_OK) return e;
+  if ((e = score_group(m, wst, wn.w, b.xp, 1, unfused, unfused ? logits_out : b.logits_p, kl, b, s)) != RK_OK)
+    return e;
+  RK_TRY(launch_window_mean(kl, wst.rows, 1, wst, 0, d_out, s));
   return RK_OK;
 }
 

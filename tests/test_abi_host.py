@@ -393,6 +393,38 @@ def test_compression_damage_layers_validates_before_launching():
     lib.rk_model_destroy(h32)
 
 
+def test_policy_damage_validates_before_launching():
+    lib = rk.load()
+    fake = ctypes.c_void_p(0x1000)
+    offs = np.array([0, 100, 250], dtype=np.int64)
+    batch = rk._Batch(fake, offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 2, 0)
+    big = 1 << 40
+    st, h = _create(_FakeCfg())
+    assert st == rk.RK_OK
+
+    def call(keep=(10, 0), loff=(0, 0), stride=20, P=50, pos=fake, sb=big, wb=big, null_arrays=False):
+        k = (ctypes.c_int32 * 2)(*keep)
+        o = (ctypes.c_int64 * 2)(*loff)
+        return lib.rk_policy_damage(h, ctypes.byref(batch), P, pos, None if null_arrays else o, stride,
+                                    None if null_arrays else k, fake, sb, fake, None, None, fake, wb, None)
+    assert call(null_arrays=True) == rk.RK_ERR_ARG
+    assert call(keep=(-1, 0)) == rk.RK_ERR_ARG
+    assert call(keep=(51, 0)) == rk.RK_ERR_ARG            # more than the prompt
+    assert call(loff=(-4, 0)) == rk.RK_ERR_ARG
+    assert call(pos=None) == rk.RK_ERR_ARG                 # positions needed for a compressed layer
+    assert call(stride=19) == rk.RK_ERR_ARG                # below n_kv_heads * max(n_keep)
+    assert call(P=100) == rk.RK_ERR_SHAPE                  # no window in the first sequence
+    assert call(sb=16) == rk.RK_ERR_WORKSPACE
+    assert call(wb=16) == rk.RK_ERR_WORKSPACE
+    lib.rk_model_destroy(h)
+    st, h32 = _create(_FakeCfg(dtype="f32"))
+    k = (ctypes.c_int32 * 2)(0, 0)
+    o = (ctypes.c_int64 * 2)(0, 0)
+    assert lib.rk_policy_damage(h32, ctypes.byref(batch), 50, None, o, 0, k, fake, big, fake, None, None, fake, big,
+                                None) == rk.RK_ERR_UNSUPPORTED
+    lib.rk_model_destroy(h32)
+
+
 def test_size_queries_reject_rows_beyond_int32():
     lib = rk.load()
     st, h = _create(_FakeCfg())
