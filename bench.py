@@ -455,6 +455,142 @@ def cpu_baseline_damage(w, W, toks, P: int, b: int):
                       f"per KV head, float32 oracle: {dt:.1f} s (window reference included)"}
 
 
+def cpu_baseline_policy(w, W, toks, P: int, budgets):
+    """Oracle whole-policy damage of sequence 0 (window reference included): every
+    layer compressed to its budget, positions drawn by fixtures (the oracle's cost
+    does not depend on which positions are kept)."""
+    import fixtures as F
+    from oracle import damage as OD
+    from oracle import model as OM
+    from oracle import profile as OPR
+    from tests.gpu_helpers import f32_weights  # noqa: E402
+    cfg = w.model
+    m = OM.Model(cfg, f32_weights(cfg, W), np.float32)
+    t = toks[0]
+    keep = [list(F.random_keep(1, cfg.n_kv_heads, P, int(b), seed_id=20 + l)[0]) for l, b in enumerate(budgets)]
+    t0 = time.perf_counter()
+    ws = OPR.window_clean_state(m, t, P)
+    OD.policy_damage(m, ws, keep)
+    dt = time.perf_counter() - t0
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max(int(x.get("num_threads", 1)) for x in threadpool_info()) if threadpool_info() else os.cpu_count()
+    except Exception:
+        cores = os.cpu_count()
+    n = (len(t) - P) * cfg.n_layers
+    return {"value": n / dt, "unit": "window token-layers/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"sequence 0 (prompt {P}, window {len(t) - P}), all {cfg.n_layers} layers compressed to the "
+                      f"RippleKV budgets, float32 oracle: {dt:.1f} s (window reference included)"}
+
+
+def policy_main(args):
+    """The damage of whole per-layer budget policies on the GPT-2-small-shaped
+    workload: the cached-window sensitivity profile of the batch gives RippleKV
+    budgets (ratio 2, the same total as SnapKV's uniform b = 20% of the prompt at
+    every layer); SnapKV selects each policy's positions on the prompts; one step
+    = one rk_policy_damage call for the RippleKV policy (the window evaluated with
+    every layer's prompt cache compressed, fused LM head + KL against the
+    full-cache window) and the batch mean.  The uniform policy's damage is
+    reported beside it."""
+    import torch
+    import fixtures as F
+    import paper_2608_08684_amd as rk
+    from tests.gpu_helpers import make_batch, upload_weights
+    w = F.get_workload(args.workload)
+    cfg = w.model
+    L, Hkv, dh = cfg.n_layers, cfg.n_kv_heads, cfg.head_dim
+    window = args.window if args.window > 0 else 256
+    lens = w.lengths()
+    P = min(lens) - window
+    b = int(round(DMG_RHO * P))
+    t0 = time.perf_counter()
+    W = F.make_weights(cfg)
+    model = rk.Model(cfg, upload_weights(cfg, W))
+    toks = F.make_tokens(w)
+    batch = make_batch(toks)
+    rows = batch.rows
+    Rw = sum(T - P for T in lens)
+    state = torch.empty(model.window_state_size(rows), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(model.workspace_size(rows, L, rk.RK_FLAG_CACHED_WINDOW), dtype=torch.uint8, device="cuda")
+    model.window_reference(batch, P, state, ws)
+    s_out = torch.empty(1, L, dtype=torch.float32, device="cuda")
+    pws = torch.empty(model.workspace_size(rows, L, rk.RK_WS_CLEAN_STATE | rk.RK_FLAG_CACHED_WINDOW),
+                      dtype=torch.uint8, device="cuda")
+    model.sensitivity_profile(batch, list(range(L)), [max(w.alphas)], s_out, pws, rows, L, window_start=P,
+                              flags=rk.RK_FLAG_CACHED_WINDOW)
+    s_prof = s_out.cpu().numpy()[0].astype(np.float64)
+    del pws
+    _, ripple = rk.layer_budgets(s_prof, b * L, 2.0)
+    ripple = [max(1, min(int(x), P)) for x in ripple]
+    pb = make_batch([t[:P] for t in toks])
+    sst = torch.empty(model.snapkv_state_size(pb.rows, pb.n_seqs, DMG_OBS), dtype=torch.uint8, device="cuda")
+    sws = torch.empty(model.snapkv_workspace_size(pb.rows, pb.n_seqs, DMG_OBS), dtype=torch.uint8, device="cuda")
+    model.snapkv_prefill(pb, DMG_OBS, sst, sws)
+    policies = {}
+    for name, bl in (("uniform", [b] * L), ("ripplekv", ripple)):
+        budgets = np.tile(np.asarray(bl, dtype=np.int64), (pb.n_seqs, 1))
+        total, offs = rk.snapkv_layout(pb, L, budgets)
+        pos = torch.empty(Hkv * total, dtype=torch.int32, device="cuda")
+        ko = torch.empty(Hkv * total, dh, dtype=torch.int16, device="cuda")
+        vo = torch.empty_like(ko)
+        model.snapkv_compress(pb, budgets, sst, pos, ko, vo, sws, obs_window=DMG_OBS)
+        policies[name] = (pos, [int(offs[l]) * Hkv for l in range(L)], int(offs[L]) * Hkv, bl)
+        del ko, vo
+    del sst, sws
+    d_out = torch.empty(batch.n_seqs, dtype=torch.float32, device="cuda")
+    log(f"policy inputs ready in {time.perf_counter() - t0:.1f} s (prompt {P}, window {window}, uniform b = {b}, "
+        f"RippleKV budgets {ripple})")
+
+    def run(name):
+        pos, loff, stride, bl = policies[name]
+        model.policy_damage(batch, P, pos, loff, stride, bl, state, d_out, ws)
+        return float(d_out.mean().item())     # synchronises
+
+    D_uniform = run("uniform")
+    for _ in range(args.warmup):
+        rk.timing_begin(args.family)
+        run("ripplekv")
+        rk.timing_end()
+    torch.cuda.synchronize()
+    launches, fam_ms = 0, 0.0
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        rk.timing_begin(args.family)
+        D_ripple = run("ripplekv")
+        n, ms = rk.timing_end()
+        launches += n
+        fam_ms += ms
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    value = Rw * L / (ms_per_step / 1e3)
+    avg = fam_ms / max(launches, 1)
+    if args.family == "lm_kl":
+        flops = family_flops(args.family, cfg, Rw, 1) * args.steps / max(launches, 1)
+    else:   # every layer once over the window rows
+        flops = family_flops(args.family, cfg, Rw * L, 1) * args.steps / max(launches, 1)
+    achieved = flops / (avg / 1e3) / 1e12
+    roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": args.family,
+            "launches": launches, "avg_ms": round(avg, 4), "flop_per_launch": flops}
+    log(f"{args.family}: {launches} launches, avg {avg:.4f} ms, {achieved:.1f} TFLOP/s; "
+        f"D uniform {D_uniform:.6e}, D RippleKV {D_ripple:.6e}")
+    res = {
+        "metric": "window token-layers/s (whole-policy compressed-cache window evaluation)",
+        "value": round(value, 1), "unit": "token-layers/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (random-init N(0,0.02) weights, Zipf(1.1) tokens)",
+        "config": {"workload": f"{w.name} budget policies: {L}L d{cfg.d_model} {cfg.n_heads}x{dh}; "
+                               f"{batch.n_seqs}x{max(lens)} tokens, prompt {P} + window {window}; SnapKV selection "
+                               f"(window {DMG_OBS}, max pooling 7) with uniform b = {b} or RippleKV budgets "
+                               f"(ratio 2, same total) at every layer at once",
+                   "ripplekv_budgets": ripple, "damage_uniform": D_uniform, "damage_ripplekv": D_ripple},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline_policy(w, W, toks, P, ripple)
+    print(json.dumps(res), flush=True)
+
+
 def damage_main(args):
     """Isolated single-layer compression damage (Section 2) of every layer on the
     GPT-2-small-shaped workload: the prompt [0, P) of each sequence compressed by
@@ -574,6 +710,9 @@ def main():
                          "prefix (0: the resumed full-sequence profile)")
     ap.add_argument("--snapkv", action="store_true",
                     help="time the SnapKV selection with per-layer budgets (the budgets' consumer) instead")
+    ap.add_argument("--policy", action="store_true",
+                    help="the damage of whole per-layer budget policies (RippleKV vs uniform) in the cached-window "
+                         "split, every layer compressed at once")
     ap.add_argument("--damage", action="store_true",
                     help="time the isolated single-layer compression damage of every layer instead (prompt = all "
                          "but the last WINDOW tokens, default 256)")
@@ -618,6 +757,9 @@ def main():
         return
     if args.damage:
         damage_main(args)
+        return
+    if args.policy:
+        policy_main(args)
         return
     import fixtures as F
     import paper_2608_08684_amd as rk
