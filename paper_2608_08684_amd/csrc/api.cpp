@@ -1273,6 +1273,53 @@ rk_status rk_snapkv_compress(const rk_model* m, const rk_batch* batch, const rk_
   return RK_OK;
 }
 
+}  // extern "C"
+
+// The set-up shared by the calls that evaluate a batch's window rows against its
+// window state: the prefix and window tables, the size checks, the workspace
+// carve-up (G passes per LM-head launch, workspace flags wf) and the window's
+// rotary table (its only launch, after every check).
+struct WinCall {
+  SeqTable st, pst, wst;
+  Bufs b;
+  Win wn;
+  hipStream_t s;
+};
+
+static rk_status win_call(const rk_model* m, const rk_batch* batch, int32_t window_start, const void* state,
+                          size_t state_bytes, void* workspace, size_t ws_bytes, int G, uint32_t wf, void* stream,
+                          WinCall* c) {
+  rk_status e;
+  if ((e = make_table(batch, 0, batch->n_seqs, &c->st)) != RK_OK) return e;
+  if ((e = window_tables(c->st, window_start, &c->pst, &c->wst)) != RK_OK) return e;
+  if (state_bytes < win_plan(m, c->st.rows).total) { set_error("window state too small"); return RK_ERR_WORKSPACE; }
+  const WsPlan wp = ws_plan(m, c->st.rows, G, wf);
+  if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
+  c->b = carve(wp, workspace);
+  c->wn = win_view(m, c->st.rows, state);
+  c->s = (hipStream_t)stream;
+  RK_TRY(launch_rope_table(c->b.rope, c->b.rope_pos, c->wst, m->cfg.head_dim, m->cfg.rope_theta, c->s, window_start));
+  return RK_OK;
+}
+
+// Scores G finished window passes (slots of b.xp) against the full-cache window
+// and takes the window means: d_out[g * n_seqs + i]; logits_out selects the
+// unfused LM head and receives the passes' fp32 logits.
+static rk_status score_window(const rk_model* m, const WinCall& c, int G, float* logits_out, float* kl_pos,
+                              float* d_out) {
+  rk_status e;
+  float* kl = kl_pos ? kl_pos : c.b.kl;
+  const bool unfused = logits_out != nullptr;
+  if (unfused && (e = clean_logits(m, c.wst, c.wn.w, c.b.logits_c, c.s)) != RK_OK) return e;
+  if ((e = score_group(m, c.wst, c.wn.w, c.b.xp, G, unfused, unfused ? logits_out : c.b.logits_p, kl, c.b, c.s)) !=
+      RK_OK)
+    return e;
+  RK_TRY(launch_window_mean(kl, c.wst.rows, G, c.wst, 0, d_out, c.s));
+  return RK_OK;
+}
+
+extern "C" {
+
 rk_status rk_compression_damage(const rk_model* m, const rk_batch* batch, int32_t window_start, int32_t layer,
                                 const int32_t* positions, int64_t seq_stride, int32_t n_keep, const void* state,
                                 size_t state_bytes, float* d_out, float* kl_pos, void* workspace, size_t ws_bytes,
@@ -1284,22 +1331,14 @@ rk_status rk_compression_damage(const rk_model* m, const rk_batch* batch, int32_
   if (layer < 0 || layer >= m->cfg.n_layers) { set_error("layer %d out of range", layer); return RK_ERR_ARG; }
   if (n_keep < 1 || n_keep > window_start) { set_error("n_keep must be in [1, window_start]"); return RK_ERR_ARG; }
   if (seq_stride < (int64_t)m->cfg.n_kv_heads * n_keep) { set_error("seq_stride below n_kv_heads * n_keep"); return RK_ERR_ARG; }
-  SeqTable st, pst, wst;
-  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
-  if ((e = window_tables(st, window_start, &pst, &wst)) != RK_OK) return e;
-  if (state_bytes < win_plan(m, st.rows).total) { set_error("window state too small"); return RK_ERR_WORKSPACE; }
-  const WsPlan wp = ws_plan(m, st.rows, 1, RK_FLAG_CACHED_WINDOW);
-  if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
-  const Bufs b = carve(wp, workspace);
-  const Win wn = win_view(m, st.rows, state);
-  hipStream_t s = (hipStream_t)stream;
-  RK_TRY(launch_rope_table(b.rope, b.rope_pos, wst, m->cfg.head_dim, m->cfg.rope_theta, s, window_start));
-  if ((e = window_compressed_final(m, pst, wst, wn, layer, positions, seq_stride, n_keep, b.xp, b, s)) != RK_OK)
+  WinCall c;
+  if ((e = win_call(m, batch, window_start, state, state_bytes, workspace, ws_bytes, 1, RK_FLAG_CACHED_WINDOW, stream,
+                    &c)) != RK_OK)
     return e;
-  float* kl = kl_pos ? kl_pos : b.kl;
-  if ((e = score_group(m, wst, wn.w, b.xp, 1, false, b.logits_p, kl, b, s)) != RK_OK) return e;
-  RK_TRY(launch_window_mean(kl, wst.rows, 1, wst, 0, d_out, s));
-  return RK_OK;
+  if ((e = window_compressed_final(m, c.pst, c.wst, c.wn, layer, positions, seq_stride, n_keep, c.b.xp, c.b, c.s)) !=
+      RK_OK)
+    return e;
+  return score_window(m, c, 1, nullptr, kl_pos, d_out);
 }
 
 rk_status rk_compression_damage_layers(const rk_model* m, const rk_batch* batch, int32_t window_start,
@@ -1320,25 +1359,16 @@ rk_status rk_compression_damage_layers(const rk_model* m, const rk_batch* batch,
   if (n_keep < 1 || n_keep > window_start) { set_error("n_keep must be in [1, window_start]"); return RK_ERR_ARG; }
   if (seq_stride < (int64_t)m->cfg.n_kv_heads * n_keep) { set_error("seq_stride below n_kv_heads * n_keep"); return RK_ERR_ARG; }
   if (layer_stride < 0) { set_error("layer_stride must be >= 0"); return RK_ERR_ARG; }
-  SeqTable st, pst, wst;
-  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
-  if ((e = window_tables(st, window_start, &pst, &wst)) != RK_OK) return e;
-  if (state_bytes < win_plan(m, st.rows).total) { set_error("window state too small"); return RK_ERR_WORKSPACE; }
-  const WsPlan wp = ws_plan(m, st.rows, n_sel, RK_FLAG_CACHED_WINDOW);
-  if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
-  const Bufs b = carve(wp, workspace);
-  const Win wn = win_view(m, st.rows, state);
-  hipStream_t s = (hipStream_t)stream;
-  RK_TRY(launch_rope_table(b.rope, b.rope_pos, wst, m->cfg.head_dim, m->cfg.rope_theta, s, window_start));
+  WinCall c;
+  if ((e = win_call(m, batch, window_start, state, state_bytes, workspace, ws_bytes, n_sel, RK_FLAG_CACHED_WINDOW,
+                    stream, &c)) != RK_OK)
+    return e;
   const int32_t* ps[RK_MAX_GROUP];
   for (int k = 0; k < n_sel; ++k) ps[k] = positions + (int64_t)layers[k] * layer_stride;
-  if ((e = window_group_final(m, pst, wst, wn, n_sel, layers, nullptr, nullptr, st.rows, b.xp, b, s, ps, seq_stride,
-                              n_keep)) != RK_OK)
+  if ((e = window_group_final(m, c.pst, c.wst, c.wn, n_sel, layers, nullptr, nullptr, c.st.rows, c.b.xp, c.b, c.s, ps,
+                              seq_stride, n_keep)) != RK_OK)
     return e;
-  float* kl = kl_pos ? kl_pos : b.kl;
-  if ((e = score_group(m, wst, wn.w, b.xp, n_sel, false, b.logits_p, kl, b, s)) != RK_OK) return e;
-  RK_TRY(launch_window_mean(kl, wst.rows, n_sel, wst, 0, d_out, s));
-  return RK_OK;
+  return score_window(m, c, n_sel, nullptr, kl_pos, d_out);
 }
 
 rk_status rk_policy_damage(const rk_model* m, const rk_batch* batch, int32_t window_start, const int32_t* positions,
@@ -1364,26 +1394,14 @@ rk_status rk_policy_damage(const rk_model* m, const rk_batch* batch, int32_t win
     set_error("seq_stride below n_kv_heads * max(n_keep)");
     return RK_ERR_ARG;
   }
-  SeqTable st, pst, wst;
-  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
-  if ((e = window_tables(st, window_start, &pst, &wst)) != RK_OK) return e;
-  if (state_bytes < win_plan(m, st.rows).total) { set_error("window state too small"); return RK_ERR_WORKSPACE; }
+  WinCall c;
   const uint32_t wf = RK_FLAG_CACHED_WINDOW | (logits_out ? RK_FLAG_UNFUSED_KL : 0);
-  const WsPlan wp = ws_plan(m, st.rows, 1, wf);
-  if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
-  const Bufs b = carve(wp, workspace);
-  const Win wn = win_view(m, st.rows, state);
-  hipStream_t s = (hipStream_t)stream;
-  RK_TRY(launch_rope_table(b.rope, b.rope_pos, wst, m->cfg.head_dim, m->cfg.rope_theta, s, window_start));
-  if ((e = window_policy_final(m, pst, wst, wn, positions, layer_offsets, seq_stride, n_keep, b.xp, b, s)) != RK_OK)
+  if ((e = win_call(m, batch, window_start, state, state_bytes, workspace, ws_bytes, 1, wf, stream, &c)) != RK_OK)
     return e;
-  float* kl = kl_pos ? kl_pos : b.kl;
-  const bool unfused = logits_out != nullptr;
-  if (unfused && (e = clean_logits(m, wst, wn.w, b.logits_c, s)) != RK_OK) return e;
-  if ((e = score_group(m, wst, wn.w, b.xp, 1, unfused, unfused ? logits_out : b.logits_p, kl, b, s)) != RK_OK)
+  if ((e = window_policy_final(m, c.pst, c.wst, c.wn, positions, layer_offsets, seq_stride, n_keep, c.b.xp, c.b,
+                               c.s)) != RK_OK)
     return e;
-  RK_TRY(launch_window_mean(kl, wst.rows, 1, wst, 0, d_out, s));
-  return RK_OK;
+  return score_window(m, c, 1, logits_out, kl_pos, d_out);
 }
 
 size_t rk_workspace_size(const rk_model* m, int64_t max_rows, int32_t max_group, uint32_t flags) {
