@@ -490,8 +490,8 @@ def policy_main(args):
     every layer); SnapKV selects each policy's positions on the prompts; one step
     = one rk_policy_damage call for the RippleKV policy (the window evaluated with
     every layer's prompt cache compressed, fused LM head + KL against the
-    full-cache window) and the batch mean.  The uniform policy's damage is
-    reported beside it."""
+    full-cache window) and the batch mean.  The uniform policy's damage and a
+    sweep over the ratio (1 = uniform, 1.5, 2, 4, 8) are reported beside it."""
     import torch
     import fixtures as F
     import paper_2608_08684_amd as rk
@@ -520,14 +520,17 @@ def policy_main(args):
                               flags=rk.RK_FLAG_CACHED_WINDOW)
     s_prof = s_out.cpu().numpy()[0].astype(np.float64)
     del pws
-    _, ripple = rk.layer_budgets(s_prof, b * L, 2.0)
-    ripple = [max(1, min(int(x), P)) for x in ripple]
+    def ripple_budgets(r):
+        _, bl = rk.layer_budgets(s_prof, b * L, r)
+        return [max(1, min(int(x), P)) for x in bl]
+    ripple = ripple_budgets(2.0)
+    sweep_r = (1.5, 4.0, 8.0)
     pb = make_batch([t[:P] for t in toks])
     sst = torch.empty(model.snapkv_state_size(pb.rows, pb.n_seqs, DMG_OBS), dtype=torch.uint8, device="cuda")
     sws = torch.empty(model.snapkv_workspace_size(pb.rows, pb.n_seqs, DMG_OBS), dtype=torch.uint8, device="cuda")
     model.snapkv_prefill(pb, DMG_OBS, sst, sws)
     policies = {}
-    for name, bl in (("uniform", [b] * L), ("ripplekv", ripple)):
+    for name, bl in [("uniform", [b] * L), ("ripplekv", ripple)] + [(f"r{r}", ripple_budgets(r)) for r in sweep_r]:
         budgets = np.tile(np.asarray(bl, dtype=np.int64), (pb.n_seqs, 1))
         total, offs = rk.snapkv_layout(pb, L, budgets)
         pos = torch.empty(Hkv * total, dtype=torch.int32, device="cuda")
@@ -547,6 +550,9 @@ def policy_main(args):
         return float(d_out.mean().item())     # synchronises
 
     D_uniform = run("uniform")
+    sweep = {"1.0": D_uniform}
+    for r in sweep_r:
+        sweep[str(r)] = run(f"r{r}")
     for _ in range(args.warmup):
         rk.timing_begin(args.family)
         run("ripplekv")
@@ -583,7 +589,8 @@ def policy_main(args):
                                f"{batch.n_seqs}x{max(lens)} tokens, prompt {P} + window {window}; SnapKV selection "
                                f"(window {DMG_OBS}, max pooling 7) with uniform b = {b} or RippleKV budgets "
                                f"(ratio 2, same total) at every layer at once",
-                   "ripplekv_budgets": ripple, "damage_uniform": D_uniform, "damage_ripplekv": D_ripple},
+                   "ripplekv_budgets": ripple, "damage_uniform": D_uniform, "damage_ripplekv": D_ripple,
+                   "damage_by_ratio": dict(sorted({**sweep, "2.0": D_ripple}.items(), key=lambda kv: float(kv[0])))},
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
