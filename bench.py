@@ -130,6 +130,23 @@ def derive_counters(dirs):
         wt = v.get("SQ_WAIT_ANY", float("nan")) / v.get("SQ_WAVE_CYCLES", float("nan"))
         ck = v.get("GRBM_GUI_ACTIVE", float("nan")) / 8.0 / dur
         print(f"| {fam} | {n} | {dur / 1e3:.1f} | {mf:.3f} | {wt:.3f} | {ck:.2f} |")
+    # LDS pass (when collected): the share of cycles the LDS of a CU is busy with
+    # indexed accesses (SQ_LDS_IDX_ACTIVE over GRBM_GUI_ACTIVE per XCD x 256 CUs),
+    # bank-conflict cycles per busy cycle, and the share of wave cycles spent
+    # waiting to issue LDS instructions
+    if not any("SQ_LDS_IDX_ACTIVE" in vals[f] for f in vals):
+        return
+    print()
+    print("| family | LDS busy / elapsed | bank conflicts / LDS busy | waiting on LDS issue / wave cycles |")
+    print("|---|---|---|---|")
+    for fam, _ in FAMILIES:
+        if fam not in vals or "SQ_LDS_IDX_ACTIVE" not in vals[fam]:
+            continue
+        v = {k: mean(x) for k, x in vals[fam].items()}
+        busy = v["SQ_LDS_IDX_ACTIVE"] / (v.get("GRBM_GUI_ACTIVE", float("nan")) / 8.0 * 256.0)
+        conf = v.get("SQ_LDS_BANK_CONFLICT", float("nan")) / v["SQ_LDS_IDX_ACTIVE"] if v["SQ_LDS_IDX_ACTIVE"] else 0.0
+        wl = v.get("SQ_WAIT_INST_LDS", float("nan")) / v.get("SQ_WAVE_CYCLES", float("nan"))
+        print(f"| {fam} | {busy:.3f} | {conf:.4f} | {wl:.3f} |")
 
 
 def derive_traffic_table(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir):
