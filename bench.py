@@ -761,7 +761,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the profile's passes are independent and "
-              "would shard by sequence or layer, which this build does not implement", file=sys.stderr)
+              "would shard by sequence or layer, which is not implemented", file=sys.stderr)
         sys.exit(2)
 
     import torch

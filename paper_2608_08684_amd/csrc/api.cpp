@@ -660,7 +660,7 @@ static rk_status window_compressed_final(const rk_model* m, const SeqTable& pst,
                                          int layer, const int32_t* pos, int64_t seq_stride, int b, void* xf_out,
                                          const Bufs& bf, hipStream_t s);
 
-// A group of cached-window passes, layer-synchronously (the survey's pass
+// A group of cached-window passes, layer-synchronously (pass
 // batching): the passes, ordered by their perturbed layer, join the batch at that
 // layer from the window's cached block input, and from then on every norm,
 // projection and feed-forward of a layer runs once over the window rows of all
