@@ -434,6 +434,22 @@ rk_status rk_policy_damage(const rk_model *m, const rk_batch *batch, int32_t win
                            const void *state, size_t state_bytes, float *d_out, float *kl_pos, float *logits_out,
                            void *workspace, size_t ws_bytes, void *stream);
 
+/* Several budget policies in one call: d_out[q * n_seqs + i] (and kl_pos [q,
+ * window rows], DEVICE fp32 or NULL) are rk_policy_damage's values for policy q
+ * (1 <= n_policies <= 16).  Per policy q: positions[q] (a HOST array of DEVICE
+ * pointers; NULL allowed when every n_keep of the policy is 0), layer offsets
+ * layer_offsets[q * n_layers + l] and counts n_keep[q * n_layers + l] (HOST),
+ * sequence stride seq_stride[q] (HOST int64 [n_policies]).  The policies are
+ * evaluated together from block 0: every norm, projection and feed-forward runs
+ * once per layer over the window rows of all of them, each attending to its own
+ * caches; the results are bitwise those of separate rk_policy_damage calls.
+ * Workspace: rk_workspace_size(m, rows, n_policies, RK_FLAG_CACHED_WINDOW).     */
+rk_status rk_policy_damage_group(const rk_model *m, const rk_batch *batch, int32_t window_start, int32_t n_policies,
+                                 const int32_t *const *positions, const int64_t *layer_offsets,
+                                 const int64_t *seq_stride, const int32_t *n_keep, const void *state,
+                                 size_t state_bytes, float *d_out, float *kl_pos, void *workspace, size_t ws_bytes,
+                                 void *stream);
+
 /* Spearman's rho of two profiles x, y [n] (Section 2, Table
  * sensitivity-correlation): the Pearson correlation of their ranks, ties sharing
  * the mean rank; NaN when a profile is constant.  Host only, float64.          */

@@ -125,6 +125,8 @@ def load() -> ctypes.CDLL:
                                               i64, i32, vp, sz, vp, vp, vp, sz, vp]),
         "rk_policy_damage": (st, [vp, ctypes.POINTER(_Batch), i32, vp, ctypes.POINTER(i64), i64, ctypes.POINTER(i32),
                                   vp, sz, vp, vp, vp, vp, sz, vp]),
+        "rk_policy_damage_group": (st, [vp, ctypes.POINTER(_Batch), i32, i32, ctypes.POINTER(vp), ctypes.POINTER(i64),
+                                        ctypes.POINTER(i64), ctypes.POINTER(i32), vp, sz, vp, vp, vp, sz, vp]),
         "rk_spearman": (st, [ctypes.POINTER(f64), ctypes.POINTER(f64), i32, ctypes.POINTER(f64)]),
         "rk_snapkv_state_size": (sz, [vp, i64, i32, i32]),
         "rk_snapkv_workspace_size": (sz, [vp, i64, i32, i32]),
@@ -295,6 +297,22 @@ class Model:
                                        int(seq_stride), keep, _ptr(state), state.numel() * state.element_size(),
                                        _ptr(d_out), _ptr(kl_pos), _ptr(logits_out), _ptr(workspace),
                                        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+    def policy_damage_group(self, batch: Batch, window_start: int, policies, state, d_out, workspace, kl_pos=None,
+                            stream=None):
+        """rk_policy_damage_group.  policies: sequence of (positions or None,
+        layer_offsets [L], seq_stride, n_keep [L]); d_out [len(policies), n_seqs]."""
+        L, G = self.cfg.n_layers, len(policies)
+        pos = (ctypes.c_void_p * G)(*[_ptr(p[0]) for p in policies])
+        offs = (ctypes.c_int64 * (G * L))(*[int(x) for p in policies for x in p[1]])
+        strides = (ctypes.c_int64 * G)(*[int(p[2]) for p in policies])
+        keep = (ctypes.c_int32 * (G * L))(*[int(x) for p in policies for x in p[3]])
+        if any(len(p[1]) != L or len(p[3]) != L for p in policies):
+            raise ValueError(f"layer_offsets and n_keep need {L} entries per policy")
+        _check(load().rk_policy_damage_group(self._h, ctypes.byref(batch._c), int(window_start), G, pos, offs, strides,
+                                             keep, _ptr(state), state.numel() * state.element_size(), _ptr(d_out),
+                                             _ptr(kl_pos), _ptr(workspace),
+                                             workspace.numel() * workspace.element_size(), _stream(stream)))
 
     # -- SnapKV consumer of the budgets
     def snapkv_state_size(self, rows: int, n_seqs: int, obs_window: int) -> int:

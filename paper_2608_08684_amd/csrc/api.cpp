@@ -289,6 +289,19 @@ struct WinBatch {
   const int32_t* const* pos;
   int64_t seq_stride;
   int n_keep;
+  // whole budget policies instead: at layer l, pass q attends to its own
+  // compressed prompt cache, pol->keep[q][l] retained positions per KV head at
+  // pol->pos[q] + pol->off[q][l] (per sequence at pol->stride[q]), or to the whole
+  // cache when that count is 0
+  const struct Policies* pol;
+};
+
+// Per pass of a group of whole budget policies (indexes of the group's batch).
+struct Policies {
+  const int32_t* pos[RK_MAX_GROUP];
+  const int64_t* off[RK_MAX_GROUP];    // HOST [n_layers]
+  const int32_t* keep[RK_MAX_GROUP];   // HOST [n_layers]
+  int64_t stride[RK_MAX_GROUP];
 };
 static rk_status batch_attention(const rk_model* m, int l, const Bufs& b, const WinBatch& wb, hipStream_t s);
 
@@ -587,6 +600,30 @@ static rk_status batch_attention(const rk_model* m, int l, const Bufs& b, const 
   int n_at_l = 0, alt = -1;
   for (int q = 0; q < wb.n; ++q)
     if (wb.layer[q] == l) { ++n_at_l; alt = q; }
+  if (wb.pol) {
+    // every pass reads its own (compressed or whole) prompt cache of this layer
+    const char* kv_l = (const char*)wb.wn->kv + (size_t)l * Rp * kc * a;
+    for (int q = 0; q < wb.n; ++q) {
+      const int keep = wb.pol->keep[q][l];
+      KvPrefix pk{};
+      if (keep > 0) {
+        RK_TRY(launch_prefix_gather(kv_l, kc, wb.pst->n, wb.pst->max_len, c.n_kv_heads, c.head_dim,
+                                    wb.pol->pos[q] + wb.pol->off[q][l], wb.pol->stride[q], keep, b.cpre, s));
+        pk.alt_pass = -1;
+        pk.k = (const bf16_t*)b.cpre;
+        pk.v = (const bf16_t*)b.cpre + kc / 2;
+        pk.ldk = pk.ldv = kc;
+        pk.P = keep;
+      } else {
+        pk = cache_prefix(m, *wb.wn, *wb.pst, l, nullptr);
+      }
+      Timed t("attention", s);
+      RK_TRY(launch_attention((const char*)b.qkv + (size_t)q * wb.rw * m->qkv_cols * a, m->qkv_cols,
+                              (char*)b.att + (size_t)q * wb.rw * m->attn_cols * a, m->attn_cols, *wb.wst, c.n_heads,
+                              c.n_kv_heads, c.head_dim, m->bf16, s, &pk));
+    }
+    return RK_OK;
+  }
   if (wb.pos) {
     // the passes ordered by layer: those below l read the full cache in one launch,
     // those starting at l (the last ones) their own compressed prompt cache
@@ -659,6 +696,9 @@ static rk_status batch_attention(const rk_model* m, int l, const Bufs& b, const 
 static rk_status window_compressed_final(const rk_model* m, const SeqTable& pst, const SeqTable& wst, const Win& wn,
                                          int layer, const int32_t* pos, int64_t seq_stride, int b, void* xf_out,
                                          const Bufs& bf, hipStream_t s);
+static rk_status window_policy_final(const rk_model* m, const SeqTable& pst, const SeqTable& wst, const Win& wn,
+                                     const int32_t* positions, const int64_t* layer_off, int64_t seq_stride,
+                                     const int32_t* n_keep, void* xf_out, const Bufs& bf, hipStream_t s);
 
 // A group of cached-window passes, layer-synchronously (pass
 // batching): the passes, ordered by their perturbed layer, join the batch at that
@@ -672,7 +712,8 @@ static rk_status window_compressed_final(const rk_model* m, const SeqTable& pst,
 static rk_status window_group_final(const rk_model* m, const SeqTable& pst, const SeqTable& wst, const Win& wn,
                                     int G, const int* layers, const float* alphas, const rk_perturb_params* p,
                                     int64_t max_rows, void* xp, const Bufs& b, hipStream_t s,
-                                    const int32_t* const* pos = nullptr, int64_t seq_stride = 0, int n_keep = 0) {
+                                    const int32_t* const* pos = nullptr, int64_t seq_stride = 0, int n_keep = 0,
+                                    const Policies* pol = nullptr) {
   const rk_model_config& c = m->cfg;
   const int64_t d = c.d_model, Rw = wst.rows, xstride = pad_rows(Rw) * d * act_bytes(m);
   const int L = c.n_layers, P = pst.max_len;
@@ -681,8 +722,10 @@ static rk_status window_group_final(const rk_model* m, const SeqTable& pst, cons
   if (B < 2) {
     for (int k = 0; k < G; ++k) {
       void* xk = (char*)xp + (size_t)k * xstride;
-      rk_status e = pos ? window_compressed_final(m, pst, wst, wn, layers[k], pos[k], seq_stride, n_keep, xk, b, s)
-                        : window_perturbed_final(m, pst, wst, wn, layers[k], alphas[k], p, xk, b, s);
+      rk_status e =
+          pol ? window_policy_final(m, pst, wst, wn, pol->pos[k], pol->off[k], pol->stride[k], pol->keep[k], xk, b, s)
+          : pos ? window_compressed_final(m, pst, wst, wn, layers[k], pos[k], seq_stride, n_keep, xk, b, s)
+                : window_perturbed_final(m, pst, wst, wn, layers[k], alphas[k], p, xk, b, s);
       if (e != RK_OK) return e;
     }
     return RK_OK;
@@ -695,10 +738,18 @@ static rk_status window_group_final(const rk_model* m, const SeqTable& pst, cons
     int lay[RK_MAX_GROUP];
     float al[RK_MAX_GROUP];
     const int32_t* ps[RK_MAX_GROUP];
+    Policies pc{};
     for (int q = 0; q < cb; ++q) {
-      lay[q] = layers[order[c0 + q]];
-      al[q] = alphas ? alphas[order[c0 + q]] : 0.0f;
-      ps[q] = pos ? pos[order[c0 + q]] : nullptr;
+      const int k = order[c0 + q];
+      lay[q] = layers[k];
+      al[q] = alphas ? alphas[k] : 0.0f;
+      ps[q] = pos ? pos[k] : nullptr;
+      if (pol) {
+        pc.pos[q] = pol->pos[k];
+        pc.off[q] = pol->off[k];
+        pc.keep[q] = pol->keep[k];
+        pc.stride[q] = pol->stride[k];
+      }
     }
     // batch table: sequence i of pass slot q at rows q * Rw + wst.off[i]
     SeqTable bst = wst;
@@ -718,7 +769,8 @@ static rk_status window_group_final(const rk_model* m, const SeqTable& pst, cons
       SeqTable at = bst;   // the active passes' rows
       at.n = active * wst.n;
       at.rows = (int32_t)(active * Rw);
-      const WinBatch wb{&wn, &pst, &wst, &at, active, lay, al, p, Rw, pos ? ps : nullptr, seq_stride, n_keep};
+      const WinBatch wb{&wn, &pst, &wst, &at, active, lay, al, p, Rw, pos ? ps : nullptr, seq_stride, n_keep,
+                        pol ? &pc : nullptr};
       rk_status e = run_block(m, j, b.h, b.h, b, at, nullptr, s, nullptr, nullptr, nullptr, &wb);
       if (e != RK_OK) return e;
     }
@@ -1275,6 +1327,23 @@ rk_status rk_snapkv_compress(const rk_model* m, const rk_batch* batch, const rk_
 
 }  // extern "C"
 
+// One budget policy's arguments (see rk_policy_damage).
+static rk_status check_policy(const rk_model* m, int32_t window_start, const int32_t* positions,
+                              const int64_t* layer_offsets, int64_t seq_stride, const int32_t* n_keep) {
+  int max_keep = 0;
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    if (n_keep[l] < 0 || n_keep[l] > window_start) { set_error("n_keep[%d] must be in [0, window_start]", l); return RK_ERR_ARG; }
+    if (n_keep[l] > 0 && layer_offsets[l] < 0) { set_error("layer_offsets[%d] must be >= 0", l); return RK_ERR_ARG; }
+    max_keep = std::max(max_keep, (int)n_keep[l]);
+  }
+  if (max_keep > 0 && !positions) { set_error("null positions"); return RK_ERR_ARG; }
+  if (max_keep > 0 && seq_stride < (int64_t)m->cfg.n_kv_heads * max_keep) {
+    set_error("seq_stride below n_kv_heads * max(n_keep)");
+    return RK_ERR_ARG;
+  }
+  return RK_OK;
+}
+
 // The set-up shared by the calls that evaluate a batch's window rows against its
 // window state: the prefix and window tables, the size checks, the workspace
 // carve-up (G passes per LM-head launch, workspace flags wf) and the window's
@@ -1382,18 +1451,7 @@ rk_status rk_policy_damage(const rk_model* m, const rk_batch* batch, int32_t win
     set_error("null layer_offsets, n_keep, state, d_out or workspace");
     return RK_ERR_ARG;
   }
-  const int L = m->cfg.n_layers;
-  int max_keep = 0;
-  for (int l = 0; l < L; ++l) {
-    if (n_keep[l] < 0 || n_keep[l] > window_start) { set_error("n_keep[%d] must be in [0, window_start]", l); return RK_ERR_ARG; }
-    if (n_keep[l] > 0 && layer_offsets[l] < 0) { set_error("layer_offsets[%d] must be >= 0", l); return RK_ERR_ARG; }
-    max_keep = std::max(max_keep, (int)n_keep[l]);
-  }
-  if (max_keep > 0 && !positions) { set_error("null positions"); return RK_ERR_ARG; }
-  if (max_keep > 0 && seq_stride < (int64_t)m->cfg.n_kv_heads * max_keep) {
-    set_error("seq_stride below n_kv_heads * max(n_keep)");
-    return RK_ERR_ARG;
-  }
+  if ((e = check_policy(m, window_start, positions, layer_offsets, seq_stride, n_keep)) != RK_OK) return e;
   WinCall c;
   const uint32_t wf = RK_FLAG_CACHED_WINDOW | (logits_out ? RK_FLAG_UNFUSED_KL : 0);
   if ((e = win_call(m, batch, window_start, state, state_bytes, workspace, ws_bytes, 1, wf, stream, &c)) != RK_OK)
@@ -1402,6 +1460,42 @@ rk_status rk_policy_damage(const rk_model* m, const rk_batch* batch, int32_t win
                                c.s)) != RK_OK)
     return e;
   return score_window(m, c, 1, logits_out, kl_pos, d_out);
+}
+
+rk_status rk_policy_damage_group(const rk_model* m, const rk_batch* batch, int32_t window_start, int32_t n_policies,
+                                 const int32_t* const* positions, const int64_t* layer_offsets,
+                                 const int64_t* seq_stride, const int32_t* n_keep, const void* state,
+                                 size_t state_bytes, float* d_out, float* kl_pos, void* workspace, size_t ws_bytes,
+                                 void* stream) {
+  rk_status e = check_batch(m, batch);
+  if (e != RK_OK) return e;
+  if ((e = check_window_model(m)) != RK_OK) return e;
+  if (!positions || !layer_offsets || !seq_stride || !n_keep || !state || !d_out || !workspace) {
+    set_error("null positions, layer_offsets, seq_stride, n_keep, state, d_out or workspace");
+    return RK_ERR_ARG;
+  }
+  if (n_policies < 1 || n_policies > RK_MAX_GROUP) { set_error("n_policies must be in [1, %d]", RK_MAX_GROUP); return RK_ERR_ARG; }
+  const int L = m->cfg.n_layers;
+  Policies pol{};
+  for (int q = 0; q < n_policies; ++q) {
+    pol.pos[q] = positions[q];
+    pol.off[q] = layer_offsets + (size_t)q * L;
+    pol.keep[q] = n_keep + (size_t)q * L;
+    pol.stride[q] = seq_stride[q];
+    if ((e = check_policy(m, window_start, pol.pos[q], pol.off[q], pol.stride[q], pol.keep[q])) != RK_OK) {
+      set_error("policy %d: %s", q, rk_last_error());
+      return e;
+    }
+  }
+  WinCall c;
+  if ((e = win_call(m, batch, window_start, state, state_bytes, workspace, ws_bytes, n_policies,
+                    RK_FLAG_CACHED_WINDOW, stream, &c)) != RK_OK)
+    return e;
+  const int zero[RK_MAX_GROUP] = {0};   // every policy's pass starts at block 0
+  if ((e = window_group_final(m, c.pst, c.wst, c.wn, n_policies, zero, nullptr, nullptr, c.st.rows, c.b.xp, c.b, c.s,
+                              nullptr, 0, 0, &pol)) != RK_OK)
+    return e;
+  return score_window(m, c, n_policies, nullptr, kl_pos, d_out);
 }
 
 size_t rk_workspace_size(const rk_model* m, int64_t max_rows, int32_t max_group, uint32_t flags) {

@@ -425,6 +425,33 @@ def test_policy_damage_validates_before_launching():
     lib.rk_model_destroy(h32)
 
 
+def test_policy_damage_group_validates_before_launching():
+    lib = rk.load()
+    fake = ctypes.c_void_p(0x1000)
+    offs = np.array([0, 100, 250], dtype=np.int64)
+    batch = rk._Batch(fake, offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 2, 0)
+    big = 1 << 40
+    st, h = _create(_FakeCfg())
+    assert st == rk.RK_OK
+
+    def call(G=2, keep=(10, 0, 5, 5), P=50, wb=big, null_pos=False):
+        pos = (ctypes.c_void_p * max(G, 1))(*([0x1000] * max(G, 1)))
+        o = (ctypes.c_int64 * 4)(0, 0, 0, 10)
+        strides = (ctypes.c_int64 * 2)(20, 20)
+        k = (ctypes.c_int32 * 4)(*keep)
+        return lib.rk_policy_damage_group(h, ctypes.byref(batch), P, G, None if null_pos else pos, o, strides, k,
+                                          fake, big, fake, None, fake, wb, None)
+    assert call(G=0) == rk.RK_ERR_ARG
+    assert call(G=17) == rk.RK_ERR_ARG
+    assert call(null_pos=True) == rk.RK_ERR_ARG
+    assert call(keep=(10, 0, 5, 60)) == rk.RK_ERR_ARG       # policy 1 keeps more than the prompt
+    assert "policy 1" in lib.rk_last_error().decode()
+    assert call(keep=(10, 0, 11, 11)) == rk.RK_ERR_ARG      # policy 1: stride below n_kv_heads * 11
+    assert call(P=100) == rk.RK_ERR_SHAPE
+    assert call(wb=16) == rk.RK_ERR_WORKSPACE
+    lib.rk_model_destroy(h)
+
+
 def test_size_queries_reject_rows_beyond_int32():
     lib = rk.load()
     st, h = _create(_FakeCfg())

@@ -319,3 +319,42 @@ def test_policy_from_snapkv_selection_and_budgets():
         D[name] = float(d.mean())
     assert D["whole"] == 0.0
     log(f"profile s = {s}; budgets ripple {ripple} (uniform {keep}); policy damage {D}")
+
+
+@pytest.mark.parametrize("lens,P", [([260, 300], 200), ([200, 260], 70)])
+def test_policy_group_equals_separate_calls(lens, P):
+    """Several budget policies in one rk_policy_damage_group call (batched from
+    block 0 when their window rows fit, one at a time otherwise) give bitwise the
+    d and window KL of separate rk_policy_damage calls; the all-whole policy gives
+    exactly 0."""
+    import torch
+    import paper_2608_08684_amd as rk
+    cfg = CASES[0][0]
+    L, Hkv = cfg.n_layers, cfg.n_kv_heads
+    W = F.make_weights(cfg)
+    run = Runner(cfg, W)
+    toks = F.make_tokens(F.make_workload("polg", cfg, lens, seed_id=91))
+    batch = make_batch(toks)
+    state, _ = _state(run, batch, P)
+    budget_sets = [[23, 0, 11], [0] * L, [5, 40, 17], [0, 9, 0]]
+    policies = []
+    for k, bl in enumerate(budget_sets):
+        if max(bl) == 0:
+            policies.append((None, [0] * L, 0, bl))
+            continue
+        flat, loff, stride, _ = _policy_positions(len(lens), Hkv, P, bl, 500 + 10 * k)
+        policies.append((torch.from_numpy(flat).cuda(), loff, stride, bl))
+    G = len(policies)
+    Rw = batch.rows - batch.n_seqs * P
+    ws = empty_bytes(run.model.workspace_size(batch.rows, G, rk.RK_FLAG_CACHED_WINDOW))
+    d = torch.empty(G, batch.n_seqs, dtype=torch.float32, device="cuda")
+    kl = torch.empty(G, Rw, dtype=torch.float32, device="cuda")
+    run.model.policy_damage_group(batch, P, policies, state, d, ws, kl_pos=kl)
+    torch.cuda.synchronize()
+    d, kl = d.cpu().numpy().astype(np.float64), kl.cpu().numpy().astype(np.float64)
+    for q, (pos, loff, stride, bl) in enumerate(policies):
+        d1, kl1, _ = _policy(run, batch, P, pos, loff, stride, bl, state)
+        np.testing.assert_array_equal(d[q], d1, err_msg=f"policy {q} d")
+        np.testing.assert_array_equal(kl[q], kl1, err_msg=f"policy {q} window KL")
+    assert np.all(d[1] == 0.0)
+    log(f"lens {lens} P {P}: {G} policies in one call = separate calls; d = {d.tolist()}")
