@@ -1,20 +1,23 @@
 #!/usr/bin/env python3
 """Benchmark of the RippleKV sensitivity profile on one MI355X.
 
-One step is the whole profiling path of Algorithm 1 on the GPT-2-small-shaped
-workload: for 8 calibration sequences of 2048 Zipf(1.1) tokens, a 12-layer
-d_model-768 bf16 decoder (12 heads x 64, SwiGLU 3072, vocab 32000) and both
-perturbation strengths alpha in {0.05, 0.1}: the clean reference pass, the 24
-resumed perturbed passes per sequence (prefix reuse), the fused LM-head + KL,
-the window and calibration means, then the budget mapping for every ratio and
-global budget.  Inputs (random-init weights, tokens) are synthetic and resident
-in HBM before timing.
+Default workload: the Llama-3-8B-shaped decoder at long context (32 layers,
+d_model 4096, 32 query / 8 KV heads of 128, SwiGLU 14336, vocab 128256, rotary
+theta 5e5, bf16) on 2 calibration sequences of 32768 Zipf(1.1) tokens with
+alpha in {0.05, 0.1, 0.2}.  One step is the whole profiling path of Algorithm 1
+for one (sequence, alpha) pair: the clean reference pass, the 32 resumed
+perturbed passes (prefix reuse), the fused LM-head + KL, the window and
+calibration means, then the budget mapping for every ratio and global budget;
+steps cycle over the six pairs.  With ``--workload NAME`` (and ``--step-unit
+profile``) one step is the whole profile of that workload instead.  Inputs
+(random-init weights, tokens) are synthetic and resident in HBM before timing.
 
 Prints one JSON line: perturbed token-layers per second (whole job), the
 roofline of the dominant kernel measured live with HIP events over the timed
 steps, and the CPU oracle's rate on a bounded sample of the same workload.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+                    [--workload NAME] [--step-unit auto|pair|profile]
                     [--window N | --snapkv | --damage]
 """
 from __future__ import annotations
@@ -231,7 +234,7 @@ def cpu_baseline_window(w, W, toks, window: int):
     reference included), every layer, the largest alpha."""
     from oracle import model as OM
     from oracle import profile as OPR
-    from tests.gpu_helpers import f32_weights  # noqa: E402
+    from fixtures import f32_weights
     cfg = w.model
     m = OM.Model(cfg, f32_weights(cfg, W), np.float32)
     t = toks[0]
@@ -270,7 +273,7 @@ def cpu_baseline(w, W, toks, local: bool = False):
     signal with `local`)."""
     from oracle import model as OM
     from oracle import profile as OPR
-    from tests.gpu_helpers import f32_weights  # noqa: E402  (exact fp32 view of the bf16 weights)
+    from fixtures import f32_weights  # exact fp32 view of the bf16 weights
     cfg = w.model
     prefix, layers = cpu_sample(cfg)
     m = OM.Model(cfg, f32_weights(cfg, W), np.float32)
@@ -357,7 +360,7 @@ def snapkv_main(args):
     import torch
     import fixtures as F
     import paper_2608_08684_amd as rk
-    from tests.gpu_helpers import make_batch
+    from paper_2608_08684_amd.inputs import batch_from_tokens as make_batch
     w = F.get_workload("llama3-8b-bf16")
     cfg = w.model
     L, H, Hkv, dh = cfg.n_layers, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim
@@ -451,7 +454,7 @@ def cpu_baseline_damage(w, W, toks, P: int, b: int):
     from oracle import damage as OD
     from oracle import model as OM
     from oracle import profile as OPR
-    from tests.gpu_helpers import f32_weights  # noqa: E402
+    from fixtures import f32_weights
     cfg = w.model
     m = OM.Model(cfg, f32_weights(cfg, W), np.float32)
     t = toks[0]
@@ -480,7 +483,7 @@ def cpu_baseline_policy(w, W, toks, P: int, budgets):
     from oracle import damage as OD
     from oracle import model as OM
     from oracle import profile as OPR
-    from tests.gpu_helpers import f32_weights  # noqa: E402
+    from fixtures import f32_weights
     cfg = w.model
     m = OM.Model(cfg, f32_weights(cfg, W), np.float32)
     t = toks[0]
@@ -513,7 +516,7 @@ def policy_main(args):
     import torch
     import fixtures as F
     import paper_2608_08684_amd as rk
-    from tests.gpu_helpers import make_batch, upload_weights
+    from paper_2608_08684_amd.inputs import batch_from_tokens as make_batch, upload_weights
     w = F.get_workload(args.workload)
     cfg = w.model
     L, Hkv, dh = cfg.n_layers, cfg.n_kv_heads, cfg.head_dim
@@ -523,7 +526,7 @@ def policy_main(args):
     b = int(round(DMG_RHO * P))
     t0 = time.perf_counter()
     W = F.make_weights(cfg)
-    model = rk.Model(cfg, upload_weights(cfg, W))
+    model = rk.Model(cfg, upload_weights(W))
     toks = F.make_tokens(w)
     batch = make_batch(toks)
     rows = batch.rows
@@ -639,7 +642,7 @@ def damage_main(args):
     import torch
     import fixtures as F
     import paper_2608_08684_amd as rk
-    from tests.gpu_helpers import make_batch, upload_weights
+    from paper_2608_08684_amd.inputs import batch_from_tokens as make_batch, upload_weights
     w = F.get_workload(args.workload)
     cfg = w.model
     L, Hkv, dh = cfg.n_layers, cfg.n_kv_heads, cfg.head_dim
@@ -649,7 +652,7 @@ def damage_main(args):
     b = int(round(DMG_RHO * P))
     t0 = time.perf_counter()
     W = F.make_weights(cfg)
-    model = rk.Model(cfg, upload_weights(cfg, W))
+    model = rk.Model(cfg, upload_weights(W))
     toks = F.make_tokens(w)
     batch = make_batch(toks)
     rows = batch.rows
@@ -729,12 +732,173 @@ def damage_main(args):
     print(json.dumps(res), flush=True)
 
 
+def budget_tref(w) -> int:
+    """Reference length of the global budget B = rho * T_ref * |A|: the common
+    length of fixed-length workloads, 8192 for the variable-length set."""
+    lens = w.lengths()
+    return lens[0] if len(set(lens)) == 1 else 8192
+
+
+def describe_lengths(lens) -> str:
+    if len(set(lens)) == 1:
+        return f"{len(lens)}x{lens[0]} tokens"
+    return f"{len(lens)} sequences of {min(lens)}-{max(lens)} tokens (sum {sum(lens)})"
+
+
+PAIR_FAMILIES = ("attention", "gemm_gate_up")
+
+
+def family_step_flops(fam: str, cfg, lens, n_block_runs: int) -> float:
+    """Algorithmic flops of one kernel family over `n_block_runs` block
+    evaluations of a batch with sequence lengths `lens` (every row evaluated)."""
+    H, dh, d, ff = cfg.n_heads, cfg.head_dim, cfg.d_model, cfg.d_ff
+    if fam == "attention":
+        per = sum(4.0 * H * dh * T * (T + 1) / 2 for T in lens)
+    elif fam == "gemm_gate_up":
+        per = 2.0 * sum(lens) * d * 2 * ff
+    else:
+        raise ValueError(fam)
+    return per * n_block_runs
+
+
+def pair_main(args):
+    """Long-context profile, one step per (sequence, alpha) pair.
+
+    A step is the whole profiling path for one calibration sequence at one
+    perturbation strength: its clean reference pass (every layer, clean
+    log-sum-exp), the resumed perturbed pass of every layer (prefix reuse), the
+    fused LM-head + KL, the window mean, then the budget mapping of the running
+    calibration mean of that alpha for every ratio and global budget.  Steps
+    cycle over the pairs (sequence-major within an alpha); the whole workload is
+    one cycle, whose clean passes the steps repeat once per alpha."""
+    import torch
+    import fixtures as F
+    import paper_2608_08684_amd as rk
+    from paper_2608_08684_amd.inputs import batch_from_tokens, upload_weights
+
+    w = F.get_workload(args.workload)
+    cfg = w.model
+    t0 = time.perf_counter()
+    W = F.make_weights(cfg)
+    model = rk.Model(cfg, upload_weights(W))
+    toks = F.make_tokens(w)
+    lens = w.lengths()
+    N, L = len(lens), cfg.n_layers
+    alphas = list(w.alphas)
+    batches = [batch_from_tokens([toks[i]], seq_index0=i) for i in range(N)]
+    pairs = [(i, a) for a in range(len(alphas)) for i in range(N)]
+    max_rows = max(lens)
+    G = min(args.max_group, rk.RK_MAX_GROUP)
+    layers = list(range(L))
+    flags = 0   # eager launches: consecutive steps differ in their arguments, and ms-long kernels hide launches
+    ws = torch.empty(model.workspace_size(max_rows, G, rk.RK_WS_CLEAN_STATE), dtype=torch.uint8, device="cuda")
+    s_out = torch.empty(1, L, dtype=torch.float32, device="cuda")
+    d_out = torch.empty(1, 1, L, dtype=torch.float32, device="cuda")
+    T_ref = budget_tref(w)
+    budgets = [int(round(rho * T_ref * L)) for rho in (0.1, 0.2, 0.3)]
+    dsum = np.zeros((len(alphas), N, L))
+    have = np.zeros((len(alphas), N), dtype=bool)
+    log(f"fixtures ready in {time.perf_counter() - t0:.1f} s; {len(pairs)} (sequence, alpha) pairs, "
+        f"max_rows {max_rows}, group {G}")
+
+    def step(k):
+        i, a = pairs[k % len(pairs)]
+        model.sensitivity_profile(batches[i], layers, [alphas[a]], s_out, ws, max_rows, G, d_out=d_out, flags=flags)
+        dsum[a, i] = d_out.cpu().numpy().astype(np.float64)[0, 0]     # synchronises
+        have[a, i] = True
+        s_cal = dsum[a][have[a]].mean(axis=0)        # calibration mean over the sequences done so far
+        return [rk.layer_budgets(s_cal, B, r)[1] for r in w.ratios for B in budgets]
+
+    for k in range(args.warmup):
+        tw = time.perf_counter()
+        rk.timing_begin(PAIR_FAMILIES[k % 2])
+        step(k)
+        rk.timing_end()
+        log(f"warm-up step {k + 1}/{args.warmup} (pair {pairs[k % len(pairs)]}): {time.perf_counter() - tw:.2f} s")
+    torch.cuda.synchronize()
+    fam_ms = {f: 0.0 for f in PAIR_FAMILIES}
+    fam_n = {f: 0 for f in PAIR_FAMILIES}
+    fam_steps = {f: 0 for f in PAIR_FAMILIES}
+    tl = 0
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        kk = args.warmup + k
+        f = PAIR_FAMILIES[k % 2]           # the timed family alternates step by step
+        rk.timing_begin(f)
+        step(kk)
+        n, ms = rk.timing_end()
+        fam_n[f] += n
+        fam_ms[f] += ms
+        fam_steps[f] += 1
+        tl += lens[pairs[kk % len(pairs)][0]] * L
+        log(f"timed step {k + 1}/{args.steps} (pair {pairs[kk % len(pairs)]}) done at "
+            f"{time.perf_counter() - t0:.2f} s")
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+    value = tl / elapsed
+
+    # per family: algorithmic flops per launch (block evaluations per step: the
+    # clean pass's L plus sum_l (L - l) resumed ones), live HIP-event durations
+    runs = L + sum(L - l for l in layers)
+    kern = {}
+    for f in PAIR_FAMILIES:
+        if not fam_n[f]:
+            continue
+        per_launch = family_step_flops(f, cfg, [lens[0]], runs) / (fam_n[f] / fam_steps[f])
+        avg = fam_ms[f] / fam_n[f]
+        kern[f] = {"launches": fam_n[f], "avg_ms": round(avg, 4), "flop_per_launch": per_launch,
+                   "achieved": round(per_launch / (avg / 1e3) / 1e12, 2),
+                   "ms_per_step": round(fam_ms[f] / fam_steps[f], 1)}
+    dom = max(kern, key=lambda f: kern[f]["ms_per_step"])
+    kd = kern[dom]
+    roof = {"bound": "mfma", "achieved": kd["achieved"], "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(kd["achieved"] / BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": dom,
+            "launches": kd["launches"], "avg_ms": kd["avg_ms"], "flop_per_launch": kd["flop_per_launch"]}
+    for f, r in kern.items():
+        log(f"{f}: {r['launches']} launches, avg {r['avg_ms']:.4f} ms, {r['achieved']:.1f} TFLOP/s, "
+            f"{r['ms_per_step']:.0f} ms per step")
+    pair_flops = step_flops(cfg, [lens[0]], layers, [alphas[0]])
+    cfg_flops = step_flops(cfg, lens, layers, alphas)
+    util = {"step_tflop": round(pair_flops / 1e12, 2), "achieved": round(pair_flops / (ms_per_step / 1e3) / 1e12, 1),
+            "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(pair_flops / (ms_per_step / 1e3) / 1e12 / BF16_PEAK_TFLOPS, 4)}
+    # the whole workload (one clean pass per sequence, shared by the alphas) at the
+    # steps' algorithmic rate
+    wall_est = cfg_flops / (pair_flops / (ms_per_step / 1e3)) * 1e3
+    res = {
+        "metric": "perturbed token-layers/s (sensitivity-profile throughput)",
+        "value": round(value, 1), "unit": "token-layers/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (random-init N(0,0.02) weights, Zipf(1.1) tokens)",
+        "launch": "eager",
+        "config": {"workload": f"{w.name}: {L}L d{cfg.d_model} {cfg.n_heads}q/{cfg.n_kv_heads}kv x{cfg.head_dim} "
+                               f"FFN{cfg.d_ff} V{cfg.vocab} theta {cfg.rope_theta:g}; {describe_lengths(lens)}; "
+                               f"alpha {alphas}; all layers; ratios {list(w.ratios)}; budgets {budgets}; one step = "
+                               f"one (sequence, alpha) pair: its clean pass, all {L} perturbed passes, fused "
+                               f"LM-head + KL, means and the budget mapping; steps cycle over the {len(pairs)} pairs",
+                   "perturbed_token_layers_per_step": lens[0] * L,
+                   "profile_wall_ms_est": round(wall_est, 1),
+                   "profile_wall_note": "whole workload (one clean pass per sequence) at the steps' algorithmic "
+                                        f"rate: {cfg_flops / 1e15:.2f} PFLOP"},
+        "roofline": roof,
+        "kernels": kern,
+        "mfma_util": util,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, W, toks)
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="gpt2s-bf16")
+    ap.add_argument("--workload", default="llama3-8b-long-bf16")
+    ap.add_argument("--step-unit", choices=("auto", "pair", "profile"), default="auto",
+                    help="pair: one step = one (sequence, alpha) pair of the profile; profile: one step = the "
+                         "whole profile of the workload; auto: pair for the 2x32768 workload, else profile")
     ap.add_argument("--max-group", type=int, default=12)
     ap.add_argument("--family", default="gemm_gate_up", help="kernel family for the roofline figure")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -798,15 +962,24 @@ def main():
     if args.policy:
         policy_main(args)
         return
+    unit = args.step_unit
+    if unit == "auto":
+        unit = "pair" if args.workload == "llama3-8b-long-bf16" and args.window == 0 and args.signal == "downstream" \
+            else "profile"
+    if unit == "pair":
+        if args.window or args.signal != "downstream":
+            raise SystemExit("--step-unit pair runs the resumed downstream profile only")
+        pair_main(args)
+        return
     import fixtures as F
     import paper_2608_08684_amd as rk
-    from tests.gpu_helpers import make_batch, upload_weights
+    from paper_2608_08684_amd.inputs import batch_from_tokens as make_batch, upload_weights
 
     w = F.get_workload(args.workload)
     cfg = w.model
     t0 = time.perf_counter()
     W = F.make_weights(cfg)
-    dw = upload_weights(cfg, W)
+    dw = upload_weights(W)
     toks = F.make_tokens(w)
     batch = make_batch(toks)
     model = rk.Model(cfg, dw)
@@ -828,7 +1001,7 @@ def main():
                      dtype=torch.uint8, device="cuda")
     s_out = torch.empty(len(alphas), len(layers), dtype=torch.float32, device="cuda")
     d_out = torch.empty(len(alphas), batch.n_seqs, len(layers), dtype=torch.float32, device="cuda")
-    T_ref = max(w.lengths())
+    T_ref = budget_tref(w)
     budgets = [int(round(rho * T_ref * len(layers))) for rho in (0.1, 0.2, 0.3)]
 
     def step():
@@ -921,7 +1094,7 @@ def main():
         "data": "synthetic (random-init N(0,0.02) weights, Zipf(1.1) tokens)",
         "launch": "eager" if args.no_graph else "HIP graph replay",
         "config": {"workload": f"{w.name}: {cfg.n_layers}L d{cfg.d_model} {cfg.n_heads}x{cfg.head_dim} "
-                               f"FFN{cfg.d_ff} V{cfg.vocab}; {batch.n_seqs}x{T_ref} tokens; "
+                               f"FFN{cfg.d_ff} V{cfg.vocab}; {describe_lengths(w.lengths())}; "
                                f"alpha {alphas}; all layers; ratios {list(w.ratios)}; budgets {budgets}{mode}",
                    "perturbed_token_layers_per_step": tokens_layers, "profile_wall_ms": round(ms_per_step, 3)},
         "roofline": roof,

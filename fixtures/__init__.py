@@ -35,7 +35,7 @@ import numpy as np
 __all__ = [
     "ModelConfig", "CalibConfig", "Workload", "WORKLOADS", "get_workload",
     "bf16_round", "bf16_bits", "make_weights", "make_tokens", "make_lengths",
-    "zipf_cdf", "weight_shapes",
+    "zipf_cdf", "weight_shapes", "f32_weights",
 ]
 
 
@@ -222,6 +222,18 @@ def make_weights(m: ModelConfig, *, bits: Optional[bool] = None, threads: int = 
     out["attn_norm"] = [one.copy() for _ in range(m.n_layers)]
     out["mlp_norm"] = [one.copy() for _ in range(m.n_layers)]
     out["final_norm"] = one.copy()
+    return out
+
+
+def f32_weights(cfg: ModelConfig, W: dict) -> dict:
+    """Exact fp32 view of a weight dict (bf16 bit patterns upcast; fp32 kept)."""
+    def cv(a):
+        if a is None:
+            return None
+        return bf16_to_f32(a) if a.dtype == np.uint16 else a
+    out = {k: cv(W[k]) for k in ("tok_emb", "lm_head", "final_norm")}
+    for k in ("w_qkv", "w_o", "w_gate_up", "w_down", "attn_norm", "mlp_norm"):
+        out[k] = [cv(x) for x in W[k]]
     return out
 
 

@@ -63,7 +63,11 @@ def rope(x: np.ndarray, positions: np.ndarray, theta: float) -> np.ndarray:
 
 
 def silu(x: np.ndarray) -> np.ndarray:
-    return x / (x.dtype.type(1) + np.exp(-x))
+    """x / (1 + exp(-x)), elementwise in x's dtype (PyTorch CPU operations, which
+    use every host core on the large feed-forward activations)."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x))
+    return (t / (1 + torch.exp(-t))).numpy()
 
 
 def softmax(x: np.ndarray, axis: int = -1) -> np.ndarray:
@@ -72,22 +76,34 @@ def softmax(x: np.ndarray, axis: int = -1) -> np.ndarray:
     return e / np.sum(e, axis=axis, keepdims=True)
 
 
+def _heads_first(x: np.ndarray):
+    """[T, n, d_h] numpy -> [n, T, d_h] contiguous torch CPU tensor (same dtype)."""
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x)).permute(1, 0, 2).contiguous()
+
+
 def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_chunk: int = 1024) -> np.ndarray:
-    """q [T, H, d_h], k/v [T, H_kv, d_h] -> o [T, H, d_h]; position t sees u <= t."""
+    """q [T, H, d_h], k/v [T, H_kv, d_h] -> o [T, H, d_h]; position t sees u <= t.
+
+    Per query head and chunk of query rows: scores, mask, max-subtracted softmax,
+    weighted sum of Values.  Written with plain PyTorch CPU tensor operations
+    (which use every host core) in the dtype of the inputs."""
+    import torch
     T, H, dh = q.shape
     Hkv = k.shape[1]
     group = H // Hkv
-    scale = q.dtype.type(1.0 / np.sqrt(dh))
-    o = np.empty_like(q)
+    scale = float(q.dtype.type(1.0 / np.sqrt(dh)))
+    qh, kh, vh = _heads_first(q), _heads_first(k), _heads_first(v)
+    o = torch.empty_like(qh)
     for hq in range(H):
         hk = hq // group
         for t0 in range(0, T, q_chunk):
             t1 = min(T, t0 + q_chunk)
-            s = (q[t0:t1, hq, :] @ k[:t1, hk, :].T) * scale          # [tq, t1]
-            mask = np.arange(t1)[None, :] > np.arange(t0, t1)[:, None]
-            s = np.where(mask, -np.inf, s)
-            o[t0:t1, hq, :] = softmax(s, axis=-1) @ v[:t1, hk, :]
-    return o
+            s = (qh[hq, t0:t1] @ kh[hk, :t1].T) * scale                  # [tq, t1]
+            mask = torch.arange(t1)[None, :] > torch.arange(t0, t1)[:, None]
+            s = s.masked_fill(mask, float("-inf"))
+            o[hq, t0:t1] = torch.softmax(s, dim=-1) @ vh[hk, :t1]
+    return o.permute(1, 0, 2).contiguous().numpy()
 
 
 def cached_attention(q: np.ndarray, k_prefix: np.ndarray, v_prefix: np.ndarray, k: np.ndarray, v: np.ndarray,
@@ -98,23 +114,25 @@ def cached_attention(q: np.ndarray, k_prefix: np.ndarray, v_prefix: np.ndarray, 
     [P, H_kv, d_h] are the cached states of positions 0..P-1.  New position
     P + j sees every cached position and the new positions P + j' with j' <= j.
     """
+    import torch
     W, H, dh = q.shape
     P = k_prefix.shape[0]
     Hkv = k.shape[1]
     group = H // Hkv
-    scale = q.dtype.type(1.0 / np.sqrt(dh))
-    kk = np.concatenate([k_prefix, k], axis=0)
-    vv = np.concatenate([v_prefix, v], axis=0)
-    o = np.empty_like(q)
+    scale = float(q.dtype.type(1.0 / np.sqrt(dh)))
+    qh = _heads_first(q)
+    kk = _heads_first(np.concatenate([k_prefix, k], axis=0))
+    vv = _heads_first(np.concatenate([v_prefix, v], axis=0))
+    o = torch.empty_like(qh)
     for hq in range(H):
         hk = hq // group
         for t0 in range(0, W, q_chunk):
             t1 = min(W, t0 + q_chunk)
-            s = (q[t0:t1, hq, :] @ kk[:P + t1, hk, :].T) * scale      # [tq, P + t1]
-            mask = np.arange(P + t1)[None, :] > (P + np.arange(t0, t1))[:, None]
-            s = np.where(mask, -np.inf, s)
-            o[t0:t1, hq, :] = softmax(s, axis=-1) @ vv[:P + t1, hk, :]
-    return o
+            s = (qh[hq, t0:t1] @ kk[hk, :P + t1].T) * scale              # [tq, P + t1]
+            mask = torch.arange(P + t1)[None, :] > (P + torch.arange(t0, t1))[:, None]
+            s = s.masked_fill(mask, float("-inf"))
+            o[hq, t0:t1] = torch.softmax(s, dim=-1) @ vv[hk, :P + t1]
+    return o.permute(1, 0, 2).contiguous().numpy()
 
 
 def block(m: Model, l: int, h: np.ndarray, positions: np.ndarray,

@@ -105,9 +105,7 @@ def profile_layer(m: M.Model, st: M.CleanState, tokens: np.ndarray, seq: int, la
     """(d_{i,l}, KL_t for every position) for one sequence and one layer."""
     xp = perturbed_final(m, st, tokens, seq, layer, p, full_recompute)
     kl = kl_per_position(m, st.xfinal, xp)
-    w0 = min(max(p.window_start, 0), len(tokens))
-    d = float(np.mean(kl[w0:])) if w0 < len(tokens) else 0.0
-    return d, kl
+    return window_mean(kl, p.window_start), kl
 
 
 def local_response_rows(h_ref: np.ndarray, h_pert: np.ndarray) -> np.ndarray:
@@ -121,8 +119,12 @@ def local_response_rows(h_ref: np.ndarray, h_pert: np.ndarray) -> np.ndarray:
 
 
 def window_mean(x: np.ndarray, window_start: int) -> float:
-    w0 = min(max(window_start, 0), len(x))
-    return float(np.mean(x[w0:])) if w0 < len(x) else 0.0
+    """d_{i,l}: the mean of the per-position values over W_i = [window_start, T_i)
+    (Eq. sample-response).  An empty window has no mean and raises."""
+    w0 = max(window_start, 0)
+    if w0 >= len(x):
+        raise ValueError(f"empty window: window_start {window_start} with {len(x)} positions")
+    return float(np.mean(x[w0:]))
 
 
 def local_profile_layer(m: M.Model, st: M.CleanState, tokens: np.ndarray, seq: int, layer: int,

@@ -879,6 +879,19 @@ static rk_status check_batch(const rk_model* m, const rk_batch* b) {
   return RK_OK;
 }
 
+// The window W_i = [window_start, T_i) of every sequence must hold a position:
+// d_{i,l} is a mean over it (Eq. sample-response), undefined when it is empty.
+static rk_status check_windows(const SeqTable& st, int32_t window_start) {
+  for (int k = 0; k < st.n; ++k) {
+    const int len = st.off[k + 1] - st.off[k];
+    if (len <= window_start) {
+      set_error("sequence %d (%d tokens) has an empty window: window_start %d", k, len, window_start);
+      return RK_ERR_SHAPE;
+    }
+  }
+  return RK_OK;
+}
+
 // ----------------------------------------------------------------------------- state tags
 // Each state written by rk_reference_forward (window start -1) or
 // rk_window_reference records which model and batch produced it: the model
@@ -1077,6 +1090,17 @@ static rk_status run_graphed(std::vector<uint64_t> key, F&& run, hipStream_t s) 
   return RK_OK;
 }
 
+// Forget the recorded sequence when its model goes away: a new model at the
+// same address must never replay launches baked for the old one.
+static void drop_graph(const rk_model* m) {
+  std::lock_guard<std::mutex> lock(g_graph_mu);
+  if (g_graph.exec && !g_graph.key.empty() && g_graph.key[0] == (uint64_t)(uintptr_t)m) {
+    (void)hipGraphExecDestroy(g_graph.exec);
+    g_graph.exec = nullptr;
+    g_graph.key.clear();
+  }
+}
+
 }  // namespace rk
 
 using namespace rk;
@@ -1175,7 +1199,11 @@ rk_status rk_model_create(const rk_model_config* cfg, const rk_model_weights* w,
   return RK_OK;
 }
 
-void rk_model_destroy(rk_model* m) { delete m; }
+void rk_model_destroy(rk_model* m) {
+  if (!m) return;
+  drop_graph(m);
+  delete m;
+}
 
 size_t rk_clean_state_size(const rk_model* m, int64_t n_rows) {
   if (!m || n_rows < 1 || n_rows > kMaxRows) return 0;
@@ -1530,6 +1558,7 @@ rk_status rk_profile_layer(const rk_model* m, const rk_batch* batch, int32_t lay
   if (!(alpha >= 0.0f) || !isfinite(alpha)) { set_error("alpha must be finite and >= 0"); return RK_ERR_ARG; }
   SeqTable st;
   if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  if ((e = check_windows(st, p->window_start)) != RK_OK) return e;
   const bool local = (p->flags & RK_FLAG_LOCAL_SIGNAL) != 0;
   if (local && logits_out) { set_error("RK_FLAG_LOCAL_SIGNAL produces no logits"); return RK_ERR_ARG; }
   const bool unfused = !local && (!m->bf16 || logits_out || (p->flags & RK_FLAG_UNFUSED_KL));
@@ -1625,6 +1654,10 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
     if (len < 0) { set_error("offsets must be non-decreasing"); return RK_ERR_SHAPE; }
     if (len > max_rows) { set_error("sequence %d (%lld tokens) exceeds max_rows", i, (long long)len); return RK_ERR_SHAPE; }
     if (len == 0) { set_error("sequence %d is empty", i); return RK_ERR_SHAPE; }
+    if (len <= p->window_start) {
+      set_error("sequence %d (%lld tokens) has an empty window: window_start %d", i, (long long)len, p->window_start);
+      return RK_ERR_SHAPE;
+    }
     if ((p->flags & RK_FLAG_CACHED_WINDOW) && (p->window_start < 1 || len <= p->window_start)) {
       set_error("sequence %d (%lld tokens) needs a non-empty prefix and window around window_start %d", i,
                 (long long)len, p->window_start);
@@ -1732,6 +1765,7 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
   std::vector<uint64_t> key;
   auto put = [&](uint64_t v) { key.push_back(v); };
   put((uint64_t)(uintptr_t)m);
+  put(m->ident);   // the config (dims, dtype, rotary theta, RMSNorm eps) and the weight pointers
   put((uint64_t)(uintptr_t)m->tok_emb); put((uint64_t)(uintptr_t)m->lm_head); put((uint64_t)(uintptr_t)m->final_norm);
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     put((uint64_t)(uintptr_t)m->w_qkv[l]); put((uint64_t)(uintptr_t)m->w_o[l]);

@@ -19,40 +19,16 @@ def log(msg: str):
 
 def upload_weights(cfg, W: dict):
     """fixtures.make_weights(cfg) output (bf16 bits or fp32) -> dict of cuda tensors."""
-    import torch
-    dev = torch.device("cuda")
-
-    def up(a):
-        a = np.ascontiguousarray(a)
-        if a.dtype == np.uint16:
-            return torch.from_numpy(a.view(np.int16)).to(dev)
-        return torch.from_numpy(a.astype(np.float32, copy=False)).to(dev)
-
-    out = {"tok_emb": up(W["tok_emb"]), "lm_head": up(W["lm_head"]), "final_norm": up(W["final_norm"])}
-    for k in ("w_qkv", "w_o", "w_gate_up", "w_down", "attn_norm", "mlp_norm"):
-        out[k] = [up(x) for x in W[k]]
-    return out
+    from paper_2608_08684_amd.inputs import upload_weights as up
+    return up(W)
 
 
-def f32_weights(cfg, W: dict) -> dict:
-    """Exact fp32 view of the weights for the oracle (bf16 bits upcast)."""
-    def cv(a):
-        if a is None:
-            return None
-        return F.bf16_to_f32(a) if a.dtype == np.uint16 else a
-    out = {k: cv(W[k]) for k in ("tok_emb", "lm_head", "final_norm")}
-    for k in ("w_qkv", "w_o", "w_gate_up", "w_down", "attn_norm", "mlp_norm"):
-        out[k] = [cv(x) for x in W[k]]
-    return out
+f32_weights = F.f32_weights
 
 
 def make_batch(token_seqs, seq_index0: int = 0):
-    import torch
-    import paper_2608_08684_amd as rk
-    offs = np.zeros(len(token_seqs) + 1, dtype=np.int64)
-    offs[1:] = np.cumsum([len(t) for t in token_seqs])
-    toks = torch.from_numpy(np.concatenate(token_seqs).astype(np.int32)).cuda()
-    return rk.Batch(toks, offs, seq_index0)
+    from paper_2608_08684_amd.inputs import batch_from_tokens
+    return batch_from_tokens(token_seqs, seq_index0)
 
 
 def empty_bytes(n: int):

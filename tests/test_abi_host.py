@@ -203,6 +203,31 @@ def test_profile_entry_points_validate_before_launching():
     lib.rk_model_destroy(h)
 
 
+def test_empty_windows_are_rejected():
+    """d_{i,l} is a mean over W_i = [window_start, T_i) (Eq. sample-response): a
+    sequence with T_i <= window_start has no window, so both the single-layer and
+    the whole-profile entry points refuse the batch (RK_ERR_SHAPE) instead of
+    averaging a 0 into s, in the resumed and in the cached-window mode."""
+    lib = rk.load()
+    st, h = _create(_FakeCfg())
+    assert st == rk.RK_OK
+    fake = ctypes.c_void_p(0x1000)
+    offs = np.array([0, 100, 250], dtype=np.int64)      # lengths 100 and 150
+    batch = rk._Batch(fake, offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 2, 0)
+    big = 1 << 40
+    lay = (ctypes.c_int32 * 2)(0, 1)
+    alp = (ctypes.c_float * 1)(0.1)
+    for flags in (0, rk.RK_FLAG_CACHED_WINDOW):
+        for ws in (100, 120, 150, 400):
+            p = rk._Params(2, ws, 0, 0, flags)
+            assert lib.rk_profile_layer(h, ctypes.byref(batch), 0, 0.1, ctypes.byref(p), fake, big, fake, None,
+                                        None, fake, big, None) == rk.RK_ERR_SHAPE, (flags, ws)
+            assert lib.rk_sensitivity_profile(h, ctypes.byref(batch), lay, 2, alp, 1, ctypes.byref(p), 1000, 1,
+                                              fake, None, fake, big, None) == rk.RK_ERR_SHAPE, (flags, ws)
+            assert b"empty window" in lib.rk_last_error() or flags, lib.rk_last_error()
+    lib.rk_model_destroy(h)
+
+
 def test_binding_fails_loudly_without_library(monkeypatch):
     monkeypatch.setattr(rk, "_lib", None)
     monkeypatch.setattr(rk, "LIB_PATH", "/nonexistent/librk.so")

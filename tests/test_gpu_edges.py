@@ -3,9 +3,10 @@
 * sequences of one and two tokens, and lengths on and next to the 64-key and
   128-query tile boundaries, in one batch (bf16 GQA model and the fp32 model):
   d_{i,l} and the KL of every position against the oracle;
-* windows that are empty (window_start >= T_i gives d = 0 by definition) or hold
-  a single position; an eligible range that is empty (protect_head >= T_i) gives
-  exactly 0;
+* windows that hold a single position (the sequences longer than the window
+  start, as their own batch); a batch with an empty window (window_start >=
+  T_i) is refused with RK_ERR_SHAPE; an eligible range that is empty
+  (protect_head >= T_i) gives exactly 0;
 * a calibration set of 70 sequences, more than one batch holds (64), split by
   rk_sensitivity_profile into consecutive batches: s is the unweighted mean of
   the 70 per-sequence values, each equal to its single-batch value;
@@ -16,6 +17,7 @@ import numpy as np
 import pytest
 
 import fixtures as F
+import paper_2608_08684_amd as rk
 from oracle import model as OM
 from oracle import profile as OPR
 
@@ -47,17 +49,27 @@ def test_short_and_boundary_lengths(cfg):
     cs = run.clean(batch)
     off = np.concatenate([[0], np.cumsum(LENS)])
     sts = [OM.clean_pass(m, t) for t in toks]
+    # the sequences whose window [64, T) is not empty, as a batch of their own
+    keep = [k for k, T in enumerate(LENS) if T > 64]
+    sub_toks = [toks[k] for k in keep]
+    sub = make_batch(sub_toks)
+    sub_cs = run.clean(sub)
+    sub_off = np.concatenate([[0], np.cumsum([LENS[k] for k in keep])])
+    sub_sts = [OM.clean_pass(m, t) for t in sub_toks]
     for l in range(cfg.n_layers):
         for ws in (0, 1, 64):
-            d, kl, _ = run.layer(batch, cs, l, 0.1, window_start=ws)
+            whole = ws < min(LENS)
+            bt, cst, tk, of, ss = (batch, cs, toks, off, sts) if whole else (sub, sub_cs, sub_toks, sub_off, sub_sts)
+            d, kl, _ = run.layer(bt, cst, l, 0.1, window_start=ws)
             ref = []
-            for k, t in enumerate(toks):
-                dk, klk = OPR.profile_layer(m, sts[k], t, k, l, OPR.PerturbParams(0.1, window_start=ws))
+            for k, t in enumerate(tk):
+                dk, klk = OPR.profile_layer(m, ss[k], t, k, l, OPR.PerturbParams(0.1, window_start=ws))
                 ref.append(dk)
-                _kl_rows_close(kl[off[k]:off[k + 1]], klk, f"{cfg.dtype} layer {l} seq {k} (T={LENS[k]})")
-                if ws >= LENS[k]:
-                    assert d[k] == 0.0, "an empty window gives d = 0"
+                _kl_rows_close(kl[of[k]:of[k + 1]], klk, f"{cfg.dtype} layer {l} seq {k} (T={len(t)})")
             assert_kl_close(d, ref, f"{cfg.dtype} layer {l} window_start {ws}")
+            if not whole:
+                with pytest.raises(rk.RKError, match="RK_ERR_SHAPE"):
+                    run.layer(batch, cs, l, 0.1, window_start=ws)
         # nothing eligible: exactly zero everywhere
         d0, kl0, _ = run.layer(batch, cs, l, 0.5, protect_head=max(LENS))
         assert np.all(d0 == 0.0) and np.all(kl0 == 0.0)

@@ -76,3 +76,41 @@ def test_graph_timing_sessions():
         assert ms > 0.0
     # clean pass (3 layers) + passes at layers 0, 1, 2 (3 + 2 + 1 blocks)
     assert counts == [9, 9, 9, 9], counts
+
+
+def test_graph_not_replayed_for_a_recreated_model():
+    """A model destroyed and created again on the same weight buffers with another
+    rotary theta and RMSNorm eps (it usually lands at the same host address) must
+    not replay the launches recorded for the old model: the graphed call equals
+    the eager call of the new model, and differs from the old model's result."""
+    import torch
+    import paper_2608_08684_amd as rk
+    cfg, run, batch = _setup()
+    layers, alphas = [0, 1, 2], [0.1]
+    rows = batch.rows
+    ws = empty_bytes(run.model.workspace_size(rows, 3, rk.RK_WS_CLEAN_STATE))
+    s = torch.empty(1, 3, dtype=torch.float32, device="cuda")
+
+    def graphed(model):
+        for _ in range(2):      # the eager first call records, the second replays
+            s.fill_(-1.0)
+            model.sensitivity_profile(batch, layers, alphas, s, ws, rows, 3, flags=rk.RK_FLAG_GRAPH)
+            torch.cuda.synchronize()
+        return s.cpu().numpy().astype(np.float64)
+
+    s_old = graphed(run.model)
+    weights = run.model.weights
+    run.model.close()
+    import dataclasses
+    cfg2 = dataclasses.replace(cfg, rope_theta=5.0e5, rms_eps=1.0e-6)
+    m2 = rk.Model(cfg2, weights)
+    s_new = graphed(m2)
+    s_eager = np.zeros_like(s_new)
+    st = torch.empty(1, 3, dtype=torch.float32, device="cuda")
+    m2.sensitivity_profile(batch, layers, alphas, st, ws, rows, 3, flags=0)
+    torch.cuda.synchronize()
+    s_eager[:] = st.cpu().numpy()
+    assert np.array_equal(s_new, s_eager)
+    assert not np.array_equal(s_new, s_old)
+    m2.close()
+    log(f"re-created model: graphed {s_new[0].tolist()} = eager; old model {s_old[0].tolist()}")

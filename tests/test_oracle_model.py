@@ -257,6 +257,14 @@ def test_protect_and_window(small):
     # the window mean is the mean over [window_start, T)
     d_w, kl_w = P.profile_layer(m, st, t, 0, 1, P.PerturbParams(0.1, window_start=50))
     assert d_w == pytest.approx(np.mean(kl_all[50:]), rel=1e-15)
+    # a single-position window is that position's KL; an empty window has no mean
+    d_1, _ = P.profile_layer(m, st, t, 0, 1, P.PerturbParams(0.1, window_start=T - 1))
+    assert d_1 == kl_all[T - 1]
+    for ws in (T, T + 5):
+        with pytest.raises(ValueError, match="empty window"):
+            P.profile_layer(m, st, t, 0, 1, P.PerturbParams(0.1, window_start=ws))
+        with pytest.raises(ValueError, match="empty window"):
+            P.window_mean(kl_all, ws)
 
 
 def test_sensitivity_is_mean_of_sequence_means(small):
