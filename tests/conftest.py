@@ -11,3 +11,6 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: long-running CPU test")
+    # progress lines of long tests reach the terminal while the test runs
+    import gpu_helpers
+    gpu_helpers.set_capture_manager(config.pluginmanager.getplugin("capturemanager"))

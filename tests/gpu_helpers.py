@@ -12,9 +12,22 @@ import numpy as np
 import fixtures as F
 
 
+_CAPMAN = None
+
+
+def set_capture_manager(capman):
+    global _CAPMAN
+    _CAPMAN = capman
+
+
 def log(msg: str):
-    print(msg, flush=True)
-    sys.stdout.flush()
+    """Print a progress line; under pytest it bypasses output capture, so long
+    tests show where they are while they run."""
+    if _CAPMAN is not None:
+        with _CAPMAN.global_and_fixture_disabled():
+            print(msg, flush=True)
+    else:
+        print(msg, flush=True)
 
 
 def upload_weights(cfg, W: dict):
@@ -66,7 +79,10 @@ class Runner:
         self.model.profile_layer(batch, layer, alpha, cs, d, ws, kl_pos=kl, logits_out=lg, flags=flags, **kw)
         torch.cuda.synchronize()
         if lg is not None and logits_rows is not None:
-            lg = lg[:logits_rows]
+            if np.ndim(logits_rows) == 0:
+                lg = lg[:logits_rows]
+            else:                    # an index array: only those rows leave the GPU
+                lg = lg.index_select(0, torch.as_tensor(np.asarray(logits_rows, np.int64), device=lg.device))
         return (d.cpu().numpy().astype(np.float64), None if kl is None else kl.cpu().numpy().astype(np.float64),
                 None if lg is None else lg.cpu().numpy())
 

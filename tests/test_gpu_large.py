@@ -1,7 +1,7 @@
 """GPU parity on the Llama-3-8B- and Mistral-7B-shaped workloads at full size.
 
 Each workload runs through rk_sensitivity_profile at its real shape (all
-sequences, full lengths, every alpha) for the first and the last layer.  The
+sequences, full lengths, every alpha) for the first, a middle and the last layer.  The
 oracle cannot afford the full sequences, so it checks what it can compute
 exactly: the KL at every position of a 200-token prefix of sequence 0 (the model
 is causal, so a prefix computes the same per-position values) and the logits of
@@ -23,6 +23,11 @@ pytestmark = pytest.mark.gpu
 
 P = 200
 KL_REL, KL_ABS = 0.02, 1e-6
+# KL of single positions: the 2% bar is for the window mean d; one position carries
+# the unaveraged bf16 noise of its logit differences (up to 5% at the last layer
+# of the 32-layer models), so it is held to 10% or 1e-5, and the median position
+# to the per-layer 2%
+POS_REL, POS_ABS, POS_MEDIAN = 0.10, 1e-5, 0.02
 # Logits at 32 layers: bf16 rounding of the activations (GEMM operands, q/k/v,
 # P, attention output, SwiGLU output) is amplified through depth by this
 # random-init model, the same way the injected Value noise is (s_0 ~ 0.9 nats).
@@ -65,7 +70,7 @@ def test_large_workload(name, llama_weights):
     W = _weights_for(name, llama_weights)
     toks = F.make_tokens(w)
     L = cfg.n_layers
-    layers = [0, L - 1]
+    layers = [0, L // 2, L - 1]
     alphas = list(w.alphas)
     log(f"{name}: {len(toks)} sequences, {sum(len(t) for t in toks)} tokens")
     run = Runner(cfg, W)
@@ -99,8 +104,12 @@ def test_large_workload(name, llama_weights):
     for l in layers:
         _, kl_ref = OPR.profile_layer(m, st, t, 0, l, OPR.PerturbParams(a_max))
         g, r = got[l][0].mean(), kl_ref.mean()
-        log(f"{name} layer {l}: prefix-mean KL gpu {g:.6e} oracle {r:.6e} rel {abs(g - r) / r:.2e}")
+        e = np.abs(got[l][0] - kl_ref)
+        log(f"{name} layer {l}: prefix-mean KL gpu {g:.6e} oracle {r:.6e} rel {abs(g - r) / r:.2e}; "
+            f"per-position rel err max {(e / kl_ref).max():.2e}")
         assert abs(g - r) <= KL_REL * r or abs(g - r) <= KL_ABS
+        assert np.all((e <= POS_REL * kl_ref) | (e <= POS_ABS))
+        assert np.median(e / np.maximum(kl_ref, 1e-30)) <= POS_MEDIAN
         if got[l][1] is not None:
             xp = OPR.perturbed_final(m, st, t, 0, l, OPR.PerturbParams(a_max))
             ref_logits = OM.logits(m, xp)
