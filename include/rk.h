@@ -276,6 +276,29 @@ rk_status rk_sensitivity_profile(const rk_model *m, const rk_batch *calib, const
                                  float *s_out, float *d_out, void *workspace, size_t ws_bytes,
                                  void *stream);
 
+/* Allocation-free variant of rk_sensitivity_profile, for callers that cannot
+ * allocate device memory (code running under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Same arguments, results and errors
+ * as rk_sensitivity_profile, without the workspace: the buffers live in a
+ * device array of RK_STATIC_SCRATCH_BYTES bytes inside the library (one per
+ * GPU, held until the process ends).  It calls no allocator; the caller still
+ * owns calib, s_out and d_out.
+ *   - Calls whose workspace plan, rk_workspace_size(m, max_rows, max_group,
+ *     RK_WS_CLEAN_STATE | (p->flags & (RK_FLAG_UNFUSED_KL |
+ *     RK_FLAG_CACHED_WINDOW | RK_FLAG_LOCAL_SIGNAL))), exceeds
+ *     RK_STATIC_SCRATCH_BYTES return RK_ERR_WORKSPACE before any device work.
+ *   - RK_FLAG_GRAPH is refused (RK_ERR_ARG): recording a graph allocates.
+ *   - Every call on one GPU uses that GPU's single array, so calls that
+ *     overlap on one GPU (other streams, other threads) race: order them.
+ *     Nothing is assumed about the array's previous contents.
+ *   - stream, if not NULL, must belong to the current device (RK_ERR_HIP).
+ *   - Its launches are not recorded by rk_timing_begin sessions.              */
+#define RK_STATIC_SCRATCH_BYTES ((size_t)128 << 20)
+rk_status rk_sensitivity_profile_static(const rk_model *m, const rk_batch *calib, const int32_t *layers,
+                                        int32_t n_A, const float *alphas, int32_t n_alpha,
+                                        const rk_perturb_params *p, int64_t max_rows, int32_t max_group,
+                                        float *s_out, float *d_out, void *stream);
+
 /* Eq. value-perturbation on its own: v (DEVICE, model dtype) holds the Values of
  * one layer for a batch, row r at v + r * row_stride elements, n_kv_heads *
  * head_dim contiguous values per row; they are replaced in place by

@@ -27,7 +27,7 @@ import numpy as np
 
 __all__ = ["RKError", "load", "Model", "Batch", "layer_budgets", "timing_begin", "timing_end", "LIB_PATH", "RK_FLAG_FULL_RECOMPUTE",
            "RK_FLAG_UNFUSED_KL", "RK_FLAG_CACHED_WINDOW", "RK_FLAG_GRAPH", "RK_FLAG_LOCAL_SIGNAL", "RK_FLAG_CHECK_STATE", "RK_WS_CLEAN_STATE", "RK_MAX_BATCH_SEQS", "RK_MAX_GROUP",
-           "RK_POOL_MAX", "RK_POOL_AVG", "RK_SNAPKV_MAX_PREFIX", "snapkv_layout", "spearman"]
+           "RK_POOL_MAX", "RK_POOL_AVG", "RK_SNAPKV_MAX_PREFIX", "RK_STATIC_SCRATCH_BYTES", "snapkv_layout", "spearman"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librk.so")
 
@@ -46,6 +46,7 @@ RK_MAX_GROUP = 16
 RK_POOL_MAX = 0
 RK_POOL_AVG = 1
 RK_SNAPKV_MAX_PREFIX = 36864
+RK_STATIC_SCRATCH_BYTES = 128 << 20
 
 _STATUS = {0: "RK_OK", -1: "RK_ERR_ARG", -2: "RK_ERR_SHAPE", -3: "RK_ERR_WORKSPACE", -4: "RK_ERR_HIP",
            -5: "RK_ERR_UNSUPPORTED", -6: "RK_ERR_STATE"}
@@ -113,6 +114,9 @@ def load() -> ctypes.CDLL:
                                   vp, sz, vp]),
         "rk_sensitivity_profile": (st, [vp, ctypes.POINTER(_Batch), ctypes.POINTER(i32), i32, ctypes.POINTER(f32),
                                         i32, ctypes.POINTER(_Params), i64, i32, vp, vp, vp, sz, vp]),
+        "rk_sensitivity_profile_static": (st, [vp, ctypes.POINTER(_Batch), ctypes.POINTER(i32), i32,
+                                               ctypes.POINTER(f32), i32, ctypes.POINTER(_Params), i64, i32, vp, vp,
+                                               vp]),
         "rk_perturb_values": (st, [vp, ctypes.POINTER(_Batch), i32, f32, ctypes.POINTER(_Params), vp, i64, vp]),
         "rk_layer_budgets": (st, [ctypes.POINTER(f64), i32, i64, f64, f64, f64, ctypes.c_int, ctypes.POINTER(f64),
                                   ctypes.POINTER(i64)]),
@@ -262,6 +266,19 @@ class Model:
                                              ctypes.byref(p), int(max_rows), int(max_group), _ptr(s_out),
                                              _ptr(d_out), _ptr(workspace),
                                              workspace.numel() * workspace.element_size(), _stream(stream)))
+
+    def sensitivity_profile_static(self, calib: Batch, layers: Sequence[int], alphas: Sequence[float], s_out,
+                                   max_rows: int, max_group: int = 1, d_out=None, seed: int = 2,
+                                   window_start: int = 0, protect_head: int = 0, protect_tail: int = 0,
+                                   flags: int = 0, stream=None):
+        """sensitivity_profile without a workspace (the library's device-resident
+        scratch of RK_STATIC_SCRATCH_BYTES bytes; allocates nothing)."""
+        lay = (ctypes.c_int32 * len(layers))(*[int(x) for x in layers])
+        alp = (ctypes.c_float * len(alphas))(*[float(x) for x in alphas])
+        p = _params(seed, window_start, protect_head, protect_tail, flags)
+        _check(load().rk_sensitivity_profile_static(self._h, ctypes.byref(calib._c), lay, len(layers), alp,
+                                                    len(alphas), ctypes.byref(p), int(max_rows), int(max_group),
+                                                    _ptr(s_out), _ptr(d_out), _stream(stream)))
 
     def compression_damage(self, batch: Batch, window_start: int, layer: int, positions, n_keep: int, state, d_out,
                            workspace, seq_stride=None, kl_pos=None, stream=None):

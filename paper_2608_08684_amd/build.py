@@ -20,7 +20,8 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "librk.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["api.cpp", "budgets.cpp", "elementwise.hip", "gemm.hip", "attention.hip", "lm_kl.hip", "snapkv.hip"]
+SOURCES = ["api.cpp", "budgets.cpp", "elementwise.hip", "gemm.hip", "attention.hip", "lm_kl.hip", "snapkv.hip",
+           "scratch.hip"]
 ARCH = "gfx950"
 # Per-file code-generation options.  Attention keeps its MFMA accumulators in
 # ordinary VGPRs: its softmax reads and rescales them every tile, and the AGPR

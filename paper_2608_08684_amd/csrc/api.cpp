@@ -1090,6 +1090,151 @@ static rk_status run_graphed(std::vector<uint64_t> key, F&& run, hipStream_t s) 
   return RK_OK;
 }
 
+// Argument checks of the whole-profile entry points (everything but the
+// workspace); on success *wp is the workspace plan for max_rows and max_group.
+static rk_status check_profile(const rk_model* m, const rk_batch* calib, const int32_t* layers, int32_t n_A,
+                               const float* alphas, int32_t n_alpha, const rk_perturb_params* p, int64_t max_rows,
+                               int32_t max_group, const float* s_out, WsPlan* wp) {
+  if (!m || !calib || !calib->tokens || !calib->offsets) { set_error("null model or calibration set"); return RK_ERR_ARG; }
+  rk_status e = check_params(p);
+  if (e != RK_OK) return e;
+  if (calib->n_seqs < 1 || calib->seq_index0 < 0) { set_error("n_seqs must be >= 1, seq_index0 >= 0"); return RK_ERR_ARG; }
+  if (calib->offsets[0] != 0) { set_error("offsets[0] must be 0"); return RK_ERR_SHAPE; }
+  if (!layers || n_A < 1 || !alphas || n_alpha < 1 || !s_out) {
+    set_error("null layers/alphas/s_out or empty layer/alpha set");
+    return RK_ERR_ARG;
+  }
+  if ((int64_t)n_A * n_alpha > kMaxSAcc) { set_error("n_A * n_alpha must be <= %d", kMaxSAcc); return RK_ERR_ARG; }
+  for (int j = 0; j < n_A; ++j)
+    if (layers[j] < 0 || layers[j] >= m->cfg.n_layers) { set_error("layer %d out of range", layers[j]); return RK_ERR_ARG; }
+  for (int a = 0; a < n_alpha; ++a)
+    if (!(alphas[a] >= 0.0f) || !isfinite(alphas[a])) { set_error("alphas must be finite and >= 0"); return RK_ERR_ARG; }
+  if (max_group < 1 || max_group > RK_MAX_GROUP) { set_error("max_group must be in [1, %d]", RK_MAX_GROUP); return RK_ERR_ARG; }
+  if (max_rows < 1 || max_rows > kMaxRows) { set_error("max_rows must be in [1, 2^31 - 1]"); return RK_ERR_ARG; }
+  const int N = calib->n_seqs;
+  for (int i = 0; i < N; ++i) {
+    const int64_t len = calib->offsets[i + 1] - calib->offsets[i];
+    if (len < 0) { set_error("offsets must be non-decreasing"); return RK_ERR_SHAPE; }
+    if (len > max_rows) { set_error("sequence %d (%lld tokens) exceeds max_rows", i, (long long)len); return RK_ERR_SHAPE; }
+    if (len == 0) { set_error("sequence %d is empty", i); return RK_ERR_SHAPE; }
+    if (len <= p->window_start) {
+      set_error("sequence %d (%lld tokens) has an empty window: window_start %d", i, (long long)len, p->window_start);
+      return RK_ERR_SHAPE;
+    }
+    if ((p->flags & RK_FLAG_CACHED_WINDOW) && (p->window_start < 1 || len <= p->window_start)) {
+      set_error("sequence %d (%lld tokens) needs a non-empty prefix and window around window_start %d", i,
+                (long long)len, p->window_start);
+      return RK_ERR_SHAPE;
+    }
+  }
+  const bool local = (p->flags & RK_FLAG_LOCAL_SIGNAL) != 0;
+  const bool unfused = !local && (!m->bf16 || (p->flags & RK_FLAG_UNFUSED_KL));
+  const bool cw = (p->flags & RK_FLAG_CACHED_WINDOW) != 0;
+  if (cw && (e = check_window_model(m)) != RK_OK) return e;
+  const uint32_t wflags = RK_WS_CLEAN_STATE | (unfused ? RK_FLAG_UNFUSED_KL : 0) | (cw ? RK_FLAG_CACHED_WINDOW : 0) |
+                          (local ? RK_FLAG_LOCAL_SIGNAL : 0);
+  *wp = ws_plan(m, max_rows, max_group, wflags);
+  return RK_OK;
+}
+
+// The profile of a calibration set (Algorithm 1, profiling half) on a checked
+// argument set, with the buffers of plan wp carved from workspace.
+static rk_status profile_run(const rk_model* m, const rk_batch* calib, const int32_t* layers, int32_t n_A,
+                             const float* alphas, int32_t n_alpha, const rk_perturb_params* p, int64_t max_rows,
+                             int32_t max_group, float* s_out, float* d_out, const WsPlan& wp, void* workspace,
+                             hipStream_t s) {
+  rk_status e = RK_OK;
+  const int N = calib->n_seqs;
+  const bool local = (p->flags & RK_FLAG_LOCAL_SIGNAL) != 0;
+  const bool unfused = !local && (!m->bf16 || (p->flags & RK_FLAG_UNFUSED_KL));
+  const bool cw = (p->flags & RK_FLAG_CACHED_WINDOW) != 0;
+  // Buffers are carved for max_rows; each batch uses the leading rows of each.
+  const Bufs b = carve(wp, workspace);
+  RK_TRY(launch_zero_f64(b.sacc, n_A * n_alpha, s));
+  const int n_pass = n_A * n_alpha;
+  int first = 0;
+  while (first < N) {
+    int count = 0;
+    int64_t rows = 0;
+    while (first + count < N && count < RK_MAX_BATCH_SEQS) {
+      const int64_t len = calib->offsets[first + count + 1] - calib->offsets[first + count];
+      if (count > 0 && rows + len > max_rows) break;
+      rows += len;
+      ++count;
+    }
+    SeqTable st;
+    if ((e = make_table(calib, first, count, &st)) != RK_OK) return e;
+    const int32_t* tokens = calib->tokens + calib->offsets[first];
+    const int64_t R = st.rows;
+    if (cw) {
+      // cached-window mode: the same grouping over the window rows of the batch
+      SeqTable pst, wst;
+      if ((e = window_tables(st, p->window_start, &pst, &wst)) != RK_OK) return e;
+      const Win wn = win_view(m, R, b.clean);
+      if ((e = window_reference(m, tokens, st, pst, wst, wn, b, s, local ? b.hloc : nullptr, !local)) != RK_OK)
+        return e;
+      if (unfused && (e = clean_logits(m, wst, wn.w, b.logits_c, s)) != RK_OK) return e;
+      const int64_t Rw = wst.rows;
+      for (int g0 = 0; g0 < n_pass; g0 += max_group) {
+        const int G = (n_pass - g0 < max_group) ? n_pass - g0 : max_group;
+        PassMap pm{};
+        pm.G = G;
+        pm.seq_index0 = first;
+        pm.d_seq_stride = n_A;
+        int glay[RK_MAX_GROUP];
+        float galpha[RK_MAX_GROUP];
+        for (int k = 0; k < G; ++k) {
+          const int idx = g0 + k, a = idx / n_A, j = idx % n_A;
+          glay[k] = layers[j];
+          galpha[k] = alphas[a];
+          if (local &&
+              (e = window_local_pass(m, pst, wst, wn, layers[j], alphas[a], p, b.hloc, b.kl + (size_t)k * Rw, b,
+                                     s)) != RK_OK)
+            return e;
+          pm.d_base[k] = (int64_t)a * N * n_A + j;
+          pm.s_index[k] = a * n_A + j;
+        }
+        if (!local && (e = window_group_final(m, pst, wst, wn, G, glay, galpha, p, max_rows, b.xp, b, s)) != RK_OK)
+          return e;
+        if (!local && (e = score_group(m, wst, wn.w, b.xp, G, unfused, b.logits_p, b.kl, b, s)) != RK_OK) return e;
+        RK_TRY(launch_window_mean(b.kl, Rw, G, wst, 0, b.dbatch, s));
+        RK_TRY(launch_accumulate(b.dbatch, st.n, pm, d_out, b.sacc, s));
+      }
+      first += count;
+      continue;
+    }
+    const Clean cl = clean_view(m, R, b.clean);
+    if ((e = reference_forward(m, tokens, st, cl, b, s, local ? b.hloc : nullptr, !local)) != RK_OK) return e;
+    if (unfused && (e = clean_logits(m, st, cl, b.logits_c, s)) != RK_OK) return e;
+    for (int g0 = 0; g0 < n_pass; g0 += max_group) {
+      const int G = (n_pass - g0 < max_group) ? n_pass - g0 : max_group;
+      PassMap pm{};
+      pm.G = G;
+      pm.seq_index0 = first;
+      pm.d_seq_stride = n_A;
+      for (int k = 0; k < G; ++k) {
+        const int idx = g0 + k, a = idx / n_A, j = idx % n_A;
+        if (local) {
+          if ((e = local_pass(m, tokens, st, cl, layers[j], alphas[a], p, b.hloc, b.kl + (size_t)k * R, b, s)) !=
+              RK_OK)
+            return e;
+        } else {
+          void* xf = (char*)b.xp + (size_t)k * pad_rows(R) * m->cfg.d_model * act_bytes(m);
+          if ((e = perturbed_final(m, tokens, st, cl, layers[j], alphas[a], p, xf, b, s)) != RK_OK) return e;
+        }
+        pm.d_base[k] = (int64_t)a * N * n_A + j;
+        pm.s_index[k] = a * n_A + j;
+      }
+      if (!local && (e = score_group(m, st, cl, b.xp, G, unfused, b.logits_p, b.kl, b, s)) != RK_OK) return e;
+      RK_TRY(launch_window_mean(b.kl, R, G, st, p->window_start, b.dbatch, s));
+      RK_TRY(launch_accumulate(b.dbatch, st.n, pm, d_out, b.sacc, s));
+    }
+    first += count;
+  }
+  RK_TRY(launch_finalize(b.sacc, n_pass, 1.0 / (double)N, s_out, s));
+  return RK_OK;
+}
+
 // Forget the recorded sequence when its model goes away: a new model at the
 // same address must never replay launches baked for the old one.
 static void drop_graph(const rk_model* m) {
@@ -1632,133 +1777,14 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
                                  const float* alphas, int32_t n_alpha, const rk_perturb_params* p, int64_t max_rows,
                                  int32_t max_group, float* s_out, float* d_out, void* workspace, size_t ws_bytes,
                                  void* stream) {
-  if (!m || !calib || !calib->tokens || !calib->offsets) { set_error("null model or calibration set"); return RK_ERR_ARG; }
-  rk_status e = check_params(p);
+  WsPlan wp;
+  rk_status e = check_profile(m, calib, layers, n_A, alphas, n_alpha, p, max_rows, max_group, s_out, &wp);
   if (e != RK_OK) return e;
-  if (calib->n_seqs < 1 || calib->seq_index0 < 0) { set_error("n_seqs must be >= 1, seq_index0 >= 0"); return RK_ERR_ARG; }
-  if (calib->offsets[0] != 0) { set_error("offsets[0] must be 0"); return RK_ERR_SHAPE; }
-  if (!layers || n_A < 1 || !alphas || n_alpha < 1 || !s_out || !workspace) {
-    set_error("null layers/alphas/s_out/workspace or empty layer/alpha set");
-    return RK_ERR_ARG;
-  }
-  if ((int64_t)n_A * n_alpha > kMaxSAcc) { set_error("n_A * n_alpha must be <= %d", kMaxSAcc); return RK_ERR_ARG; }
-  for (int j = 0; j < n_A; ++j)
-    if (layers[j] < 0 || layers[j] >= m->cfg.n_layers) { set_error("layer %d out of range", layers[j]); return RK_ERR_ARG; }
-  for (int a = 0; a < n_alpha; ++a)
-    if (!(alphas[a] >= 0.0f) || !isfinite(alphas[a])) { set_error("alphas must be finite and >= 0"); return RK_ERR_ARG; }
-  if (max_group < 1 || max_group > RK_MAX_GROUP) { set_error("max_group must be in [1, %d]", RK_MAX_GROUP); return RK_ERR_ARG; }
-  if (max_rows < 1 || max_rows > kMaxRows) { set_error("max_rows must be in [1, 2^31 - 1]"); return RK_ERR_ARG; }
-  const int N = calib->n_seqs;
-  for (int i = 0; i < N; ++i) {
-    const int64_t len = calib->offsets[i + 1] - calib->offsets[i];
-    if (len < 0) { set_error("offsets must be non-decreasing"); return RK_ERR_SHAPE; }
-    if (len > max_rows) { set_error("sequence %d (%lld tokens) exceeds max_rows", i, (long long)len); return RK_ERR_SHAPE; }
-    if (len == 0) { set_error("sequence %d is empty", i); return RK_ERR_SHAPE; }
-    if (len <= p->window_start) {
-      set_error("sequence %d (%lld tokens) has an empty window: window_start %d", i, (long long)len, p->window_start);
-      return RK_ERR_SHAPE;
-    }
-    if ((p->flags & RK_FLAG_CACHED_WINDOW) && (p->window_start < 1 || len <= p->window_start)) {
-      set_error("sequence %d (%lld tokens) needs a non-empty prefix and window around window_start %d", i,
-                (long long)len, p->window_start);
-      return RK_ERR_SHAPE;
-    }
-  }
-  const bool local = (p->flags & RK_FLAG_LOCAL_SIGNAL) != 0;
-  const bool unfused = !local && (!m->bf16 || (p->flags & RK_FLAG_UNFUSED_KL));
-  const bool cw = (p->flags & RK_FLAG_CACHED_WINDOW) != 0;
-  if (cw && (e = check_window_model(m)) != RK_OK) return e;
-  const uint32_t wflags = RK_WS_CLEAN_STATE | (unfused ? RK_FLAG_UNFUSED_KL : 0) | (cw ? RK_FLAG_CACHED_WINDOW : 0) |
-                          (local ? RK_FLAG_LOCAL_SIGNAL : 0);
-  const WsPlan wp = ws_plan(m, max_rows, max_group, wflags);
+  if (!workspace) { set_error("null workspace"); return RK_ERR_ARG; }
   if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
-
-  // Buffers are carved for max_rows; each batch uses the leading rows of each.
-  const Bufs b = carve(wp, workspace);
+  const int N = calib->n_seqs;
   auto run = [&](hipStream_t s) -> rk_status {
-  RK_TRY(launch_zero_f64(b.sacc, n_A * n_alpha, s));
-  const int n_pass = n_A * n_alpha;
-  int first = 0;
-  while (first < N) {
-    int count = 0;
-    int64_t rows = 0;
-    while (first + count < N && count < RK_MAX_BATCH_SEQS) {
-      const int64_t len = calib->offsets[first + count + 1] - calib->offsets[first + count];
-      if (count > 0 && rows + len > max_rows) break;
-      rows += len;
-      ++count;
-    }
-    SeqTable st;
-    if ((e = make_table(calib, first, count, &st)) != RK_OK) return e;
-    const int32_t* tokens = calib->tokens + calib->offsets[first];
-    const int64_t R = st.rows;
-    if (cw) {
-      // cached-window mode: the same grouping over the window rows of the batch
-      SeqTable pst, wst;
-      if ((e = window_tables(st, p->window_start, &pst, &wst)) != RK_OK) return e;
-      const Win wn = win_view(m, R, b.clean);
-      if ((e = window_reference(m, tokens, st, pst, wst, wn, b, s, local ? b.hloc : nullptr, !local)) != RK_OK)
-        return e;
-      if (unfused && (e = clean_logits(m, wst, wn.w, b.logits_c, s)) != RK_OK) return e;
-      const int64_t Rw = wst.rows;
-      for (int g0 = 0; g0 < n_pass; g0 += max_group) {
-        const int G = (n_pass - g0 < max_group) ? n_pass - g0 : max_group;
-        PassMap pm{};
-        pm.G = G;
-        pm.seq_index0 = first;
-        pm.d_seq_stride = n_A;
-        int glay[RK_MAX_GROUP];
-        float galpha[RK_MAX_GROUP];
-        for (int k = 0; k < G; ++k) {
-          const int idx = g0 + k, a = idx / n_A, j = idx % n_A;
-          glay[k] = layers[j];
-          galpha[k] = alphas[a];
-          if (local &&
-              (e = window_local_pass(m, pst, wst, wn, layers[j], alphas[a], p, b.hloc, b.kl + (size_t)k * Rw, b,
-                                     s)) != RK_OK)
-            return e;
-          pm.d_base[k] = (int64_t)a * N * n_A + j;
-          pm.s_index[k] = a * n_A + j;
-        }
-        if (!local && (e = window_group_final(m, pst, wst, wn, G, glay, galpha, p, max_rows, b.xp, b, s)) != RK_OK)
-          return e;
-        if (!local && (e = score_group(m, wst, wn.w, b.xp, G, unfused, b.logits_p, b.kl, b, s)) != RK_OK) return e;
-        RK_TRY(launch_window_mean(b.kl, Rw, G, wst, 0, b.dbatch, s));
-        RK_TRY(launch_accumulate(b.dbatch, st.n, pm, d_out, b.sacc, s));
-      }
-      first += count;
-      continue;
-    }
-    const Clean cl = clean_view(m, R, b.clean);
-    if ((e = reference_forward(m, tokens, st, cl, b, s, local ? b.hloc : nullptr, !local)) != RK_OK) return e;
-    if (unfused && (e = clean_logits(m, st, cl, b.logits_c, s)) != RK_OK) return e;
-    for (int g0 = 0; g0 < n_pass; g0 += max_group) {
-      const int G = (n_pass - g0 < max_group) ? n_pass - g0 : max_group;
-      PassMap pm{};
-      pm.G = G;
-      pm.seq_index0 = first;
-      pm.d_seq_stride = n_A;
-      for (int k = 0; k < G; ++k) {
-        const int idx = g0 + k, a = idx / n_A, j = idx % n_A;
-        if (local) {
-          if ((e = local_pass(m, tokens, st, cl, layers[j], alphas[a], p, b.hloc, b.kl + (size_t)k * R, b, s)) !=
-              RK_OK)
-            return e;
-        } else {
-          void* xf = (char*)b.xp + (size_t)k * pad_rows(R) * m->cfg.d_model * act_bytes(m);
-          if ((e = perturbed_final(m, tokens, st, cl, layers[j], alphas[a], p, xf, b, s)) != RK_OK) return e;
-        }
-        pm.d_base[k] = (int64_t)a * N * n_A + j;
-        pm.s_index[k] = a * n_A + j;
-      }
-      if (!local && (e = score_group(m, st, cl, b.xp, G, unfused, b.logits_p, b.kl, b, s)) != RK_OK) return e;
-      RK_TRY(launch_window_mean(b.kl, R, G, st, p->window_start, b.dbatch, s));
-      RK_TRY(launch_accumulate(b.dbatch, st.n, pm, d_out, b.sacc, s));
-    }
-    first += count;
-  }
-  RK_TRY(launch_finalize(b.sacc, n_pass, 1.0 / (double)N, s_out, s));
-  return RK_OK;
+    return profile_run(m, calib, layers, n_A, alphas, n_alpha, p, max_rows, max_group, s_out, d_out, wp, workspace, s);
   };
   if (!(p->flags & RK_FLAG_GRAPH)) return run((hipStream_t)stream);
   // the key: everything the launch sequence bakes in
@@ -1783,6 +1809,39 @@ rk_status rk_sensitivity_profile(const rk_model* m, const rk_batch* calib, const
   put((uint64_t)(uintptr_t)s_out); put((uint64_t)(uintptr_t)d_out); put((uint64_t)(uintptr_t)workspace);
   put((uint64_t)ws_bytes);
   return run_graphed(key, run, (hipStream_t)stream);
+}
+
+rk_status rk_sensitivity_profile_static(const rk_model* m, const rk_batch* calib, const int32_t* layers,
+                                        int32_t n_A, const float* alphas, int32_t n_alpha,
+                                        const rk_perturb_params* p, int64_t max_rows, int32_t max_group,
+                                        float* s_out, float* d_out, void* stream) {
+  if (p && (p->flags & RK_FLAG_GRAPH)) {
+    set_error("RK_FLAG_GRAPH is not available here: recording a graph allocates");
+    return RK_ERR_ARG;
+  }
+  WsPlan wp;
+  rk_status e = check_profile(m, calib, layers, n_A, alphas, n_alpha, p, max_rows, max_group, s_out, &wp);
+  if (e != RK_OK) return e;
+  if (wp.total > (size_t)RK_STATIC_SCRATCH_BYTES) {
+    set_error("this profile needs %zu bytes of scratch (max_rows %lld, max_group %d); the allocation-free entry "
+              "point holds %zu: use rk_sensitivity_profile with a workspace", wp.total, (long long)max_rows,
+              max_group, (size_t)RK_STATIC_SCRATCH_BYTES);
+    return RK_ERR_WORKSPACE;
+  }
+  void* scratch = nullptr;
+  hipError_t he = static_scratch((hipStream_t)stream, &scratch);
+  if (he != hipSuccess) {
+    set_error("scratch address of this device: %s", hipGetErrorString(he));
+    return RK_ERR_HIP;
+  }
+  // a timing session would create its events on first use; this entry point's launches are not timed
+  struct Untimed {
+    bool was = g_timing.on;
+    Untimed() { g_timing.on = false; }
+    ~Untimed() { g_timing.on = was; }
+  } untimed;
+  return profile_run(m, calib, layers, n_A, alphas, n_alpha, p, max_rows, max_group, s_out, d_out, wp, scratch,
+                     (hipStream_t)stream);
 }
 
 rk_status rk_perturb_values(const rk_model* m, const rk_batch* batch, int32_t layer, float alpha,

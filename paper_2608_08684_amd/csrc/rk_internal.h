@@ -60,6 +60,11 @@ template <> struct Act<bf16_t> {
 };
 #endif
 
+// Device address of this device's RK_STATIC_SCRATCH_BYTES-byte scratch array
+// (looked up once per device).  A non-null stream must belong to the current
+// device (hipErrorInvalidDevice otherwise).
+hipError_t static_scratch(hipStream_t stream, void** out);
+
 // --------------------------------------------------------------------------- launchers
 // Each returns hipSuccess or the launch error.  `act_bf16` selects the element type
 // of activation buffers (bf16 when true, fp32 otherwise).

@@ -192,6 +192,17 @@ def test_profile_entry_points_validate_before_launching():
                                       None, fake, big, None) == rk.RK_ERR_ARG        # group too large
     assert lib.rk_sensitivity_profile(h, ctypes.byref(batch), lay, 2, alp, 1, ctypes.byref(p), 1000, 4, s_out,
                                       None, fake, 16, None) == rk.RK_ERR_WORKSPACE
+    # the allocation-free variant: the same argument checks, a plan beyond its scratch
+    # and graph recording are refused before any device work
+    st_ = lib.rk_sensitivity_profile_static
+    assert st_(h, ctypes.byref(batch), lay_bad, 2, alp, 1, ctypes.byref(p), 1000, 1, s_out, None, None) == rk.RK_ERR_ARG
+    assert st_(h, ctypes.byref(batch), lay, 2, alp, 1, ctypes.byref(p), 100, 1, s_out, None, None) == rk.RK_ERR_SHAPE
+    assert lib.rk_workspace_size(h, 1 << 20, 16, rk.RK_WS_CLEAN_STATE) > rk.RK_STATIC_SCRATCH_BYTES
+    assert st_(h, ctypes.byref(batch), lay, 2, alp, 1, ctypes.byref(p), 1 << 20, 16, s_out, None,
+               None) == rk.RK_ERR_WORKSPACE
+    assert b"rk_sensitivity_profile with a workspace" in lib.rk_last_error()
+    pg = rk._Params(2, 0, 0, 0, rk.RK_FLAG_GRAPH)
+    assert st_(h, ctypes.byref(batch), lay, 2, alp, 1, ctypes.byref(pg), 1000, 1, s_out, None, None) == rk.RK_ERR_ARG
     # perturb_values: row stride too small
     assert lib.rk_perturb_values(h, ctypes.byref(batch), 0, 0.1, ctypes.byref(p), fake, 10, None) == rk.RK_ERR_SHAPE
     # ... not a multiple of 4, or a misaligned buffer (four values per vector access)
