@@ -8,10 +8,10 @@
 //   * the queries arrive pre-multiplied by log2(e) / sqrt(d_h) (the q|k|v
 //     projection's epilogue does it before rounding), so a score is already
 //     the exponent of 2;
-//   * one workgroup = 4 waves x 32 queries of one head; it runs a pair of
-//     128-query blocks (nqb - 1 - x, then x) so all pairs of a sequence cost the
-//     same, longest sequences first (one block per workgroup when the rows sit
-//     behind a cached prefix, which every block reads in full);
+//   * one workgroup = 4 waves (d_h 64) or 8 waves (d_h 128) x 32 queries of one
+//     head; it runs a pair of query blocks (nqb - 1 - x, then x) so all pairs of
+//     a sequence cost the same, longest sequences first (one block per workgroup
+//     when the rows sit behind a cached prefix, which every block reads in full);
 //   * 64-key tiles of K and V go global -> LDS by buffer_load ... lds (no
 //     staging registers; rows past the sequence read as zero) through a
 //     ring of 2-3 stages;
@@ -19,7 +19,8 @@
 //     -m (the running max), so each lane owns one query column and exp2 is
 //     applied to the MFMA result directly; m is raised lazily (only when a
 //     tile's max exceeds it by 2^8), with one exchange with the partner
-//     half-wave;
+//     half-wave (v_permlane32_swap); the two 32-key halves of a tile run as two
+//     interleaved accumulator chains;
 //   * O^T = V^T P^T: P^T is the lane's own S^T registers rounded to bf16, and
 //     the V^T operand comes from the row-major V tile through ds_read_b64_tr_b16
 //     in the same key order; the softmax denominator is summed from the rounded
@@ -78,24 +79,40 @@ __device__ __forceinline__ int k_swz(int row) { return DH == 128 ? (row & 15) : 
 template <int DH>
 __device__ __forceinline__ int v_swz(int row) { return DH == 128 ? ((row & 3) << 2) : (((row >> 1) & 1) << 2); }
 
-// K/V tile ring depth: three stages (prefetch two tiles ahead) where the LDS
-// allows three workgroups per CU, two for d_h = 128.
+// max / sum of a lane's value and that of lane l ^ 32 (the other half-wave):
+// v_permlane32_swap with both operands x hands lanes 0-31 the upper half's x and
+// lanes 32-63 the lower half's, each keeping its own in the other result.
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Workgroup shape per head size.  d_h = 64: 4 waves (128 queries), a three-stage
+// K/V ring (prefetch two tiles ahead), three workgroups per CU.  d_h = 128: 8 waves
+// (256 queries) share one two-stage ring, one workgroup per CU (two waves per SIMD
+// either way; the wider group halves the copies per query).
 template <int DH>
 struct AttnTraits {
+  static constexpr int kWaves = DH == 64 ? 4 : 8;
   static constexpr int kStages = DH == 64 ? 3 : 2;
-  static constexpr int kMinBlocks = DH == 64 ? 3 : 2;
+  static constexpr int kMinBlocks = DH == 64 ? 3 : 1;
 };
 
 template <int DH, bool PREFIX>
-__global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_kernel(const bf16_t* __restrict__ qkv, int64_t ldq,
+__global__ __launch_bounds__(64 * AttnTraits<DH>::kWaves, AttnTraits<DH>::kMinBlocks) void attn_bf16_kernel(const bf16_t* __restrict__ qkv, int64_t ldq,
                                                         bf16_t* __restrict__ out, int64_t ldo, SeqTable st,
                                                         AttnWork wk, int H, int Hkv, int n_items, KvPrefix pk) {
-  constexpr int BQ = 128, BKV = 64;
+  constexpr int NW = AttnTraits<DH>::kWaves;
+  constexpr int BQ = 32 * NW, BKV = 64;
   constexpr int CH = DH / 8;                // 16-byte chunks per row
   constexpr int NKS = DH / 16;              // k-steps of S^T
   constexpr int NDB = DH / 32;              // 32-row blocks of O^T
   constexpr int SLOTS = BKV * CH;           // 16-byte slots per tile
-  constexpr int NLD = SLOTS / 256;          // DMA instructions per thread, per tile and matrix
+  constexpr int NLD = SLOTS / (64 * NW);    // DMA instructions per thread, per tile and matrix
   constexpr int ROWB = DH * 2;              // bytes per tile row
   constexpr int S = AttnTraits<DH>::kStages;
   __shared__ __attribute__((aligned(16))) v4u Ks[S][SLOTS];
@@ -141,7 +158,7 @@ __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_ker
   uint32_t koff[NLD], voff[NLD];
 #pragma unroll
   for (int i = 0; i < NLD; ++i) {
-    const int slot = (i * 4 + w) * 64 + lane, r = slot / CH, ph = slot % CH;
+    const int slot = (i * NW + w) * 64 + lane, r = slot / CH, ph = slot % CH;
     koff[i] = (uint32_t)(r * ldq * 2 + (kcol + (ph ^ k_swz<DH>(r)) * 8) * 2);
     voff[i] = (uint32_t)(r * ldq * 2 + (vcol + (ph ^ v_swz<DH>(r)) * 8) * 2);
   }
@@ -160,7 +177,7 @@ __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_ker
     rv_p = make_rsrc(vb + (int64_t)ps * P * ldv_p, (int64_t)P * ldv_p * 2);
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
-      const int slot = (i * 4 + w) * 64 + lane, r = slot / CH, ph = slot % CH;
+      const int slot = (i * NW + w) * 64 + lane, r = slot / CH, ph = slot % CH;
       koff_p[i] = (uint32_t)(r * pk.ldk * 2 + (hk * DH + (ph ^ k_swz<DH>(r)) * 8) * 2);
       voff_p[i] = (uint32_t)(r * ldv_p * 2 + (hk * DH + (ph ^ v_swz<DH>(r)) * 8) * 2);
     }
@@ -175,7 +192,7 @@ __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_ker
       const int sv = __builtin_amdgcn_readfirstlane(t * BKV * (int)ldv_p * 2);
 #pragma unroll
       for (int i = 0; i < NLD; ++i) {
-        const uint32_t o = (uint32_t)((b * SLOTS + (i * 4 + w) * 64) * 16);
+        const uint32_t o = (uint32_t)((b * SLOTS + (i * NW + w) * 64) * 16);
         dma16(rk_p, __builtin_amdgcn_readfirstlane(ks_lds + o), koff_p[i], sk);
         dma16(rv_p, __builtin_amdgcn_readfirstlane(vs_lds + o), voff_p[i], sv);
       }
@@ -183,7 +200,7 @@ __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_ker
       const int so = __builtin_amdgcn_readfirstlane((t - n_pre) * BKV * (int)ldq * 2);
 #pragma unroll
       for (int i = 0; i < NLD; ++i) {
-        const uint32_t o = (uint32_t)((b * SLOTS + (i * 4 + w) * 64) * 16);
+        const uint32_t o = (uint32_t)((b * SLOTS + (i * NW + w) * 64) * 16);
         dma16(rsrc, __builtin_amdgcn_readfirstlane(ks_lds + o), koff[i], so);
         dma16(rsrc, __builtin_amdgcn_readfirstlane(vs_lds + o), voff[i], so);
       }
@@ -248,17 +265,14 @@ __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_ker
       if (t + S - 1 < n_tiles) issue(t + S - 1, nbuf);
       if (pre || k0 <= wave_qmax) {
         const char* kt = reinterpret_cast<const char*>(Ks[buf]);
-        f32x16_t s[2];
+        f32x16_t s[2] = {negm, negm};
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
-          bf16x8_t a[NKS];
+        for (int ks = 0; ks < NKS; ++ks)
 #pragma unroll
-          for (int ks = 0; ks < NKS; ++ks)
-            a[ks] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const v4u*>(kt + rb * 32 * ROWB + kfo[ks]));
-          s[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], qf[0], negm, 0, 0, 0);
-#pragma unroll
-          for (int ks = 1; ks < NKS; ++ks) s[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks], qf[ks], s[rb], 0, 0, 0);
-        }
+          for (int rb = 0; rb < 2; ++rb) {
+            const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const v4u*>(kt + rb * 32 * ROWB + kfo[ks]));
+            s[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s[rb], 0, 0, 0);
+          }
         // masks only where a key can exceed the query or the segment (wave-uniform test);
         // every cached prefix key precedes every query of the sequence's own rows
         if (pre ? (k0 + BKV > P) : (k0 + BKV - 1 > wave_qmin || k0 + BKV > T)) {
@@ -276,7 +290,7 @@ __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_ker
         for (int i = 2; i < 16; i += 2) mx = fmaxf(mx, fmaxf(s[0][i], s[0][i + 1]));
 #pragma unroll
         for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(s[1][i], s[1][i + 1]));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        mx = max_halves(mx);
         if (t == 0 || __any(mx > kLazy)) {
           // raise the running max: by the tile max on the first tile, else where it grew past 2^kLazy
           const float dm = (t == 0 || mx > kLazy) ? mx : 0.f;
@@ -325,7 +339,7 @@ __global__ __launch_bounds__(256, AttnTraits<DH>::kMinBlocks) void attn_bf16_ker
     }
     __syncthreads();   // the next q-block refills the ring
 
-    const float l = l_run + __shfl_xor(l_run, 32, 64);
+    const float l = sum_halves(l_run);
     const float inv = 1.0f / l;
     const int q_out = q0 + w * 32 + l32;
     if (q_out < T) {
@@ -393,9 +407,10 @@ hipError_t launch_attention(const void* qkv, int64_t ldq, void* out, int64_t ldo
       wk.order[b] = v;
     }
     const bool pre = prefix && prefix->P > 0;
+    const int bq = 32 * (head_dim == 64 ? AttnTraits<64>::kWaves : AttnTraits<128>::kWaves);   // queries per block
     wk.cum[0] = 0;
     for (int j = 0; j < st.n; ++j) {
-      const int k = wk.order[j], nqb = (st.off[k + 1] - st.off[k] + 127) / 128;
+      const int k = wk.order[j], nqb = (st.off[k + 1] - st.off[k] + bq - 1) / bq;
       wk.cum[j + 1] = wk.cum[j] + (pre ? nqb : (nqb + 1) / 2);
     }
     wk.total = wk.cum[st.n];
@@ -414,8 +429,8 @@ hipError_t launch_attention(const void* qkv, int64_t ldq, void* out, int64_t ldo
       if (pk.n_seq > 0 && (st.n % pk.n_seq != 0 || (pk.alt_pass >= 0 && !pk.v_alt))) return hipErrorInvalidValue;
     }
 #define RK_ATTN(D, PRE)                                                                                      \
-  attn_bf16_kernel<D, PRE><<<grid, 256, 0, s>>>((const bf16_t*)qkv, ldq, (bf16_t*)out, ldo, st, wk, n_heads, \
-                                                n_kv_heads, n_items, pk)
+  attn_bf16_kernel<D, PRE><<<grid, 64 * AttnTraits<D>::kWaves, 0, s>>>((const bf16_t*)qkv, ldq, (bf16_t*)out, ldo, \
+                                                                      st, wk, n_heads, n_kv_heads, n_items, pk)
     if (head_dim == 128) { if (pre) RK_ATTN(128, true); else RK_ATTN(128, false); }
     else if (head_dim == 64) { if (pre) RK_ATTN(64, true); else RK_ATTN(64, false); }
     else return hipErrorInvalidValue;
