@@ -89,6 +89,7 @@ def derive_traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, family)
 FAMILIES = [("gemm_gate_up", "EpiSwiGLU"), ("gemm_qkv", "EpiRope"), ("gemm_o_down", "EpiResidual"),
             ("lm_kl", "lm_kl_kernel"), ("lm_lse", "lm_lse_kernel"), ("attention", "attn_bf16_kernel"),
             ("rmsnorm", "rmsnorm_kernel"), ("noise", "value_noise_kernel"), ("kl_merge", "kl_merge_kernel"),
+            ("kl_logits", "kl_logits_kernel"), ("lm_logits", "EpiStoreF32"),
             ("local_response", "local_response_kernel")]
 
 
@@ -906,6 +907,9 @@ def main():
     ap.add_argument("--signal", choices=("downstream", "local"), default="downstream",
                     help="profile signal: the KL of the final distributions (the method) or the layer-local "
                          "response of the perturbed block (the w/o DS ablation)")
+    ap.add_argument("--unfused-kl", action="store_true",
+                    help="score the passes through materialised fp32 logits and the separate KL kernel "
+                         "(the verification path) instead of the fused LM-head + KL")
     ap.add_argument("--window", type=int, default=0,
                     help="cached-window mode: evaluate the last WINDOW tokens of every sequence against the cached "
                          "prefix (0: the resumed full-sequence profile)")
@@ -992,12 +996,13 @@ def main():
     window = int(args.window)
     local = args.signal == "local"
     flags = ((rk.RK_FLAG_CACHED_WINDOW if window > 0 else 0) | (0 if args.no_graph else rk.RK_FLAG_GRAPH) |
-             (rk.RK_FLAG_LOCAL_SIGNAL if local else 0))
+             (rk.RK_FLAG_LOCAL_SIGNAL if local else 0) | (rk.RK_FLAG_UNFUSED_KL if args.unfused_kl else 0))
     P = min(w.lengths()) - window if window > 0 else 0
     if window > 0 and P < 1:
         raise SystemExit(f"--window {window} leaves no prefix in the shortest sequence")
     ws = torch.empty(model.workspace_size(rows, G, rk.RK_WS_CLEAN_STATE |
-                                          (flags & (rk.RK_FLAG_CACHED_WINDOW | rk.RK_FLAG_LOCAL_SIGNAL))),
+                                          (flags & (rk.RK_FLAG_CACHED_WINDOW | rk.RK_FLAG_LOCAL_SIGNAL |
+                                                    rk.RK_FLAG_UNFUSED_KL))),
                      dtype=torch.uint8, device="cuda")
     s_out = torch.empty(len(alphas), len(layers), dtype=torch.float32, device="cuda")
     d_out = torch.empty(len(alphas), batch.n_seqs, len(layers), dtype=torch.float32, device="cuda")
@@ -1043,7 +1048,13 @@ def main():
     value = tokens_layers / (ms_per_step / 1e3)
 
     fam_avg_ms = fam_ms / max(launches, 1)
-    if args.family == "lm_kl":
+    hbm_family = args.family == "kl_logits"
+    if hbm_family:
+        # one launch scores a group of passes: every logit of the clean rows and of
+        # each pass read once, one fp32 KL per row and pass written
+        n_launch_pass = len(layers) * len(alphas) / max(launches / args.steps, 1)
+        flops = (1 + n_launch_pass) * eval_rows * cfg.vocab * 4.0 + n_launch_pass * eval_rows * 4.0
+    elif args.family == "lm_kl":
         n_pass_lm = G  # perturbed passes scored per LM-head launch (algorithmic: pert logits only)
         flops = family_flops(args.family, cfg, eval_rows, n_pass_lm)
     else:
@@ -1057,16 +1068,22 @@ def main():
         rows_total = rows * L + eval_rows * pass_layers if window == 0 else \
             (rows - eval_rows) * L + eval_rows * L + eval_rows * pass_layers
         flops = family_flops(args.family, cfg, rows_total, 1) * args.steps / max(launches, 1)
-    achieved = flops / (fam_avg_ms / 1e3) / 1e12
+    achieved = flops / (fam_avg_ms / 1e3) / (1e9 if hbm_family else 1e12)
     traffic = None
     rec = TRAFFIC.get((args.family, w.name))
     if rec is not None and rec["sources"] == sources_hash():
         traffic = rec["bytes_per_launch"]
-    roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": traffic,
-            "kernel": args.family, "launches": launches, "avg_ms": round(fam_avg_ms, 4),
-            "flop_per_launch": flops}
-    log(f"{args.family}: {launches} launches, avg {fam_avg_ms:.4f} ms, {achieved:.1f} TFLOP/s")
+    if hbm_family:
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": args.family,
+                "launches": launches, "avg_ms": round(fam_avg_ms, 4), "bytes_per_launch": flops}
+    else:
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": traffic,
+                "kernel": args.family, "launches": launches, "avg_ms": round(fam_avg_ms, 4),
+                "flop_per_launch": flops}
+    log(f"{args.family}: {launches} launches, avg {fam_avg_ms:.4f} ms, {achieved:.1f} "
+        f"{'GB/s' if hbm_family else 'TFLOP/s'}")
     # the whole step's MFMA utilisation: its algorithmic work over the step time
     sf = step_flops(cfg, w.lengths(), layers, alphas, P, local)
     util = {"step_tflop": round(sf / 1e12, 2), "achieved": round(sf / (ms_per_step / 1e3) / 1e12, 1),
@@ -1075,6 +1092,7 @@ def main():
 
     mode = "" if window == 0 else f"; cached window: prefix {P}, window {window} per sequence"
     mode += "; layer-local signal (w/o DS ablation)" if local else ""
+    mode += "; unfused KL (materialised fp32 logits, separate KL kernel)" if args.unfused_kl else ""
     metric = ("perturbed token-layers/s (sensitivity-profile throughput)" if window == 0 else
               "perturbed window token-layers/s (cached-window sensitivity-profile throughput)")
     if local:

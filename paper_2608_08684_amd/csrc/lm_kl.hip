@@ -390,59 +390,143 @@ hipError_t launch_lm_kl(const bf16_t* xc, const bf16_t* xp, int64_t pass_stride,
 }
 
 // --------------------------------------------------------------------------- unfused KL
-// One workgroup per (row, pass): two sweeps over the clean row (max, then sum of
-// exp) and one over both rows for F and S.  Fixed-order block reductions.
+// One workgroup (16 waves) per row scores every pass of the group: one sweep over
+// the clean row gives its log-sum-exp A (running max and rescaled sum per thread,
+// merged in a fixed order); when the row fits (vocab <= kKlLdsRow) it stays in
+// LDS, so every pass reads only its own row from memory, once (p_v =
+// 2^(a_v log2 e - A log2 e) with the hardware exp2, as in the fused kernel).  Per
+// thread F and S are summed in fp32 over its vocab / 1024 entries, then across
+// the workgroup in double, in a fixed order (lane tree, then waves in order).
+constexpr int kKlThreads = 1024;
+constexpr int kKlLdsRow = 36864;   // longest row kept in LDS (144 KB of fp32)
+
+template <typename T>
+__device__ __forceinline__ T wave_sum(T v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+  return v;
+}
+
+// sum over the workgroup: every thread gets the same value
 __device__ __forceinline__ double block_sum(double v, double* red) {
-  red[threadIdx.x] = v;
+  const int w = threadIdx.x >> 6;
+  v = wave_sum(v);
+  if ((threadIdx.x & 63) == 0) red[w] = v;
   __syncthreads();
-  for (int w = 128; w >= 1; w >>= 1) {
-    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
-    __syncthreads();
-  }
-  const double r = red[0];
+  double r = 0.0;
+  for (int i = 0; i < kKlThreads / 64; ++i) r += red[i];
   __syncthreads();
   return r;
 }
 
-__global__ __launch_bounds__(256) void kl_logits_kernel(const float* __restrict__ lc, const float* __restrict__ lp,
-                                                        int64_t pass_stride, int rows, int vocab,
-                                                        float* __restrict__ kl) {
-  __shared__ double red[256];
-  __shared__ float redf[256];
-  const int r = blockIdx.x, g = blockIdx.y;
-  const float* a = lc + (int64_t)r * vocab;
-  const float* b = lp + (int64_t)g * pass_stride + (int64_t)r * vocab;
-  float mx = -INFINITY;
-  for (int v = threadIdx.x; v < vocab; v += 256) mx = fmaxf(mx, a[v]);
-  redf[threadIdx.x] = mx;
+// merge of two (max, sum of exp(x - max)) pairs
+__device__ __forceinline__ void lse_merge(float& m, double& z, float m2, double z2) {
+  if (m2 == -INFINITY) return;
+  if (m == -INFINITY) { m = m2; z = z2; return; }
+  const float mn = fmaxf(m, m2);
+  z = z * (double)expf(m - mn) + z2 * (double)expf(m2 - mn);
+  m = mn;
+}
+
+// one step of the running (max, sum) of a thread
+__device__ __forceinline__ void lse_add(float& m, double& z, float x) {
+  if (x > m) { z = z * (double)expf(m - x) + 1.0; m = x; }   // expf(-inf) = 0 on the first element
+  else z += (double)expf(x - m);
+}
+
+__device__ __forceinline__ float block_lse(float m, double z, double* red, float* redm) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) lse_merge(m, z, __shfl_xor(m, d, 64), __shfl_xor(z, d, 64));
+  if (lane == 0) { redm[w] = m; red[w] = z; }
   __syncthreads();
-  for (int w = 128; w >= 1; w >>= 1) {
-    if ((int)threadIdx.x < w) redf[threadIdx.x] = fmaxf(redf[threadIdx.x], redf[threadIdx.x + w]);
-    __syncthreads();
-  }
-  mx = redf[0];
+  float M = -INFINITY;
+  double Z = 0.0;
+  for (int i = 0; i < kKlThreads / 64; ++i) lse_merge(M, Z, redm[i], red[i]);
   __syncthreads();
+  return (float)((double)M + log(Z));
+}
+
+// F and S terms of one entry: clean logit x, pass logit y
+__device__ __forceinline__ void kl_terms(float x, float y, float Al, float& f1, float& s1) {
+  const float p = __builtin_amdgcn_exp2f(fmaf(x, kLog2e, -Al));
+  const float dl = x - y;
+  const float f = kl_f(dl);
+  f1 = fmaf(p, f, f1);
+  s1 = fmaf(p, f - dl, s1);
+}
+
+// Rows are read as 16-byte groups of four entries (vocab is a multiple of 128),
+// four groups per thread in flight.
+template <bool IN_LDS>
+__global__ __launch_bounds__(kKlThreads) void kl_logits_kernel(const float* __restrict__ lc,
+                                                               const float* __restrict__ lp, int64_t pass_stride,
+                                                               int G, int rows, int vocab, float* __restrict__ kl) {
+  __shared__ float4 row[IN_LDS ? kKlLdsRow / 4 : 1];
+  __shared__ double red[kKlThreads / 64];
+  __shared__ float redm[kKlThreads / 64];
+  constexpr int U = 4;
+  const int r = blockIdx.x, t = threadIdx.x, n4 = vocab / 4;
+  const float4* a = reinterpret_cast<const float4*>(lc + (int64_t)r * vocab);
+  float m = -INFINITY;
   double z = 0.0;
-  for (int v = threadIdx.x; v < vocab; v += 256) z += (double)expf(a[v] - mx);
-  z = block_sum(z, red);
-  const float A = (float)((double)mx + log(z));
-  double F = 0.0, S = 0.0;
-  for (int v = threadIdx.x; v < vocab; v += 256) {
-    const float p = expf(a[v] - A);
-    const float dl = a[v] - b[v];
-    const float f = kl_f(dl);
-    F += (double)(p * f);
-    S += (double)(p * (f - dl));
+  for (int q0 = t; q0 < n4; q0 += U * kKlThreads) {
+    float4 x[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int q = q0 + u * kKlThreads;
+      if (q < n4) x[u] = a[q];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int q = q0 + u * kKlThreads;
+      if (q < n4) {
+        if (IN_LDS) row[q] = x[u];
+        lse_add(m, z, x[u].x);
+        lse_add(m, z, x[u].y);
+        lse_add(m, z, x[u].z);
+        lse_add(m, z, x[u].w);
+      }
+    }
   }
-  F = block_sum(F, red);
-  S = block_sum(S, red);
-  if (threadIdx.x == 0) kl[(int64_t)g * rows + r] = (float)(F - (S - log1p(S)));
+  const float A = block_lse(m, z, red, redm);   // its barriers also publish the LDS row
+  const float Al = A * kLog2e;
+  for (int g = 0; g < G; ++g) {
+    const float4* b = reinterpret_cast<const float4*>(lp + (int64_t)g * pass_stride + (int64_t)r * vocab);
+    float f1 = 0.f, s1 = 0.f;
+    for (int q0 = t; q0 < n4; q0 += U * kKlThreads) {
+      float4 y[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int q = q0 + u * kKlThreads;
+        if (q < n4) y[u] = b[q];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int q = q0 + u * kKlThreads;
+        if (q < n4) {
+          const float4 x = IN_LDS ? row[q] : a[q];
+          kl_terms(x.x, y[u].x, Al, f1, s1);
+          kl_terms(x.y, y[u].y, Al, f1, s1);
+          kl_terms(x.z, y[u].z, Al, f1, s1);
+          kl_terms(x.w, y[u].w, Al, f1, s1);
+        }
+      }
+    }
+    const double F = block_sum((double)f1, red);
+    const double S = block_sum((double)s1, red);
+    if (t == 0) kl[(int64_t)g * rows + r] = (float)(F - (S - log1p(S)));
+  }
 }
 
 hipError_t launch_kl_logits(const float* lc, const float* lp, int64_t pass_stride, int G, int rows, int vocab,
                             float* kl, hipStream_t s) {
   if (rows <= 0 || G <= 0) return hipSuccess;
-  kl_logits_kernel<<<dim3(rows, G), 256, 0, s>>>(lc, lp, pass_stride, rows, vocab, kl);
+  if (vocab % 4 != 0 || pass_stride % 4 != 0 || ((uintptr_t)lc | (uintptr_t)lp) % 16 != 0) return hipErrorInvalidValue;
+  if (vocab <= kKlLdsRow)
+    kl_logits_kernel<true><<<rows, kKlThreads, 0, s>>>(lc, lp, pass_stride, G, rows, vocab, kl);
+  else
+    kl_logits_kernel<false><<<rows, kKlThreads, 0, s>>>(lc, lp, pass_stride, G, rows, vocab, kl);
   return hipGetLastError();
 }
 
