@@ -891,6 +891,54 @@ def pair_main(args):
     print(json.dumps(res), flush=True)
 
 
+def fp32_cost_main(args):
+    """Cost of the fp32 path (every operand and activation fp32, the bf16 weights
+    upcast exactly) against the bf16 path on the same model: the profile of the
+    first `--fp32-tokens` tokens of sequence 0 at the last and the middle layer
+    (largest alpha), timed with each dtype.  The fp32 path is the option that
+    meets the 1e-4 fp32 logit bar at 32 layers; this prices it."""
+    import dataclasses
+    import torch
+    import fixtures as F
+    import paper_2608_08684_amd as rk
+    from paper_2608_08684_amd.inputs import batch_from_tokens, upload_weights
+
+    w = F.get_workload(args.workload)
+    cfg16 = w.model
+    T = int(args.fp32_tokens)
+    toks = [F.make_tokens(w)[0][:T]]
+    layers = [cfg16.n_layers - 1, cfg16.n_layers // 2]
+    alpha = max(w.alphas)
+    W16 = F.make_weights(cfg16)
+    out = {}
+    for name, cfg, W in (("bf16", cfg16, W16),
+                         ("f32", dataclasses.replace(cfg16, dtype="f32"), F.f32_weights(cfg16, W16))):
+        model = rk.Model(cfg, upload_weights(W))
+        batch = batch_from_tokens(toks)
+        wsf = rk.RK_WS_CLEAN_STATE | (rk.RK_FLAG_UNFUSED_KL if name == "f32" else 0)
+        ws = torch.empty(model.workspace_size(batch.rows, len(layers), wsf), dtype=torch.uint8, device="cuda")
+        s_out = torch.empty(1, len(layers), dtype=torch.float32, device="cuda")
+        run = lambda: model.sensitivity_profile(batch, layers, [alpha], s_out, ws, batch.rows, len(layers))
+        run()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            run()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        fl = step_flops(cfg16, [T], layers, [alpha])
+        out[name] = {"ms_per_profile": round(ms, 2), "tflop_per_s": round(fl / (ms / 1e3) / 1e12, 2),
+                     "s": [float(x) for x in s_out.cpu().numpy()[0]]}
+        log(f"{name}: {ms:.1f} ms per profile, {fl / (ms / 1e3) / 1e12:.1f} TFLOP/s")
+        del model, ws, s_out
+        torch.cuda.empty_cache()
+    res = {"metric": "fp32-path cost (profile wall time, fp32 vs bf16)", "workload":
+           f"{w.name}: first {T} tokens of sequence 0, layers {layers}, alpha {alpha}",
+           "bf16": out["bf16"], "f32": out["f32"],
+           "f32_over_bf16": round(out["f32"]["ms_per_profile"] / out["bf16"]["ms_per_profile"], 1)}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -907,6 +955,9 @@ def main():
     ap.add_argument("--signal", choices=("downstream", "local"), default="downstream",
                     help="profile signal: the KL of the final distributions (the method) or the layer-local "
                          "response of the perturbed block (the w/o DS ablation)")
+    ap.add_argument("--fp32-cost", action="store_true",
+                    help="price the fp32 path against the bf16 path on a prefix of the workload's first sequence")
+    ap.add_argument("--fp32-tokens", type=int, default=2048)
     ap.add_argument("--unfused-kl", action="store_true",
                     help="score the passes through materialised fp32 logits and the separate KL kernel "
                          "(the verification path) instead of the fused LM-head + KL")
@@ -956,6 +1007,9 @@ def main():
             y.copy_(x)
         torch.cuda.synchronize()
         log(f"copied {n} bytes 3 times")
+        return
+    if args.fp32_cost:
+        fp32_cost_main(args)
         return
     if args.snapkv:
         snapkv_main(args)
