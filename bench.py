@@ -39,25 +39,40 @@ HBM_PEAK_GBS = 8000.0         # MI355X HBM3E
 
 # HBM bytes per launch of a kernel family, from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # counter runs of this benchmark scaled by a 1 GiB copy (see --derive-traffic and
-# profiles/).  Keyed by (family, workload); valid only while the kernel sources
-# hash to the recorded value, so a changed kernel reports null until re-measured.
+# profiles/).  Keyed by (family, workload); valid only while the family's kernel
+# sources hash to the recorded value, so a changed kernel reports null until
+# re-measured.
 TRAFFIC = {
     ("gemm_gate_up", "gpt2s-bf16"): {"bytes_per_launch": 327091576, "fetch_bytes": 226428280,
-                                     "write_bytes": 100663296, "sources": "f14efdc2512a7226"},
+                                     "write_bytes": 100663296, "sources": "5138ba9bfc0b0ac1"},
+    ("gemm_gate_up", "llama3-8b-long-bf16"): {"bytes_per_launch": 12232403950, "fetch_bytes": 11292879854,
+                                              "write_bytes": 939524096, "sources": "5138ba9bfc0b0ac1"},
+    ("attention", "llama3-8b-long-bf16"): {"bytes_per_launch": 1675658863, "fetch_bytes": 1407164068,
+                                           "write_bytes": 268494795, "sources": "2b5f7aefbb31b8d4"},
 }
-KERNEL_SOURCES = ["paper_2608_08684_amd/csrc/gemm.hip", "paper_2608_08684_amd/csrc/mfma_tile.h",
-                  "paper_2608_08684_amd/csrc/rk_internal.h"]
+FAMILY_SOURCES = {
+    "gemm": ["paper_2608_08684_amd/csrc/gemm.hip", "paper_2608_08684_amd/csrc/mfma_tile.h"],
+    "attention": ["paper_2608_08684_amd/csrc/attention.hip"],
+    "lm_kl": ["paper_2608_08684_amd/csrc/lm_kl.hip", "paper_2608_08684_amd/csrc/mfma_tile.h"],
+}
 FAMILY_KERNEL = {"gemm_gate_up": "EpiSwiGLU", "gemm_qkv": "EpiRope", "lm_kl": "lm_kl_kernel",
                  "attention": "attn_bf16_kernel"}
 
 
-def sources_hash() -> str:
+def sources_hash(family: str) -> str:
+    """Digest of the kernel sources of a family (gemm_* share the GEMM sources)."""
     import hashlib
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
+    for rel in FAMILY_SOURCES["gemm" if family.startswith("gemm") else family]:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
+
+
+def traffic_of(family: str, workload: str):
+    """Recorded HBM bytes per launch of a family, or None once its sources changed."""
+    rec = TRAFFIC.get((family, workload))
+    return rec["bytes_per_launch"] if rec is not None and rec["sources"] == sources_hash(family) else None
 
 
 def derive_traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, family):
@@ -82,7 +97,7 @@ def derive_traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, family)
     fetch = per_dispatch(fetch_dir, key) * f_scale
     write = per_dispatch(write_dir, key) * w_scale
     return {"kernel": family, "fetch_bytes": fetch, "write_bytes": write, "bytes_per_launch": fetch + write,
-            "fetch_scale": f_scale, "write_scale": w_scale, "sources": sources_hash()}
+            "fetch_scale": f_scale, "write_scale": w_scale, "sources": sources_hash(family)}
 
 
 # kernel families of the profile, by a substring of the kernel name (first match wins)
@@ -854,7 +869,7 @@ def pair_main(args):
     dom = max(kern, key=lambda f: kern[f]["ms_per_step"])
     kd = kern[dom]
     roof = {"bound": "mfma", "achieved": kd["achieved"], "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(kd["achieved"] / BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": dom,
+            "frac": round(kd["achieved"] / BF16_PEAK_TFLOPS, 4), "traffic": traffic_of(dom, w.name), "kernel": dom,
             "launches": kd["launches"], "avg_ms": kd["avg_ms"], "flop_per_launch": kd["flop_per_launch"]}
     for f, r in kern.items():
         log(f"{f}: {r['launches']} launches, avg {r['avg_ms']:.4f} ms, {r['achieved']:.1f} TFLOP/s, "
@@ -1123,10 +1138,7 @@ def main():
             (rows - eval_rows) * L + eval_rows * L + eval_rows * pass_layers
         flops = family_flops(args.family, cfg, rows_total, 1) * args.steps / max(launches, 1)
     achieved = flops / (fam_avg_ms / 1e3) / (1e9 if hbm_family else 1e12)
-    traffic = None
-    rec = TRAFFIC.get((args.family, w.name))
-    if rec is not None and rec["sources"] == sources_hash():
-        traffic = rec["bytes_per_launch"]
+    traffic = traffic_of(args.family, w.name)
     if hbm_family:
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": args.family,
