@@ -152,7 +152,10 @@ typedef struct rk_model rk_model;      /* opaque, host-side */
  * tokens: DEVICE int32 [offsets[n_seqs]]; offsets: HOST int64 [n_seqs + 1],
  * offsets[0] = 0, non-decreasing; seq_index0: index in the calibration set of the
  * batch's first sequence (sequence k of the batch has index seq_index0 + k, which
- * keys its noise).  1 <= n_seqs <= RK_MAX_BATCH_SEQS.                          */
+ * keys its noise).  1 <= n_seqs <= RK_MAX_BATCH_SEQS.  On a bf16 model every
+ * sequence must satisfy T * (H + 2*Hkv) * head_dim * 2 < 2^31 bytes (the
+ * attention kernel's 32-bit buffer offsets; at most 174762 tokens at the
+ * Llama-3-8B shape); a longer one is RK_ERR_SHAPE before any device work.      */
 typedef struct {
   const int32_t *tokens;
   const int64_t *offsets;

@@ -469,6 +469,21 @@ static rk_status clean_logits(const rk_model* m, const SeqTable& st, const Clean
 }
 
 // ----------------------------------------------------------------------------- cached-window mode
+// The bf16 attention kernel addresses one sequence's q|k|v rows (and, in the
+// cached-window mode, that sequence's cached K and V prefix, whose rows are
+// narrower and fewer) through buffer descriptors with 32-bit byte offsets; a
+// batch with a longer sequence is refused before any launch.
+static rk_status check_span(const rk_model* m, const SeqTable& st) {
+  if (!m->bf16) return RK_OK;
+  const int64_t lim = (int64_t)1 << 31;
+  if ((int64_t)st.max_len * m->qkv_cols * 2 >= lim) {
+    set_error("a sequence of %d tokens exceeds the attention kernel's 32-bit buffer range (fewer than %lld tokens "
+              "per sequence for this model)", st.max_len, (long long)((lim - 1) / ((int64_t)m->qkv_cols * 2)));
+    return RK_ERR_SHAPE;
+  }
+  return RK_OK;
+}
+
 // Row tables of a cached-window batch: the prefix rows (P per sequence, in
 // sequence order) and the window rows (T_k - P per sequence).
 static rk_status window_tables(const SeqTable& st, int P, SeqTable* pst, SeqTable* wst) {
@@ -847,7 +862,7 @@ static rk_status window_policy_final(const rk_model* m, const SeqTable& pst, con
 }
 
 // ----------------------------------------------------------------------------- validation
-static rk_status make_table(const rk_batch* bt, int first, int count, SeqTable* st) {
+static rk_status make_table(const rk_model* m, const rk_batch* bt, int first, int count, SeqTable* st) {
   if (count < 1 || count > RK_MAX_BATCH_SEQS) {
     set_error("batch holds %d sequences (1..%d allowed)", count, RK_MAX_BATCH_SEQS);
     return RK_ERR_SHAPE;
@@ -868,7 +883,7 @@ static rk_status make_table(const rk_batch* bt, int first, int count, SeqTable* 
   }
   st->rows = st->off[count];
   if (st->rows < 1) { set_error("batch has no tokens"); return RK_ERR_SHAPE; }
-  return RK_OK;
+  return check_span(m, *st);
 }
 
 static rk_status check_batch(const rk_model* m, const rk_batch* b) {
@@ -1133,6 +1148,21 @@ static rk_status check_profile(const rk_model* m, const rk_batch* calib, const i
   if (cw && (e = check_window_model(m)) != RK_OK) return e;
   const uint32_t wflags = RK_WS_CLEAN_STATE | (unfused ? RK_FLAG_UNFUSED_KL : 0) | (cw ? RK_FLAG_CACHED_WINDOW : 0) |
                           (local ? RK_FLAG_LOCAL_SIGNAL : 0);
+  // every batch the run will form, validated before any launch
+  for (int first = 0; first < N;) {
+    int count = 0;
+    int64_t rows = 0;
+    while (first + count < N && count < RK_MAX_BATCH_SEQS) {
+      const int64_t len = calib->offsets[first + count + 1] - calib->offsets[first + count];
+      if (count > 0 && rows + len > max_rows) break;
+      rows += len;
+      ++count;
+    }
+    SeqTable st, pst, wst;
+    if ((e = make_table(m, calib, first, count, &st)) != RK_OK) return e;
+    if (cw && (e = window_tables(st, p->window_start, &pst, &wst)) != RK_OK) return e;
+    first += count;
+  }
   *wp = ws_plan(m, max_rows, max_group, wflags);
   return RK_OK;
 }
@@ -1163,7 +1193,7 @@ static rk_status profile_run(const rk_model* m, const rk_batch* calib, const int
       ++count;
     }
     SeqTable st;
-    if ((e = make_table(calib, first, count, &st)) != RK_OK) return e;
+    if ((e = make_table(m, calib, first, count, &st)) != RK_OK) return e;
     const int32_t* tokens = calib->tokens + calib->offsets[first];
     const int64_t R = st.rows;
     if (cw) {
@@ -1367,7 +1397,7 @@ rk_status rk_window_reference(const rk_model* m, const rk_batch* batch, int32_t 
   if ((e = check_window_model(m)) != RK_OK) return e;
   if (!state || !workspace) { set_error("null state or workspace"); return RK_ERR_ARG; }
   SeqTable st, pst, wst;
-  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  if ((e = make_table(m, batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
   if ((e = window_tables(st, window_start, &pst, &wst)) != RK_OK) return e;
   if (state_bytes < win_plan(m, st.rows).total) { set_error("window state too small"); return RK_ERR_WORKSPACE; }
   const WsPlan wp = ws_plan(m, st.rows, 1, RK_FLAG_CACHED_WINDOW);
@@ -1395,7 +1425,7 @@ rk_status rk_snapkv_prefill(const rk_model* m, const rk_batch* batch, int32_t ob
   if ((e = check_snap(m, obs_window)) != RK_OK) return e;
   if (!state || !workspace) { set_error("null state or workspace"); return RK_ERR_ARG; }
   SeqTable st;
-  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  if ((e = make_table(m, batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
   for (int i = 0; i < st.n; ++i)
     if (st.off[i + 1] - st.off[i] <= obs_window) {
       set_error("sequence %d is not longer than obs_window %d", i, obs_window);
@@ -1454,7 +1484,7 @@ rk_status rk_snapkv_compress(const rk_model* m, const rk_batch* batch, const rk_
   }
   if (p->pooling != RK_POOL_MAX && p->pooling != RK_POOL_AVG) { set_error("unknown pooling"); return RK_ERR_ARG; }
   SeqTable st;
-  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  if ((e = make_table(m, batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
   if ((e = check_snap_lengths(st, w)) != RK_OK) return e;
   const SnapPlan sp = snap_plan(m, st.rows, st.n, w);
   if (state_bytes < sp.total) { set_error("SnapKV state too small (%zu < %zu)", state_bytes, sp.total); return RK_ERR_WORKSPACE; }
@@ -1532,7 +1562,7 @@ static rk_status win_call(const rk_model* m, const rk_batch* batch, int32_t wind
                           size_t state_bytes, void* workspace, size_t ws_bytes, int G, uint32_t wf, void* stream,
                           WinCall* c) {
   rk_status e;
-  if ((e = make_table(batch, 0, batch->n_seqs, &c->st)) != RK_OK) return e;
+  if ((e = make_table(m, batch, 0, batch->n_seqs, &c->st)) != RK_OK) return e;
   if ((e = window_tables(c->st, window_start, &c->pst, &c->wst)) != RK_OK) return e;
   if (state_bytes < win_plan(m, c->st.rows).total) { set_error("window state too small"); return RK_ERR_WORKSPACE; }
   const WsPlan wp = ws_plan(m, c->st.rows, G, wf);
@@ -1682,7 +1712,7 @@ rk_status rk_reference_forward(const rk_model* m, const rk_batch* batch, void* c
   if (e != RK_OK) return e;
   if (!clean_state || !workspace) { set_error("null clean state or workspace"); return RK_ERR_ARG; }
   SeqTable st;
-  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  if ((e = make_table(m, batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
   if (clean_bytes < clean_plan(m, st.rows).total) { set_error("clean state too small"); return RK_ERR_WORKSPACE; }
   const WsPlan wp = ws_plan(m, st.rows, 1, 0);
   if (ws_bytes < wp.total) { set_error("workspace too small (%zu < %zu)", ws_bytes, wp.total); return RK_ERR_WORKSPACE; }
@@ -1702,7 +1732,7 @@ rk_status rk_profile_layer(const rk_model* m, const rk_batch* batch, int32_t lay
   if (layer < 0 || layer >= m->cfg.n_layers) { set_error("layer %d out of range", layer); return RK_ERR_ARG; }
   if (!(alpha >= 0.0f) || !isfinite(alpha)) { set_error("alpha must be finite and >= 0"); return RK_ERR_ARG; }
   SeqTable st;
-  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  if ((e = make_table(m, batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
   if ((e = check_windows(st, p->window_start)) != RK_OK) return e;
   const bool local = (p->flags & RK_FLAG_LOCAL_SIGNAL) != 0;
   if (local && logits_out) { set_error("RK_FLAG_LOCAL_SIGNAL produces no logits"); return RK_ERR_ARG; }
@@ -1859,7 +1889,7 @@ rk_status rk_perturb_values(const rk_model* m, const rk_batch* batch, int32_t la
     return RK_ERR_ARG;
   }
   SeqTable st;
-  if ((e = make_table(batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
+  if ((e = make_table(m, batch, 0, batch->n_seqs, &st)) != RK_OK) return e;
   const rk_model_config& c = m->cfg;
   if (c.head_dim != 32 && c.head_dim != 64 && c.head_dim != 128) { set_error("head_dim unsupported"); return RK_ERR_UNSUPPORTED; }
   RK_TRY(launch_value_noise(v, m->bf16, row_stride, st, c.n_kv_heads, c.head_dim, layer, alpha, p->seed,

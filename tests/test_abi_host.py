@@ -560,3 +560,42 @@ def test_local_signal_flag_validates_before_launching():
                                       None, fake, need_p - 1, None) == rk.RK_ERR_WORKSPACE
     assert need_p >= need + R * d * 4
     lib.rk_model_destroy(h)
+
+
+def test_sequences_beyond_the_attention_buffer_range_are_refused():
+    """The bf16 attention kernel reads a sequence's q|k|v rows through 32-bit
+    buffer offsets, so T * qkv_cols * 2 must stay below 2^31 bytes: the longest
+    admissible sequence passes validation (it then fails on the workspace size
+    given here), one token more is RK_ERR_SHAPE from every entry point, before any
+    device work, in the resumed and the cached-window mode."""
+    lib = rk.load()
+    cfg = _FakeCfg()
+    st, h = _create(cfg)
+    assert st == rk.RK_OK
+    fake = ctypes.c_void_p(0x1000)
+    qkv_cols = (cfg.n_heads + 2 * cfg.n_kv_heads) * cfg.head_dim
+    t_max = ((1 << 31) - 1) // (qkv_cols * 2)
+    lay = (ctypes.c_int32 * 1)(0)
+    alp = (ctypes.c_float * 1)(0.1)
+    for T, ok in ((t_max, True), (t_max + 1, False)):
+        offs = np.array([0, 100, 100 + T], dtype=np.int64)
+        batch = rk._Batch(fake, offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 2, 0)
+        for flags in (0, rk.RK_FLAG_CACHED_WINDOW):
+            p = rk._Params(2, 50, 0, 0, flags)
+            calls = [lib.rk_profile_layer(h, ctypes.byref(batch), 0, 0.1, ctypes.byref(p), fake, 16, fake, None,
+                                          None, fake, 16, None),
+                     lib.rk_sensitivity_profile(h, ctypes.byref(batch), lay, 1, alp, 1, ctypes.byref(p), T + 100, 1,
+                                                fake, None, fake, 16, None),
+                     lib.rk_sensitivity_profile_static(h, ctypes.byref(batch), lay, 1, alp, 1, ctypes.byref(p),
+                                                       T + 100, 1, fake, None, None)]
+            if flags == 0:
+                calls.append(lib.rk_reference_forward(h, ctypes.byref(batch), fake, 16, fake, 16, None))
+            else:
+                calls.append(lib.rk_window_reference(h, ctypes.byref(batch), 50, fake, 16, fake, 16, None))
+            for c in calls:
+                if ok:
+                    assert c == rk.RK_ERR_WORKSPACE, (T, flags, c, lib.rk_last_error())
+                else:
+                    assert c == rk.RK_ERR_SHAPE, (T, flags, c)
+                    assert b"32-bit buffer range" in lib.rk_last_error()
+    lib.rk_model_destroy(h)
