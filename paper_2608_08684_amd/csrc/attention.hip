@@ -25,7 +25,9 @@
 //     the V^T operand comes from the row-major V tile through ds_read_b64_tr_b16
 //     in the same key order; the softmax denominator is summed from the rounded
 //     P with v_dot2_f32_bf16, so the weights applied to V sum to one;
-//   * masks only on diagonal / ragged tiles.
+//   * masks only on diagonal / ragged tiles;
+//   * the K fragment reads of a tile are issued up to six ahead of the MFMAs
+//     that consume them (scheduling groups), not each right before its use.
 // fp32 kernel: one thread per (row, head), streaming keys; for the small fp32
 // model only.
 #include <math.h>
@@ -273,6 +275,18 @@ __global__ __launch_bounds__(64 * AttnTraits<DH>::kWaves, AttnTraits<DH>::kMinBl
             const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const v4u*>(kt + rb * 32 * ROWB + kfo[ks]));
             s[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s[rb], 0, 0, 0);
           }
+        {
+          // schedule: the K fragment reads run up to three MFMA pairs ahead of their
+          // MFMAs (the compiler's own order waits on each read right before its use)
+          constexpr int AHEAD = NKS >= 8 ? 6 : 4, N = 2 * NKS;
+          __builtin_amdgcn_sched_group_barrier(0x100, AHEAD, 0);   // LDS reads
+#pragma unroll
+          for (int p = 0; p < (N - AHEAD) / 2; ++p) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);     // MFMAs
+            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, AHEAD, 0);
+        }
         // masks only where a key can exceed the query or the segment (wave-uniform test);
         // every cached prefix key precedes every query of the sequence's own rows
         if (pre ? (k0 + BKV > P) : (k0 + BKV - 1 > wave_qmin || k0 + BKV > T)) {
@@ -423,9 +437,9 @@ hipError_t launch_attention(const void* qkv, int64_t ldq, void* out, int64_t ldo
     KvPrefix pk{};
     if (pre) {
       pk = *prefix;
-      const int64_t n_pre_seqs = pk.n_seq > 0 ? pk.n_seq : st.n;
+      // one descriptor per sequence's cached prefix, also with 32-bit byte offsets
       const int64_t ld = std::max(std::max(pk.ldk, pk.ldv), pk.alt_pass >= 0 && pk.n_seq > 0 ? pk.ldv_alt : 0);
-      if (n_pre_seqs * pk.P * ld * 2 >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+      if ((int64_t)pk.P * ld * 2 >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
       if (pk.n_seq > 0 && (st.n % pk.n_seq != 0 || (pk.alt_pass >= 0 && !pk.v_alt))) return hipErrorInvalidValue;
     }
 #define RK_ATTN(D, PRE)                                                                                      \
