@@ -964,6 +964,9 @@ def main():
                     help="pair: one step = one (sequence, alpha) pair of the profile; profile: one step = the "
                          "whole profile of the workload; auto: pair for the 2x32768 workload, else profile")
     ap.add_argument("--max-group", type=int, default=12)
+    ap.add_argument("--join", type=int, default=0,
+                    help="whole-profile steps: max_rows = JOIN x the batch rows, so up to JOIN resumed passes of a "
+                         "group run layer-synchronously (0: 4 for batches of at most 16384 rows, else 1)")
     ap.add_argument("--family", default="gemm_gate_up", help="kernel family for the roofline figure")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying a HIP graph")
@@ -1069,7 +1072,10 @@ def main():
     P = min(w.lengths()) - window if window > 0 else 0
     if window > 0 and P < 1:
         raise SystemExit(f"--window {window} leaves no prefix in the shortest sequence")
-    ws = torch.empty(model.workspace_size(rows, G, rk.RK_WS_CLEAN_STATE |
+    # default: up to 4 resumed passes per launch for batches of at most 16384 rows
+    join = args.join if args.join > 0 else (4 if rows <= 16384 else 1)
+    max_rows = join * rows
+    ws = torch.empty(model.workspace_size(max_rows, G, rk.RK_WS_CLEAN_STATE |
                                           (flags & (rk.RK_FLAG_CACHED_WINDOW | rk.RK_FLAG_LOCAL_SIGNAL |
                                                     rk.RK_FLAG_UNFUSED_KL))),
                      dtype=torch.uint8, device="cuda")
@@ -1079,7 +1085,8 @@ def main():
     budgets = [int(round(rho * T_ref * len(layers))) for rho in (0.1, 0.2, 0.3)]
 
     def step():
-        model.sensitivity_profile(batch, layers, alphas, s_out, ws, rows, G, d_out=d_out, window_start=P, flags=flags)
+        model.sensitivity_profile(batch, layers, alphas, s_out, ws, max_rows, G, d_out=d_out, window_start=P,
+                                  flags=flags)
         s_host = s_out.cpu().numpy().astype(np.float64)     # synchronises
         out = []
         for a in range(len(alphas)):
@@ -1180,7 +1187,8 @@ def main():
         "config": {"workload": f"{w.name}: {cfg.n_layers}L d{cfg.d_model} {cfg.n_heads}x{cfg.head_dim} "
                                f"FFN{cfg.d_ff} V{cfg.vocab}; {describe_lengths(w.lengths())}; "
                                f"alpha {alphas}; all layers; ratios {list(w.ratios)}; budgets {budgets}{mode}",
-                   "perturbed_token_layers_per_step": tokens_layers, "profile_wall_ms": round(ms_per_step, 3)},
+                   "perturbed_token_layers_per_step": tokens_layers, "profile_wall_ms": round(ms_per_step, 3),
+                   "passes_per_launch": min(join, G, 64 // batch.n_seqs) if window == 0 and not local else 1},
         "roofline": roof,
         "mfma_util": util,
     }

@@ -268,6 +268,12 @@ rk_status rk_profile_layer(const rk_model *m, const rk_batch *batch, int32_t lay
  *   finite and >= 0.  s_out: DEVICE fp32 [n_alpha, n_A].  d_out: DEVICE fp32
  *   [n_alpha, N, n_A] or NULL.  One clean pass per batch serves every alpha.
  * max_group: passes scored per LM-head launch (1..16).
+ * Pass batching: when max_rows holds at least two copies of a batch, the
+ *   resumed passes of a group run layer-synchronously, min(max_group,
+ *   max_rows / batch rows, RK_MAX_BATCH_SEQS / batch sequences) at a time:
+ *   each joins at its perturbed layer and every launch of a block covers the
+ *   rows of all joined passes.  Results are bitwise those of one pass at a
+ *   time; the workspace grows with max_rows.
  * With RK_FLAG_CACHED_WINDOW the profile is that of the cached-window mode;
  * with RK_FLAG_LOCAL_SIGNAL, the layer-local signal of the ablation.
  * workspace must be at least rk_workspace_size(m, max_rows, max_group,

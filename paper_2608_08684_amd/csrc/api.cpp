@@ -260,6 +260,12 @@ class Timed {
 struct Noise {
   float alpha;
   const rk_perturb_params* p;
+  // joined resumed passes: the block's rows are pass slots of one->rows rows each,
+  // each laid out as the single-pass table `one`; slots first .. first + n - 1
+  // (the passes that start at this block) take the noise, slot first + k at alphas[k]
+  const SeqTable* one = nullptr;
+  int first = 0, n = 0;
+  const float* alphas = nullptr;
 };
 
 // Observation queries to keep from a block (SnapKV prefill): the q columns of
@@ -334,9 +340,19 @@ static rk_status run_block(const rk_model* m, int l, const float* h_in, float* h
   if (obs) RK_TRY(launch_snap_qobs(b.qkv, m->qkv_cols, st, obs->w, c.n_heads * c.head_dim, obs->q, s));
   if (noise) {
     char* v = (char*)b.qkv + (size_t)(c.n_heads + c.n_kv_heads) * c.head_dim * act_bytes(m);
-    Timed t("noise", s);
-    RK_TRY(launch_value_noise(v, m->bf16, m->qkv_cols, st, c.n_kv_heads, c.head_dim, l, noise->alpha,
-                              noise->p->seed, noise->p->protect_head, noise->p->protect_tail, s));
+    if (noise->one) {
+      const size_t slot = (size_t)noise->one->rows * m->qkv_cols * act_bytes(m);
+      for (int k = 0; k < noise->n; ++k) {
+        Timed t("noise", s);
+        RK_TRY(launch_value_noise(v + (size_t)(noise->first + k) * slot, m->bf16, m->qkv_cols, *noise->one,
+                                  c.n_kv_heads, c.head_dim, l, noise->alphas[k], noise->p->seed,
+                                  noise->p->protect_head, noise->p->protect_tail, s));
+      }
+    } else {
+      Timed t("noise", s);
+      RK_TRY(launch_value_noise(v, m->bf16, m->qkv_cols, st, c.n_kv_heads, c.head_dim, l, noise->alpha,
+                                noise->p->seed, noise->p->protect_head, noise->p->protect_tail, s));
+    }
   }
   if (wb) {
     rk_status e = batch_attention(m, l, b, *wb, s);
@@ -415,6 +431,72 @@ static rk_status perturbed_final(const rk_model* m, const int32_t* tokens, const
     if (e != RK_OK) return e;
   }
   RK_TRY(launch_rmsnorm(b.h, m->final_norm, xf_out, m->bf16, (int)R, (int)d, c.rms_eps, s));
+  return RK_OK;
+}
+
+// A group of resumed passes, layer-synchronously (pass batching): the passes,
+// ordered by their perturbed layer, join at that block from the cached clean
+// block input h_l, and from then on every norm, projection, attention and
+// feed-forward of a block runs once over the rows of all active passes (up to
+// max_rows rows and RK_MAX_BATCH_SEQS sequences per launch; larger groups go in
+// consecutive batches).  Every kernel is row-wise or per sequence, so each pass's
+// result is bitwise that of perturbed_final.  Pass k's final hidden state goes
+// to slot k of xp (stride pad_rows(R) rows).  The rotary table of the batch is
+// rebuilt for the joined rows and restored on return.
+static rk_status resumed_group_final(const rk_model* m, const int32_t* tokens, const SeqTable& st, const Clean& cl,
+                                     int G, const int* layers, const float* alphas, const rk_perturb_params* p,
+                                     int64_t max_rows, void* xp, const Bufs& b, hipStream_t s) {
+  const rk_model_config& c = m->cfg;
+  const int64_t d = c.d_model, R = st.rows, xstride = pad_rows(R) * d * act_bytes(m);
+  const int L = c.n_layers;
+  int B = (int)std::min<int64_t>(G, max_rows / R);
+  B = std::min(B, RK_MAX_BATCH_SEQS / st.n);
+  if (B < 2 || (p->flags & RK_FLAG_FULL_RECOMPUTE)) {
+    for (int k = 0; k < G; ++k) {
+      rk_status e = perturbed_final(m, tokens, st, cl, layers[k], alphas[k], p, (char*)xp + (size_t)k * xstride, b, s);
+      if (e != RK_OK) return e;
+    }
+    return RK_OK;
+  }
+  std::vector<int> order(G);
+  for (int k = 0; k < G; ++k) order[k] = k;
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return layers[x] < layers[y]; });
+  for (int c0 = 0; c0 < G; c0 += B) {
+    const int cb = std::min(B, G - c0);
+    int lay[RK_MAX_GROUP];
+    float al[RK_MAX_GROUP];
+    for (int q = 0; q < cb; ++q) {
+      lay[q] = layers[order[c0 + q]];
+      al[q] = alphas[order[c0 + q]];
+    }
+    // batch table: sequence i of pass slot q at rows q * R + st.off[i]
+    SeqTable bst = st;
+    bst.n = cb * st.n;
+    for (int q = 0; q < cb; ++q)
+      for (int i = 0; i < st.n; ++i) bst.off[q * st.n + i] = (int32_t)(q * R) + st.off[i];
+    bst.off[bst.n] = (int32_t)(cb * R);
+    bst.rows = (int32_t)(cb * R);
+    RK_TRY(launch_rope_table(b.rope, b.rope_pos, bst, c.head_dim, c.rope_theta, s));
+    int active = 0;
+    for (int j = lay[0]; j < L; ++j) {
+      const int first = active;
+      while (active < cb && lay[active] == j) {   // joins at its layer
+        RK_TRY(hipMemcpyAsync(b.h + (size_t)active * R * d, cl.h + (size_t)j * R * d, (size_t)R * d * 4,
+                              hipMemcpyDeviceToDevice, s));
+        ++active;
+      }
+      SeqTable at = bst;   // the active passes' rows
+      at.n = active * st.n;
+      at.rows = (int32_t)(active * R);
+      Noise nz{0.0f, p, &st, first, active - first, al + first};
+      rk_status e = run_block(m, j, b.h, b.h, b, at, active > first ? &nz : nullptr, s);
+      if (e != RK_OK) return e;
+    }
+    for (int q = 0; q < cb; ++q)
+      RK_TRY(launch_rmsnorm(b.h + (size_t)q * R * d, m->final_norm, (char*)xp + (size_t)order[c0 + q] * xstride,
+                            m->bf16, (int)R, (int)d, c.rms_eps, s));
+  }
+  RK_TRY(launch_rope_table(b.rope, b.rope_pos, st, c.head_dim, c.rope_theta, s));
   return RK_OK;
 }
 
@@ -1242,19 +1324,20 @@ static rk_status profile_run(const rk_model* m, const rk_batch* calib, const int
       pm.G = G;
       pm.seq_index0 = first;
       pm.d_seq_stride = n_A;
+      int glay[RK_MAX_GROUP];
+      float galpha[RK_MAX_GROUP];
       for (int k = 0; k < G; ++k) {
         const int idx = g0 + k, a = idx / n_A, j = idx % n_A;
-        if (local) {
-          if ((e = local_pass(m, tokens, st, cl, layers[j], alphas[a], p, b.hloc, b.kl + (size_t)k * R, b, s)) !=
-              RK_OK)
-            return e;
-        } else {
-          void* xf = (char*)b.xp + (size_t)k * pad_rows(R) * m->cfg.d_model * act_bytes(m);
-          if ((e = perturbed_final(m, tokens, st, cl, layers[j], alphas[a], p, xf, b, s)) != RK_OK) return e;
-        }
+        glay[k] = layers[j];
+        galpha[k] = alphas[a];
+        if (local &&
+            (e = local_pass(m, tokens, st, cl, layers[j], alphas[a], p, b.hloc, b.kl + (size_t)k * R, b, s)) != RK_OK)
+          return e;
         pm.d_base[k] = (int64_t)a * N * n_A + j;
         pm.s_index[k] = a * n_A + j;
       }
+      if (!local && (e = resumed_group_final(m, tokens, st, cl, G, glay, galpha, p, max_rows, b.xp, b, s)) != RK_OK)
+        return e;
       if (!local && (e = score_group(m, st, cl, b.xp, G, unfused, b.logits_p, b.kl, b, s)) != RK_OK) return e;
       RK_TRY(launch_window_mean(b.kl, R, G, st, p->window_start, b.dbatch, s));
       RK_TRY(launch_accumulate(b.dbatch, st.n, pm, d_out, b.sacc, s));

@@ -127,3 +127,43 @@ def test_largest_group_in_one_lm_launch():
         assert_kl_close([d16[1, 0, l]], [ref], f"group of 16: layer {l}")
     assert run.model.workspace_size(batch.rows, rk.RK_MAX_GROUP + 1, 0) == 0
     log(f"group of {rk.RK_MAX_GROUP}: d equal to groups of 5 and to single-layer calls; s = {s16[1].tolist()}")
+
+
+def test_joined_passes_equal_separate_passes():
+    """Resumed passes of a group run layer-synchronously when max_rows holds
+    several copies of the batch (pass batching): 16 passes (8 layers x 2 alphas)
+    over a ragged 3-sequence batch, joined 5 at a time (chunks of 5, 5, 5 and 1)
+    and 2 at a time, eagerly and as a replayed HIP graph, give d and s bitwise
+    equal to the passes run one by one (every kernel is row-wise or per
+    sequence)."""
+    import torch
+    import paper_2608_08684_amd as rk
+    from gpu_helpers import empty_bytes
+    cfg = F.small_model(n_layers=8, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=512, vocab=1024,
+                        rope_theta=1.0e4, dtype="bf16")
+    W = F.make_weights(cfg)
+    run = Runner(cfg, W)
+    lens = [150, 90, 61]
+    toks = F.make_tokens(F.make_workload("join", cfg, lens, seed_id=93))
+    batch = make_batch(toks)
+    layers = list(range(cfg.n_layers))
+    alphas = [0.05, 0.1]
+    s1, d1 = run.profile(batch, layers, alphas, max_group=16)
+    for join, group in ((5, 16), (2, 7)):
+        sj, dj = run.profile(batch, layers, alphas, max_rows=join * batch.rows, max_group=group)
+        np.testing.assert_array_equal(dj, d1)
+        np.testing.assert_array_equal(sj, s1)
+        # recorded once, then replayed on the same buffers
+        max_rows = join * batch.rows
+        ws = empty_bytes(run.model.workspace_size(max_rows, group, rk.RK_WS_CLEAN_STATE))
+        s = torch.empty(len(alphas), len(layers), dtype=torch.float32, device="cuda")
+        d = torch.empty(len(alphas), batch.n_seqs, len(layers), dtype=torch.float32, device="cuda")
+        for rep in range(2):
+            s.fill_(-1.0)
+            d.fill_(-1.0)
+            run.model.sensitivity_profile(batch, layers, alphas, s, ws, max_rows, group, d_out=d,
+                                          flags=rk.RK_FLAG_GRAPH)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(d.cpu().numpy().astype(np.float64), d1)
+            np.testing.assert_array_equal(s.cpu().numpy().astype(np.float64), s1)
+    log(f"joined passes (5 and 2 per launch, eager and graphed) bitwise equal to single passes; s = {s1[1].tolist()}")
