@@ -39,16 +39,16 @@ HBM_PEAK_GBS = 8000.0         # MI355X HBM3E
 
 # HBM bytes per launch of a kernel family, from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # counter runs of this benchmark scaled by a 1 GiB copy (see --derive-traffic and
-# profiles/).  Keyed by (family, workload); valid only while the family's kernel
-# sources hash to the recorded value, so a changed kernel reports null until
-# re-measured.
+# profiles/).  Keyed by (family, workload, resumed passes per launch); valid only
+# while the family's kernel sources hash to the recorded value, so a changed
+# kernel or launch shape reports null until re-measured.
 TRAFFIC = {
-    ("gemm_gate_up", "gpt2s-bf16"): {"bytes_per_launch": 327091576, "fetch_bytes": 226428280,
+    ("gemm_gate_up", "gpt2s-bf16", 1): {"bytes_per_launch": 327091576, "fetch_bytes": 226428280,
                                      "write_bytes": 100663296, "sources": "5138ba9bfc0b0ac1"},
-    ("gemm_gate_up", "llama3-8b-long-bf16"): {"bytes_per_launch": 12232403950, "fetch_bytes": 11292879854,
+    ("gemm_gate_up", "llama3-8b-long-bf16", 1): {"bytes_per_launch": 12223959463, "fetch_bytes": 11284435367,
                                               "write_bytes": 939524096, "sources": "5138ba9bfc0b0ac1"},
-    ("attention", "llama3-8b-long-bf16"): {"bytes_per_launch": 1675658863, "fetch_bytes": 1407164068,
-                                           "write_bytes": 268494795, "sources": "2b5f7aefbb31b8d4"},
+    ("attention", "llama3-8b-long-bf16", 1): {"bytes_per_launch": 1678355417, "fetch_bytes": 1409856642,
+                                           "write_bytes": 268498775, "sources": "e2f55bc60551caaf"},
 }
 FAMILY_SOURCES = {
     "gemm": ["paper_2608_08684_amd/csrc/gemm.hip", "paper_2608_08684_amd/csrc/mfma_tile.h"],
@@ -69,9 +69,9 @@ def sources_hash(family: str) -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_of(family: str, workload: str):
+def traffic_of(family: str, workload: str, passes_per_launch: int = 1):
     """Recorded HBM bytes per launch of a family, or None once its sources changed."""
-    rec = TRAFFIC.get((family, workload))
+    rec = TRAFFIC.get((family, workload, passes_per_launch))
     return rec["bytes_per_launch"] if rec is not None and rec["sources"] == sources_hash(family) else None
 
 
@@ -1145,7 +1145,7 @@ def main():
             (rows - eval_rows) * L + eval_rows * L + eval_rows * pass_layers
         flops = family_flops(args.family, cfg, rows_total, 1) * args.steps / max(launches, 1)
     achieved = flops / (fam_avg_ms / 1e3) / (1e9 if hbm_family else 1e12)
-    traffic = traffic_of(args.family, w.name)
+    traffic = traffic_of(args.family, w.name, min(join, G, 64 // batch.n_seqs) if window == 0 and not local else 1)
     if hbm_family:
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": args.family,
