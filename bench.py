@@ -128,6 +128,7 @@ def derive_counters(dirs):
     from collections import defaultdict
     vals = defaultdict(lambda: defaultdict(list))
     durs = defaultdict(list)
+    ids = defaultdict(lambda: defaultdict(set))   # dispatches per family and counter run
     for d in dirs:
         for f in glob.glob(os.path.join(d, "*counter_collection.csv")):
             for r in csv.DictReader(open(f)):
@@ -136,6 +137,7 @@ def derive_counters(dirs):
                     continue
                 vals[fam][r["Counter_Name"]].append(float(r["Counter_Value"]))
                 durs[fam].append((float(r["End_Timestamp"]) - float(r["Start_Timestamp"])))
+                ids[fam][d].add(r["Dispatch_Id"])
     mean = lambda x: sum(x) / len(x) if x else float("nan")
     print("| family | dispatches | avg us | MFMA busy / CU busy | waiting / wave cycles | clock GHz |")
     print("|---|---|---|---|---|---|")
@@ -143,7 +145,7 @@ def derive_counters(dirs):
         if fam not in vals:
             continue
         v = {k: mean(x) for k, x in vals[fam].items()}
-        n = max(len(x) for x in vals[fam].values())
+        n = max(len(x) for x in ids[fam].values())
         dur = mean(durs[fam])
         mf = v.get("SQ_VALU_MFMA_BUSY_CYCLES", float("nan")) / (4.0 * v.get("SQ_BUSY_CU_CYCLES", float("nan")))
         wt = v.get("SQ_WAIT_ANY", float("nan")) / v.get("SQ_WAVE_CYCLES", float("nan"))
