@@ -22,6 +22,8 @@
 
 #include "mfma_tile.h"
 
+#include <type_traits>
+
 namespace rk {
 
 // f(x) = x + expm1(-x) = x^2/2 - x^3/6 + ...  (>= 0)
@@ -239,8 +241,14 @@ __global__ __launch_bounds__(512) void lm_kl_kernel(const bf16_t* __restrict__ X
   f32x16_t a[4], b[4];
   int kt = 0, g = -1, slot = 0, pslot = ST - 1;
   constexpr int PER = (NL + NKS - 1) / NKS;   // copies issued per k-slice
-  for (int s = 0; s < nsteps; ++s) {
-    wait_steps_ahead<NL, ST - 2>(issued - 1 - s);
+  // One k-step of the stream from LDS slot `slot`; COPY: it also issues its share
+  // of the copies of the step ST - 1 ahead.  The copying steps and the last ST - 1
+  // (which copy nothing) run as two loops, so each k-slice's reads, copies and
+  // MFMAs form one basic block.
+  int s = 0;
+  auto kstep = [&](auto COPY) {
+    constexpr bool CP = decltype(COPY)::value;
+    if constexpr (CP) wait_vmem_le<(ST - 2) * NL>(); else wait_steps_ahead<NL, ST - 2>(issued - 1 - s);
     __syncthreads();   // k-step s is in LDS for every wave; the slot of s - 1 is free
     if (kt == 0) {
 #pragma unroll
@@ -248,7 +256,6 @@ __global__ __launch_bounds__(512) void lm_kl_kernel(const bf16_t* __restrict__ X
 #pragma unroll
         for (int i = 0; i < 16; ++i) b[vb][i] = 0.f;
     }
-    const bool copy = issued < nsteps;
     const v4u* Wt = smem + slot * SS;
     const v4u* Xt = Wt + WS;
     bf16x8_t wf[2][4], xf[2];
@@ -264,7 +271,7 @@ __global__ __launch_bounds__(512) void lm_kl_kernel(const bf16_t* __restrict__ X
         for (int vb = 0; vb < 4; ++vb) wf[c ^ 1][vb] = frag<CH>(Wt, vb * 32 + l32, ks + 1, lane);
         xf[c ^ 1] = frag<CH>(Xt, w * 32 + l32, ks + 1, lane);
       }
-      if (copy) {
+      if constexpr (CP) {
 #pragma unroll
         for (int j = ks * PER; j < (ks + 1) * PER; ++j)
           if (j < NL) issue_one(j, pslot);
@@ -275,13 +282,15 @@ __global__ __launch_bounds__(512) void lm_kl_kernel(const bf16_t* __restrict__ X
         b[vb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[c][vb], xf[c], b[vb], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (copy) {
+    if constexpr (CP) {
       advance();
       pslot = pslot == ST - 1 ? 0 : pslot + 1;
     }
     slot = slot == ST - 1 ? 0 : slot + 1;
-    if (++kt < nk) continue;
-    // a logit tile is complete
+  };
+  // after each k-step: a complete logit tile is kept (clean) or folded (a pass)
+  auto tile_done = [&]() {
+    if (++kt < nk) return;
     kt = 0;
     if (g < 0) {
 #pragma unroll
@@ -304,6 +313,14 @@ __global__ __launch_bounds__(512) void lm_kl_kernel(const bf16_t* __restrict__ X
         if (j == g) { T1[j] += t1; S[j] += s2; }
     }
     if (++g == G) g = -1;
+  };
+  for (; s < nsteps - (ST - 1); ++s) {
+    kstep(std::true_type{});
+    tile_done();
+  }
+  for (; s < nsteps; ++s) {
+    kstep(std::false_type{});
+    tile_done();
   }
 #pragma unroll
   for (int g2 = 0; g2 < GMAX; ++g2) {
