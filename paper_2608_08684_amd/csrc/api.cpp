@@ -451,6 +451,7 @@ static rk_status resumed_group_final(const rk_model* m, const int32_t* tokens, c
   const int L = c.n_layers;
   int B = (int)std::min<int64_t>(G, max_rows / R);
   B = std::min(B, RK_MAX_BATCH_SEQS / st.n);
+  B = (int)std::min<int64_t>(B, INT32_MAX / R);   // joined row offsets are 32-bit
   if (B < 2 || (p->flags & RK_FLAG_FULL_RECOMPUTE)) {
     for (int k = 0; k < G; ++k) {
       rk_status e = perturbed_final(m, tokens, st, cl, layers[k], alphas[k], p, (char*)xp + (size_t)k * xstride, b, s);
@@ -816,6 +817,7 @@ static rk_status window_group_final(const rk_model* m, const SeqTable& pst, cons
   const int L = c.n_layers, P = pst.max_len;
   int B = (int)std::min<int64_t>(G, max_rows / Rw);
   B = std::min(B, RK_MAX_BATCH_SEQS / wst.n);
+  B = (int)std::min<int64_t>(B, INT32_MAX / Rw);   // joined row offsets are 32-bit
   if (B < 2) {
     for (int k = 0; k < G; ++k) {
       void* xk = (char*)xp + (size_t)k * xstride;
