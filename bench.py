@@ -45,8 +45,8 @@ HBM_PEAK_GBS = 8000.0         # MI355X HBM3E
 TRAFFIC = {
     ("gemm_gate_up", "gpt2s-bf16", 1): {"bytes_per_launch": 327091576, "fetch_bytes": 226428280,
                                      "write_bytes": 100663296, "sources": "5138ba9bfc0b0ac1"},
-    ("gemm_gate_up", "llama3-8b-long-bf16", 1): {"bytes_per_launch": 12226440076, "fetch_bytes": 11286915980,
-                                                 "write_bytes": 939524096, "sources": "125b9c04178a212e"},
+    ("gemm_gate_up", "llama3-8b-long-bf16", 1): {"bytes_per_launch": 12252797172, "fetch_bytes": 11313273076,
+                                                 "write_bytes": 939524096, "sources": "3637cd35c57e36e6"},
     ("attention", "llama3-8b-long-bf16", 1): {"bytes_per_launch": 1677633940, "fetch_bytes": 1409141478,
                                               "write_bytes": 268492462, "sources": "e2f55bc60551caaf"},
 }
