@@ -169,11 +169,13 @@ def test_joined_passes_equal_separate_passes():
     log(f"joined passes (5 and 2 per launch, eager and graphed) bitwise equal to single passes; s = {s1[1].tolist()}")
 
 
-@pytest.mark.parametrize("cfg,flags", [(BF16, "unfused"), (F32, "fp32")], ids=["bf16-unfused", "f32"])
+@pytest.mark.parametrize("cfg,flags", [(BF16, "unfused"), (F32, "fp32"), (BF16, "window")],
+                         ids=["bf16-unfused", "f32", "bf16-window-start"])
 def test_joined_passes_other_paths(cfg, flags):
-    """Pass batching on the unfused-KL path (materialised logits) and on the fp32
-    model (VALU GEMMs and attention): 3 sequences, every layer at two alphas,
-    three passes per launch, bitwise equal to one pass at a time."""
+    """Pass batching on the unfused-KL path (materialised logits), on the fp32
+    model (VALU GEMMs and attention) and with a window start (means over
+    [40, T_i), protected first position): 3 sequences, every layer at two
+    alphas, three passes per launch, bitwise equal to one pass at a time."""
     import paper_2608_08684_amd as rk
     W = F.make_weights(cfg)
     run = Runner(cfg, W)
@@ -183,8 +185,9 @@ def test_joined_passes_other_paths(cfg, flags):
     layers = list(range(cfg.n_layers))
     alphas = [0.05, 0.1]
     fl = rk.RK_FLAG_UNFUSED_KL if flags == "unfused" else 0
-    s1, d1 = run.profile(batch, layers, alphas, max_group=6, flags=fl)
-    sj, dj = run.profile(batch, layers, alphas, max_rows=3 * batch.rows, max_group=6, flags=fl)
+    kw = dict(window_start=40, protect_head=1) if flags == "window" else {}
+    s1, d1 = run.profile(batch, layers, alphas, max_group=6, flags=fl, **kw)
+    sj, dj = run.profile(batch, layers, alphas, max_rows=3 * batch.rows, max_group=6, flags=fl, **kw)
     np.testing.assert_array_equal(dj, d1)
     np.testing.assert_array_equal(sj, s1)
     log(f"joined passes, {flags}: bitwise equal to single passes; s = {s1[1].tolist()}")
