@@ -59,6 +59,12 @@ def test_gpt2s_whole_profile_properties(gpt2s):
     # repeatable bit for bit, and alpha = 0 is exactly zero at full size
     s2, d2 = run.profile(batch, layers, list(w.alphas), max_group=12)
     assert np.array_equal(s2, s) and np.array_equal(d2, d)
+    # the benchmark's launch configuration (four resumed passes per block launch,
+    # graph replay) gives the same profile bit for bit
+    for rep in range(2):
+        s4, d4 = run.profile(batch, layers, list(w.alphas), max_rows=4 * batch.rows, max_group=12,
+                             flags=rk.RK_FLAG_GRAPH)
+        assert np.array_equal(s4, s) and np.array_equal(d4, d)
     s0, d0 = run.profile(batch, layers, [0.0], max_group=12)
     assert np.all(s0 == 0.0) and np.all(d0 == 0.0)
     # budgets from the GPU profile: C mapping == oracle mapping, sums preserved
